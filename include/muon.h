@@ -1,0 +1,190 @@
+/*
+ * muon.h -- C ABI of the MI355X (gfx950) single-GPU Muon optimizer step.
+ *
+ * The library applies one Muon step (DMuon, arXiv 2606.27153, Sec. 2.1) to a
+ * fixed list of weight matrices that one GPU owns.  For every matrix it runs
+ *
+ *   1. momentum:  M <- mu*M + G;  NS input u = G + mu*M (Nesterov) or u = M
+ *   2. orientation: X = u^T when rows > cols, so that X is m x n, m <= n
+ *   3. Frobenius normalisation: X0 = X / (||X||_F + eps)
+ *   4. k steps of the quintic Newton-Schulz iteration of Eq. 2,
+ *        A = X X^T,  B = b*A + c*A*A,  X <- a*X + B*X
+ *      with the Gram product computed on lower-triangular tiles only and
+ *      mirrored (the symmetric kernel of Sec. 3.3), the polynomial fused into
+ *      the epilogue of the A*A product and a*X fused into the epilogue of B*X
+ *   5. O = X^T (tall) or X (wide) -- the orthogonalised update NS_k(M_t)
+ *   6. Eq. 1 with decoupled weight decay and the shape scale:
+ *        W <- W*(1 - lr*wd) - lr*sqrt(max(1, rows/cols))*O
+ *
+ * Matrices are independent (Sec. 3.3); the plan groups them by shape into
+ * buckets and advances whole groups through each NS step with grouped
+ * launches, so many small matrices do not each pay a launch.
+ *
+ * Conventions for every entry point:
+ *  - Every function returns a muon_status; nothing aborts, throws or exits.
+ *    On failure muon_last_error() returns a thread-local message.
+ *  - Device buffers are row-major (leading dimension = cols), contiguous and
+ *    16-byte aligned.  The caller owns every device buffer and the stream.
+ *  - muon_step enqueues work on the caller's HIP stream and returns; results
+ *    are visible after the stream is synchronised.  Arguments are checked
+ *    before anything is enqueued; on an error nothing is launched.
+ *  - NaN or Inf in the inputs propagate; they are not sanitised.
+ */
+#ifndef MUON_MI355X_H
+#define MUON_MI355X_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MUON_ABI_VERSION 1
+
+#if defined(__GNUC__)
+#define MUON_API __attribute__((visibility("default")))
+#else
+#define MUON_API
+#endif
+
+typedef enum muon_status {
+  MUON_OK = 0,
+  MUON_ERR_INVALID_ARG = 1,          /* a null pointer, bad shape or out-of-range value */
+  MUON_ERR_UNSUPPORTED = 2,          /* a dtype combination or option the library lacks */
+  MUON_ERR_OUT_OF_MEMORY = 3,        /* host or device allocation failed (plan create) */
+  MUON_ERR_WORKSPACE_TOO_SMALL = 4,  /* workspace_bytes below muon_plan_workspace_bytes */
+  MUON_ERR_DEVICE = 5                /* a HIP call failed; the HIP error text is kept */
+} muon_status;
+
+typedef enum muon_dtype { MUON_F32 = 0, MUON_BF16 = 1 } muon_dtype;
+
+/* Arithmetic of the Newton-Schulz GEMMs.  MUON_NS_BF16: bf16 operands in
+ * HBM, fp32 accumulation on the matrix cores (matrices with
+ * min(rows, cols) <= small_m_threshold still use fp32).  MUON_NS_FP32: fp32
+ * operands and fp32 matrix-core arithmetic for every matrix (validation). */
+typedef enum muon_ns_precision { MUON_NS_BF16 = 0, MUON_NS_FP32 = 1 } muon_ns_precision;
+
+/* Plan flags. */
+#define MUON_PLAN_HOST_ONLY 0x1u     /* build host metadata only: no device memory is
+                                        touched; such a plan can be inspected but not stepped */
+
+/* One weight matrix: stored shape and dtypes.  param in {F32, BF16},
+ * grad in {F32, BF16}, momentum must be F32. */
+typedef struct muon_matrix_desc {
+  int64_t rows;
+  int64_t cols;
+  int32_t param_dtype;
+  int32_t grad_dtype;
+  int32_t momentum_dtype;
+  int32_t reserved;                  /* must be 0 */
+} muon_matrix_desc;
+
+typedef struct muon_plan_opts {
+  int32_t precision;                 /* muon_ns_precision */
+  int32_t max_ns_steps;              /* largest ns_steps muon_step accepts, 1..64 */
+  float a, b, c;                     /* NS coefficients of Eq. 2, used for every step */
+  float eps;                         /* added to ||X||_F before dividing */
+  int32_t small_m_threshold;         /* bf16 plans: min(rows,cols) <= this -> fp32 NS */
+  uint32_t flags;                    /* MUON_PLAN_* */
+  int64_t wave_bytes;                /* cap on the NS working set of one group ("wave")
+                                        of matrices processed together; 0 = default */
+} muon_plan_opts;
+
+typedef struct muon_plan_s* muon_plan;
+
+/* Summary of a plan (for callers and tests). */
+typedef struct muon_plan_info {
+  int32_t n_matrices;
+  int32_t n_waves;                   /* groups of matrices stepped together */
+  int32_t n_buckets;                 /* distinct (m, n, padded shape, kernel class) */
+  int32_t device;                    /* HIP device the plan lives on, -1 if host-only */
+  int64_t workspace_bytes;           /* bytes muon_step needs */
+  int64_t launches_per_step;         /* kernel launches of one muon_step at max_ns_steps */
+  double ns_flops_per_ns_step;       /* algorithmic flops of one NS step over all matrices:
+                                        sum of 3 m^2 n + m^3 (symmetry-aware) */
+  double padded_flops_per_ns_step;   /* flops the kernels issue on padded tiles */
+} muon_plan_info;
+
+/* Placement of one matrix in the plan. */
+typedef struct muon_matrix_info {
+  int64_t m, n;                      /* oriented: m = min(rows, cols), n = max */
+  int64_t m_pad, n_pad;              /* padded to the kernel tile */
+  int32_t transposed;                /* 1 if rows > cols */
+  int32_t kernel_class;              /* index of the GEMM configuration */
+  int32_t tile;                      /* square output tile of that configuration */
+  int32_t fp32_ns;                   /* 1 if the NS GEMMs run in fp32 */
+  int32_t wave;                      /* group the matrix is stepped in */
+  int32_t bucket;
+} muon_matrix_info;
+
+/* Fills *o with the defaults: precision BF16, max_ns_steps 16,
+ * (a,b,c) = (3.4445, -4.7750, 2.0315), eps 1e-7, small_m_threshold 64,
+ * flags 0, wave_bytes 0.  Returns INVALID_ARG if o is NULL. */
+MUON_API muon_status muon_plan_opts_default(muon_plan_opts* o);
+
+/* Builds a plan for n matrices (orientation, buckets, kernel classes, tile
+ * tables, workspace layout).  Unless MUON_PLAN_HOST_ONLY is set, the plan is
+ * bound to the current HIP device and uploads its tables there (the only
+ * host-to-device copy outside muon_step).  opts may be NULL (defaults).
+ * Errors: INVALID_ARG (null, n < 1, rows or cols < 1 or >= 2^31, reserved != 0,
+ * opts out of range), UNSUPPORTED (dtypes), OUT_OF_MEMORY, DEVICE. */
+MUON_API muon_status muon_plan_create(const muon_matrix_desc* mats, int32_t n,
+                             const muon_plan_opts* opts, muon_plan* out);
+
+/* Releases the plan and its device tables.  NULL is accepted.  The caller
+ * must make sure no enqueued step still uses the plan. */
+MUON_API muon_status muon_plan_destroy(muon_plan plan);
+
+/* Workspace size in bytes that muon_step needs. */
+MUON_API muon_status muon_plan_workspace_bytes(muon_plan plan, size_t* bytes);
+
+MUON_API muon_status muon_plan_get_info(muon_plan plan, muon_plan_info* info);
+MUON_API muon_status muon_plan_matrix_info(muon_plan plan, int32_t index, muon_matrix_info* info);
+
+/* One Muon step over every matrix of the plan (Eq. 1, Eq. 2).
+ *
+ * params[i]   device, rows x cols of param_dtype, updated in place
+ * grads[i]    device, rows x cols of grad_dtype, read only
+ * momentum[i] device, rows x cols fp32, updated in place
+ *   (arrays of n device pointers on the host, in descriptor order; buffers of
+ *   different matrices must not overlap)
+ * lr, weight_decay: finite, >= 0;  momentum_coef in [0, 1)
+ * ns_steps in [0, max_ns_steps];  nesterov: 0 or 1
+ * workspace: device buffer of at least muon_plan_workspace_bytes bytes, owned
+ *   by the caller, contents need not be initialised; steps that may run
+ *   concurrently need distinct workspaces and distinct plans.
+ * hip_stream: hipStream_t (NULL = default stream).
+ *
+ * The plan caches the device copy of the pointer arrays: when they differ
+ * from the previous call, the new table is copied on the stream and the
+ * stream is synchronised once before the step is enqueued.  Otherwise the
+ * call only enqueues kernels and never synchronises or allocates.
+ * The plan must be used from the device it was created on. */
+MUON_API muon_status muon_step(muon_plan plan, void* const* params, const void* const* grads,
+                      void* const* momentum, float lr, float momentum_coef,
+                      float weight_decay, int32_t ns_steps, int32_t nesterov,
+                      void* workspace, size_t workspace_bytes, void* hip_stream);
+
+/* muon_step plus, for every i with update_out[i] != NULL, the orthogonalised
+ * update O_i (before lr and the shape scale) written as fp32 rows x cols
+ * row-major to update_out[i] (device, 16-byte aligned).  W and M are
+ * bitwise identical to muon_step's.  update_out may be NULL (no output). */
+MUON_API muon_status muon_step_debug(muon_plan plan, void* const* params, const void* const* grads,
+                            void* const* momentum, float lr, float momentum_coef,
+                            float weight_decay, int32_t ns_steps, int32_t nesterov,
+                            void* workspace, size_t workspace_bytes, void* hip_stream,
+                            float* const* update_out);
+
+MUON_API const char* muon_status_string(muon_status s);
+
+/* Thread-local description of the last failure on this thread ("" if none). */
+MUON_API const char* muon_last_error(void);
+
+MUON_API int32_t muon_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MUON_MI355X_H */

@@ -1,0 +1,318 @@
+// C ABI of the Muon step library: argument checking, plan lifetime, device
+// tables, and the per-step launch sequence.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "muon_internal.h"
+
+struct muon_plan_s {
+  muon::Plan p;
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+muon_status fail(muon_status s, const std::string& msg) {
+  g_last_error = msg;
+  return s;
+}
+
+muon_status ok() {
+  g_last_error.clear();
+  return MUON_OK;
+}
+
+muon_status hip_fail(hipError_t e, const char* what) {
+  return fail(MUON_ERR_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+bool valid_dtype(int32_t d) { return d == MUON_F32 || d == MUON_BF16; }
+
+muon_status check_opts(const muon_plan_opts& o) {
+  if (o.precision != MUON_NS_BF16 && o.precision != MUON_NS_FP32)
+    return fail(MUON_ERR_INVALID_ARG, "opts.precision must be MUON_NS_BF16 or MUON_NS_FP32");
+  if (o.max_ns_steps < 1 || o.max_ns_steps > 64)
+    return fail(MUON_ERR_INVALID_ARG, "opts.max_ns_steps must be in [1, 64]");
+  if (!std::isfinite(o.a) || !std::isfinite(o.b) || !std::isfinite(o.c))
+    return fail(MUON_ERR_INVALID_ARG, "opts.a, opts.b, opts.c must be finite");
+  if (!std::isfinite(o.eps) || o.eps < 0.f) return fail(MUON_ERR_INVALID_ARG, "opts.eps must be finite and >= 0");
+  if (o.small_m_threshold < 0) return fail(MUON_ERR_INVALID_ARG, "opts.small_m_threshold must be >= 0");
+  if (o.flags & ~uint32_t(MUON_PLAN_HOST_ONLY)) return fail(MUON_ERR_INVALID_ARG, "opts.flags has unknown bits");
+  if (o.wave_bytes < 0) return fail(MUON_ERR_INVALID_ARG, "opts.wave_bytes must be >= 0");
+  return MUON_OK;
+}
+
+muon_status upload_tables(muon::Plan& p) {
+  using namespace muon;
+  auto al = [](size_t v) { return (v + 255) / 256 * 256; };
+  const size_t b_mats = al(p.h_matdev.size() * sizeof(MatDev));
+  const size_t b_pref = al(p.h_prefix.size() * sizeof(int32_t));
+  const size_t b_tiles = al(p.h_tiles.size() * sizeof(TileEntry));
+  const size_t b_ptrs = al(p.mats.size() * sizeof(PtrEntry));
+  const size_t total = b_mats + b_pref + b_tiles + b_ptrs;
+  hipError_t e = hipMalloc(&p.d_block, total);
+  if (e != hipSuccess) {
+    p.d_block = nullptr;
+    return e == hipErrorOutOfMemory ? fail(MUON_ERR_OUT_OF_MEMORY, "hipMalloc of plan tables failed")
+                                    : hip_fail(e, "hipMalloc of plan tables");
+  }
+  char* base = static_cast<char*>(p.d_block);
+  p.d_mats = reinterpret_cast<MatDev*>(base);
+  p.d_prefix = reinterpret_cast<int32_t*>(base + b_mats);
+  p.d_tiles = reinterpret_cast<TileEntry*>(base + b_mats + b_pref);
+  p.d_ptrs = reinterpret_cast<PtrEntry*>(base + b_mats + b_pref + b_tiles);
+  e = hipMemcpy(p.d_mats, p.h_matdev.data(), p.h_matdev.size() * sizeof(MatDev), hipMemcpyHostToDevice);
+  if (e == hipSuccess)
+    e = hipMemcpy(p.d_prefix, p.h_prefix.data(), p.h_prefix.size() * sizeof(int32_t), hipMemcpyHostToDevice);
+  if (e == hipSuccess && !p.h_tiles.empty())
+    e = hipMemcpy(p.d_tiles, p.h_tiles.data(), p.h_tiles.size() * sizeof(TileEntry), hipMemcpyHostToDevice);
+  if (e != hipSuccess) return hip_fail(e, "upload of plan tables");
+  return MUON_OK;
+}
+
+bool aligned(const void* ptr, uintptr_t a) { return (reinterpret_cast<uintptr_t>(ptr) & (a - 1)) == 0; }
+
+muon_status step_impl(muon_plan plan, void* const* params, const void* const* grads, void* const* momentum,
+                      float lr, float mu, float wd, int32_t ns_steps, int32_t nesterov, void* workspace,
+                      size_t workspace_bytes, void* stream, float* const* update_out) {
+  using namespace muon;
+  if (!plan) return fail(MUON_ERR_INVALID_ARG, "plan is NULL");
+  Plan& p = plan->p;
+  if (!p.d_block) return fail(MUON_ERR_INVALID_ARG, "plan was created host-only and cannot be stepped");
+  if (!params || !grads || !momentum) return fail(MUON_ERR_INVALID_ARG, "params, grads and momentum must be non-NULL");
+  if (!std::isfinite(lr) || lr < 0.f) return fail(MUON_ERR_INVALID_ARG, "lr must be finite and >= 0");
+  if (!std::isfinite(wd) || wd < 0.f) return fail(MUON_ERR_INVALID_ARG, "weight_decay must be finite and >= 0");
+  if (!(mu >= 0.f && mu < 1.f)) return fail(MUON_ERR_INVALID_ARG, "momentum_coef must be in [0, 1)");
+  if (ns_steps < 0 || ns_steps > p.opts.max_ns_steps)
+    return fail(MUON_ERR_INVALID_ARG, "ns_steps must be in [0, max_ns_steps]");
+  if (nesterov != 0 && nesterov != 1) return fail(MUON_ERR_INVALID_ARG, "nesterov must be 0 or 1");
+  if (!workspace) return fail(MUON_ERR_INVALID_ARG, "workspace is NULL");
+  if (!aligned(workspace, 256)) return fail(MUON_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  if (workspace_bytes < size_t(p.ws_bytes))
+    return fail(MUON_ERR_WORKSPACE_TOO_SMALL,
+                "workspace has " + std::to_string(workspace_bytes) + " bytes, plan needs " + std::to_string(p.ws_bytes));
+  const size_t n = p.mats.size();
+  for (size_t i = 0; i < n; ++i) {
+    if (!params[i] || !grads[i] || !momentum[i])
+      return fail(MUON_ERR_INVALID_ARG, "NULL buffer pointer for matrix " + std::to_string(i));
+    if (!aligned(params[i], 16) || !aligned(grads[i], 16) || !aligned(momentum[i], 16) ||
+        (update_out && update_out[i] && !aligned(update_out[i], 16)))
+      return fail(MUON_ERR_INVALID_ARG, "buffers of matrix " + std::to_string(i) + " must be 16-byte aligned");
+  }
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev != p.device)
+    return fail(MUON_ERR_INVALID_ARG, "current device " + std::to_string(dev) + " is not the plan's device " +
+                                          std::to_string(p.device));
+
+  // Refresh the device pointer table if the caller's buffers moved.
+  bool changed = !p.ptrs_valid;
+  for (size_t i = 0; i < n && !changed; ++i) {
+    const PtrEntry& h = p.h_ptrs[i];
+    float* out = update_out ? update_out[i] : nullptr;
+    changed = h.param != params[i] || h.grad != grads[i] || h.mom != momentum[i] || h.out != out;
+  }
+  if (changed) {
+    for (size_t i = 0; i < n; ++i) {
+      p.h_ptrs[i].param = params[i];
+      p.h_ptrs[i].grad = grads[i];
+      p.h_ptrs[i].mom = static_cast<float*>(momentum[i]);
+      p.h_ptrs[i].out = update_out ? update_out[i] : nullptr;
+    }
+    p.ptrs_valid = false;
+    e = hipMemcpyAsync(p.d_ptrs, p.h_ptrs.data(), n * sizeof(PtrEntry), hipMemcpyHostToDevice,
+                       hipStream_t(stream));
+    if (e == hipSuccess) e = hipStreamSynchronize(hipStream_t(stream));
+    if (e != hipSuccess) return hip_fail(e, "upload of buffer pointers");
+    p.ptrs_valid = true;
+  }
+
+  StepScalars s{};
+  s.lr = lr;
+  s.mu = mu;
+  s.wd = wd;
+  s.decay = float(1.0 - double(lr) * double(wd));
+  s.a = p.opts.a;
+  s.b = p.opts.b;
+  s.c = p.opts.c;
+  s.eps = p.opts.eps;
+  s.nesterov = nesterov;
+  s.ns_steps = ns_steps;
+  char* ws = static_cast<char*>(workspace);
+  for (const WaveHost& w : p.waves) {
+    if (launch_momentum(p, w, ws, s, stream)) return hip_fail(hipGetLastError(), "momentum kernel launch");
+    if (launch_finalize(p, w, ws, s, stream)) return hip_fail(hipGetLastError(), "finalize kernel launch");
+    for (int32_t it = 0; it < ns_steps; ++it) {
+      const int32_t last = it == ns_steps - 1;
+      for (int32_t stage = ST_GRAM; stage <= ST_BX; ++stage)
+        for (const ClassLaunch& cl : w.launches)
+          if (launch_ns_gemm(p, w, cl, stage, it, last, ws, s, stream))
+            return hip_fail(hipGetLastError(), "NS GEMM launch");
+    }
+    if (launch_apply(p, w, ws, s, stream)) return hip_fail(hipGetLastError(), "apply kernel launch");
+  }
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t muon_abi_version(void) { return MUON_ABI_VERSION; }
+
+const char* muon_status_string(muon_status s) {
+  switch (s) {
+    case MUON_OK: return "MUON_OK";
+    case MUON_ERR_INVALID_ARG: return "MUON_ERR_INVALID_ARG";
+    case MUON_ERR_UNSUPPORTED: return "MUON_ERR_UNSUPPORTED";
+    case MUON_ERR_OUT_OF_MEMORY: return "MUON_ERR_OUT_OF_MEMORY";
+    case MUON_ERR_WORKSPACE_TOO_SMALL: return "MUON_ERR_WORKSPACE_TOO_SMALL";
+    case MUON_ERR_DEVICE: return "MUON_ERR_DEVICE";
+  }
+  return "MUON_ERR_UNKNOWN";
+}
+
+const char* muon_last_error(void) { return g_last_error.c_str(); }
+
+muon_status muon_plan_opts_default(muon_plan_opts* o) {
+  if (!o) return fail(MUON_ERR_INVALID_ARG, "opts is NULL");
+  std::memset(o, 0, sizeof(*o));
+  o->precision = MUON_NS_BF16;
+  o->max_ns_steps = 16;
+  o->a = 3.4445f;
+  o->b = -4.7750f;
+  o->c = 2.0315f;
+  o->eps = 1e-7f;
+  o->small_m_threshold = 64;
+  o->flags = 0;
+  o->wave_bytes = 0;
+  return ok();
+}
+
+muon_status muon_plan_create(const muon_matrix_desc* mats, int32_t n, const muon_plan_opts* opts, muon_plan* out) {
+  if (!out) return fail(MUON_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (!mats) return fail(MUON_ERR_INVALID_ARG, "mats is NULL");
+  if (n < 1) return fail(MUON_ERR_INVALID_ARG, "n must be >= 1");
+  muon_plan_opts o;
+  if (opts) {
+    o = *opts;
+  } else {
+    muon_plan_opts_default(&o);
+  }
+  if (muon_status st = check_opts(o)) return st;
+  for (int32_t i = 0; i < n; ++i) {
+    const muon_matrix_desc& d = mats[i];
+    const std::string who = "matrix " + std::to_string(i);
+    if (d.rows < 1 || d.cols < 1 || d.rows >= (int64_t(1) << 31) || d.cols >= (int64_t(1) << 31))
+      return fail(MUON_ERR_INVALID_ARG, who + ": rows and cols must be in [1, 2^31)");
+    if (d.reserved != 0) return fail(MUON_ERR_INVALID_ARG, who + ": reserved must be 0");
+    if (!valid_dtype(d.param_dtype) || !valid_dtype(d.grad_dtype))
+      return fail(MUON_ERR_UNSUPPORTED, who + ": param and grad dtypes must be MUON_F32 or MUON_BF16");
+    if (d.momentum_dtype != MUON_F32) return fail(MUON_ERR_UNSUPPORTED, who + ": momentum must be MUON_F32");
+  }
+  muon_plan_s* plan = new (std::nothrow) muon_plan_s();
+  if (!plan) return fail(MUON_ERR_OUT_OF_MEMORY, "host allocation of the plan failed");
+  std::string err;
+  muon_status st;
+  try {
+    st = muon::build_plan(mats, n, o, plan->p, err);
+  } catch (const std::bad_alloc&) {
+    st = MUON_ERR_OUT_OF_MEMORY;
+    err = "host allocation failed while building the plan";
+  }
+  if (st != MUON_OK) {
+    delete plan;
+    return fail(st, err);
+  }
+  if (!(o.flags & MUON_PLAN_HOST_ONLY)) {
+    hipError_t e = hipGetDevice(&plan->p.device);
+    if (e != hipSuccess) {
+      delete plan;
+      return hip_fail(e, "hipGetDevice");
+    }
+    st = upload_tables(plan->p);
+    if (st != MUON_OK) {
+      const std::string msg = g_last_error;
+      if (plan->p.d_block) (void)hipFree(plan->p.d_block);
+      delete plan;
+      return fail(st, msg);
+    }
+  }
+  *out = plan;
+  return ok();
+}
+
+muon_status muon_plan_destroy(muon_plan plan) {
+  if (!plan) return ok();
+  muon_status st = MUON_OK;
+  if (plan->p.d_block) {
+    hipError_t e = hipFree(plan->p.d_block);
+    if (e != hipSuccess) st = hip_fail(e, "hipFree of plan tables");
+  }
+  delete plan;
+  return st == MUON_OK ? ok() : st;
+}
+
+muon_status muon_plan_workspace_bytes(muon_plan plan, size_t* bytes) {
+  if (!plan || !bytes) return fail(MUON_ERR_INVALID_ARG, "plan and bytes must be non-NULL");
+  *bytes = size_t(plan->p.ws_bytes);
+  return ok();
+}
+
+muon_status muon_plan_get_info(muon_plan plan, muon_plan_info* info) {
+  if (!plan || !info) return fail(MUON_ERR_INVALID_ARG, "plan and info must be non-NULL");
+  const muon::Plan& p = plan->p;
+  std::memset(info, 0, sizeof(*info));
+  info->n_matrices = int32_t(p.mats.size());
+  info->n_waves = int32_t(p.waves.size());
+  info->n_buckets = p.n_buckets;
+  info->device = p.d_block ? p.device : -1;
+  info->workspace_bytes = p.ws_bytes;
+  info->launches_per_step = muon::launches_per_step(p, p.opts.max_ns_steps);
+  info->ns_flops_per_ns_step = p.ns_flops;
+  info->padded_flops_per_ns_step = p.padded_flops;
+  return ok();
+}
+
+muon_status muon_plan_matrix_info(muon_plan plan, int32_t index, muon_matrix_info* info) {
+  if (!plan || !info) return fail(MUON_ERR_INVALID_ARG, "plan and info must be non-NULL");
+  const muon::Plan& p = plan->p;
+  if (index < 0 || size_t(index) >= p.mats.size()) return fail(MUON_ERR_INVALID_ARG, "index out of range");
+  const muon::MatHost& h = p.mats[size_t(index)];
+  std::memset(info, 0, sizeof(*info));
+  info->m = h.m;
+  info->n = h.n;
+  info->m_pad = h.m_pad;
+  info->n_pad = h.n_pad;
+  info->transposed = h.transposed;
+  info->kernel_class = h.kclass;
+  info->tile = muon::class_info(h.kclass).tile;
+  info->fp32_ns = h.fp32_ns;
+  info->wave = h.wave;
+  info->bucket = h.bucket;
+  return ok();
+}
+
+muon_status muon_step(muon_plan plan, void* const* params, const void* const* grads, void* const* momentum,
+                      float lr, float momentum_coef, float weight_decay, int32_t ns_steps, int32_t nesterov,
+                      void* workspace, size_t workspace_bytes, void* hip_stream) {
+  return step_impl(plan, params, grads, momentum, lr, momentum_coef, weight_decay, ns_steps, nesterov, workspace,
+                   workspace_bytes, hip_stream, nullptr);
+}
+
+muon_status muon_step_debug(muon_plan plan, void* const* params, const void* const* grads, void* const* momentum,
+                            float lr, float momentum_coef, float weight_decay, int32_t ns_steps, int32_t nesterov,
+                            void* workspace, size_t workspace_bytes, void* hip_stream, float* const* update_out) {
+  return step_impl(plan, params, grads, momentum, lr, momentum_coef, weight_decay, ns_steps, nesterov, workspace,
+                   workspace_bytes, hip_stream, update_out);
+}
+
+}  // extern "C"

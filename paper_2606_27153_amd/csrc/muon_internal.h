@@ -1,0 +1,151 @@
+// Internal data structures of the Muon step library: the plan built on the
+// host and the descriptors the kernels read from device memory.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/muon.h"
+
+namespace muon {
+
+// ---------------------------------------------------------------------------
+// Kernel classes: one GEMM configuration each.  Every class computes square
+// output tiles of TILE x TILE with 256 threads (2 x 2 waves) and a 128-byte
+// K slab per stage (64 bf16 or 32 fp32 values).
+// ---------------------------------------------------------------------------
+enum KernelClass : int32_t {
+  KC_BF16_256 = 0,
+  KC_BF16_128 = 1,
+  KC_BF16_64 = 2,
+  KC_F32_128 = 3,
+  KC_F32_64 = 4,
+  KC_COUNT = 5
+};
+
+struct ClassInfo {
+  int32_t tile;
+  int32_t fp32;     // operands stored as fp32 (else bf16)
+  const char* name;
+};
+
+const ClassInfo& class_info(int32_t kc);
+
+// Elementwise kernels work on 64 x 64 tiles of the stored (rows x cols)
+// layout, padded to the GEMM tile; every padded extent is a multiple of 64.
+constexpr int32_t EW_TILE = 64;
+
+// Device descriptor of one matrix inside a wave.  All *_off fields are byte
+// offsets into the caller's workspace.
+struct MatDev {
+  int64_t x_off[2];    // oriented X, m_pad x n_pad (ping-pong pair p)
+  int64_t xt_off[2];   // X^T, n_pad x m_pad
+  int64_t a_off;       // Gram A, m_pad x m_pad
+  int64_t b_off;       // polynomial B, m_pad x m_pad
+  int64_t o_off;       // fp32 O in stored layout, rows_pad x cols_pad
+  int64_t partial_off; // fp32 partial sums of squares, one per EW tile
+  int32_t rows, cols;          // stored shape
+  int32_t rows_pad, cols_pad;  // stored shape padded to the tile
+  int32_t m_pad, n_pad;        // oriented padded shape
+  int32_t transposed;          // rows > cols
+  int32_t x_f32;               // X/A/B are fp32 (else bf16)
+  int32_t param_dtype, grad_dtype;
+  int32_t slot;                // position in its wave (scale / flag index)
+  int32_t index;               // descriptor index (pointer table index)
+  int32_t ew_tiles_c;          // cols_pad / 64
+  int32_t pad0;
+};
+
+// One output tile of a grouped GEMM launch.
+struct TileEntry {
+  int32_t mat;   // index into the MatDev array (global, wave order)
+  uint16_t ti, tj;
+};
+
+// Per-matrix device pointers, refreshed when the caller's buffers change.
+struct PtrEntry {
+  void* param;
+  const void* grad;
+  float* mom;
+  float* out;    // debug output of O, may be null
+};
+
+struct MatHost {
+  int64_t rows, cols, m, n;
+  int64_t m_pad, n_pad, rows_pad, cols_pad;
+  int32_t transposed, kclass, fp32_ns;
+  int32_t param_dtype, grad_dtype, momentum_dtype;
+  int32_t wave, slot, bucket;
+  int64_t ew_tiles;
+  int64_t x_off[2], xt_off[2], a_off, b_off, o_off, partial_off;
+  int64_t ws_bytes;    // workspace bytes of this matrix within its wave
+};
+
+struct ClassLaunch {
+  int32_t kclass;
+  int64_t lower_off;   // TileEntry offset of the lower-triangular list
+  int32_t n_lower;
+  int64_t full_off;    // TileEntry offset of the full list
+  int32_t n_full;
+};
+
+struct WaveHost {
+  int32_t first;       // first position in wave order
+  int32_t count;
+  int64_t ew_tiles;
+  int64_t prefix_off;  // int32 offset of the EW tile prefix (count + 1 entries)
+  int64_t scale_off;   // workspace byte offset: float scale[count]
+  int64_t flag_off;    // workspace byte offset: int32 flag[count]
+  int64_t ws_bytes;
+  std::vector<ClassLaunch> launches;
+};
+
+struct Plan {
+  muon_plan_opts opts;
+  std::vector<MatHost> mats;        // descriptor order
+  std::vector<int32_t> order;       // wave order -> descriptor index
+  std::vector<WaveHost> waves;
+  std::vector<MatDev> h_matdev;     // wave order
+  std::vector<int32_t> h_prefix;
+  std::vector<TileEntry> h_tiles;
+  int32_t n_buckets = 0;
+  int64_t ws_bytes = 0;
+  double ns_flops = 0, padded_flops = 0;
+
+  // device side
+  int32_t device = -1;
+  void* d_block = nullptr;
+  MatDev* d_mats = nullptr;
+  int32_t* d_prefix = nullptr;
+  TileEntry* d_tiles = nullptr;
+  PtrEntry* d_ptrs = nullptr;
+  std::vector<PtrEntry> h_ptrs;     // host shadow of d_ptrs
+  bool ptrs_valid = false;
+};
+
+// plan.cpp (host only)
+muon_status build_plan(const muon_matrix_desc* mats, int32_t n, const muon_plan_opts& o, Plan& p,
+                       std::string& err);
+int64_t launches_per_step(const Plan& p, int32_t ns_steps);
+
+// Per-launch arguments shared by the kernel launchers.
+struct StepScalars {
+  float lr, mu, wd, decay;  // decay = 1 - lr*wd
+  float a, b, c, eps;
+  int32_t nesterov, ns_steps;
+};
+
+// ew_kernels.hip
+int launch_momentum(const Plan& p, const WaveHost& w, char* ws, const StepScalars& s, void* stream);
+int launch_finalize(const Plan& p, const WaveHost& w, char* ws, const StepScalars& s, void* stream);
+int launch_apply(const Plan& p, const WaveHost& w, char* ws, const StepScalars& s, void* stream);
+
+// ns_gemm.hip.  stage: 0 Gram (lower tiles), 1 A*A + polynomial (lower tiles),
+// 2 B*X + a*X (all tiles).  iter: NS step index; last: write O.
+enum Stage : int32_t { ST_GRAM = 0, ST_POLY = 1, ST_BX = 2 };
+int launch_ns_gemm(const Plan& p, const WaveHost& w, const ClassLaunch& cl, int32_t stage, int32_t iter,
+                   int32_t last, char* ws, const StepScalars& s, void* stream);
+
+}  // namespace muon

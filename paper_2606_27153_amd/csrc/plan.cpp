@@ -1,0 +1,291 @@
+// Host-side planning of a Muon step: orientation, kernel class and padding
+// per matrix, shape buckets, waves (groups of matrices stepped together),
+// grouped tile tables and the workspace layout.
+//
+// Matrices are independent once their gradients are available, so the plan
+// may group them freely; grouping same-shape matrices into one launch is the
+// batched execution of Sec. 3.3 (small matrices below an occupancy threshold
+// are advanced together instead of each paying a launch).
+#include <algorithm>
+#include <cmath>
+#include <map>
+#include <tuple>
+
+#include "muon_internal.h"
+
+namespace muon {
+
+namespace {
+
+constexpr ClassInfo kClasses[KC_COUNT] = {
+    {256, 0, "bf16_t256"},
+    {128, 0, "bf16_t128"},
+    {64, 0, "bf16_t64"},
+    {128, 1, "f32_t128"},
+    {64, 1, "f32_t64"},
+};
+
+// Relative throughput assumed for each class when choosing a tile: larger
+// tiles re-use each loaded byte more often.
+constexpr double kClassEfficiency[KC_COUNT] = {1.0, 0.8, 0.45, 1.0, 0.6};
+
+constexpr int64_t kDefaultWaveBytes = int64_t(12) << 30;  // 12 GiB
+constexpr int64_t kAlign = 256;
+
+int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+
+double padded_cost(int64_t m, int64_t n, int32_t tile) {
+  const double mp = double(round_up(m, tile)), np = double(round_up(n, tile));
+  return 3.0 * mp * mp * np + mp * mp * mp;
+}
+
+int32_t choose_class(int64_t m, int64_t n, const muon_plan_opts& o) {
+  const bool fp32 = o.precision == MUON_NS_FP32 || m <= o.small_m_threshold;
+  const int32_t lo = fp32 ? KC_F32_128 : KC_BF16_256;
+  const int32_t hi = fp32 ? KC_F32_64 : KC_BF16_64;
+  int32_t best = hi;
+  double best_cost = 0;
+  for (int32_t kc = lo; kc <= hi; ++kc) {
+    const double cost = padded_cost(m, n, kClasses[kc].tile) / kClassEfficiency[kc];
+    if (kc == lo || cost < best_cost) {
+      best = kc;
+      best_cost = cost;
+    }
+  }
+  return best;
+}
+
+// Places logical tile i of a launch at the block index the hardware sends to
+// the XCD owning it: blocks are dispatched round-robin over the 8 XCDs, so
+// block b runs on XCD b % 8.  Each XCD receives a contiguous range of the
+// grouped tile order and therefore shares operand panels in its own L2.
+void xcd_permute(std::vector<TileEntry>& tiles) {
+  constexpr int64_t kXcd = 8;
+  const int64_t n = int64_t(tiles.size());
+  if (n < 2 * kXcd) return;
+  std::vector<TileEntry> out(tiles.size());
+  int64_t start = 0;
+  for (int64_t x = 0; x < kXcd; ++x) {
+    const int64_t cnt = (n - x + kXcd - 1) / kXcd;
+    for (int64_t i = 0; i < cnt; ++i) out[size_t(x + kXcd * i)] = tiles[size_t(start + i)];
+    start += cnt;
+  }
+  tiles.swap(out);
+}
+
+void emit_full(std::vector<TileEntry>& t, int32_t mat, int64_t tm, int64_t tn) {
+  constexpr int64_t kGroup = 4;  // output row panels that advance together
+  for (int64_t g0 = 0; g0 < tm; g0 += kGroup) {
+    const int64_t g1 = std::min(tm, g0 + kGroup);
+    for (int64_t tj = 0; tj < tn; ++tj)
+      for (int64_t ti = g0; ti < g1; ++ti) t.push_back(TileEntry{mat, uint16_t(ti), uint16_t(tj)});
+  }
+}
+
+void emit_lower(std::vector<TileEntry>& t, int32_t mat, int64_t tm) {
+  for (int64_t ti = 0; ti < tm; ++ti)
+    for (int64_t tj = 0; tj <= ti; ++tj) t.push_back(TileEntry{mat, uint16_t(ti), uint16_t(tj)});
+}
+
+}  // namespace
+
+const ClassInfo& class_info(int32_t kc) { return kClasses[kc]; }
+
+int64_t launches_per_step(const Plan& p, int32_t ns_steps) {
+  int64_t n = 0;
+  for (const auto& w : p.waves) n += 3 + int64_t(ns_steps) * 3 * int64_t(w.launches.size());
+  return n;
+}
+
+muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan_opts& o, Plan& p,
+                       std::string& err) {
+  p.opts = o;
+  p.mats.resize(size_t(n));
+  std::map<std::tuple<int32_t, int64_t, int64_t>, int32_t> buckets;
+
+  for (int32_t i = 0; i < n; ++i) {
+    const muon_matrix_desc& d = descs[i];
+    MatHost& h = p.mats[size_t(i)];
+    h.rows = d.rows;
+    h.cols = d.cols;
+    h.transposed = d.rows > d.cols ? 1 : 0;
+    h.m = std::min(d.rows, d.cols);
+    h.n = std::max(d.rows, d.cols);
+    h.param_dtype = d.param_dtype;
+    h.grad_dtype = d.grad_dtype;
+    h.momentum_dtype = d.momentum_dtype;
+    h.kclass = choose_class(h.m, h.n, o);
+    const ClassInfo& ci = kClasses[h.kclass];
+    h.fp32_ns = ci.fp32;
+    h.m_pad = round_up(h.m, ci.tile);
+    h.n_pad = round_up(h.n, ci.tile);
+    if (h.n_pad / ci.tile > 65535) {
+      err = "matrix " + std::to_string(i) + " has too many tiles along one dimension";
+      return MUON_ERR_UNSUPPORTED;
+    }
+    h.rows_pad = h.transposed ? h.n_pad : h.m_pad;
+    h.cols_pad = h.transposed ? h.m_pad : h.n_pad;
+    h.ew_tiles = (h.rows_pad / EW_TILE) * (h.cols_pad / EW_TILE);
+    const auto key = std::make_tuple(h.kclass, h.m, h.n);
+    auto it = buckets.find(key);
+    if (it == buckets.end()) it = buckets.emplace(key, int32_t(buckets.size())).first;
+    h.bucket = it->second;
+
+    const int64_t esz = ci.fp32 ? 4 : 2;
+    int64_t off = 0;
+    auto take = [&](int64_t bytes) {
+      const int64_t at = off;
+      off += round_up(bytes, kAlign);
+      return at;
+    };
+    for (int pp = 0; pp < 2; ++pp) {
+      h.x_off[pp] = take(h.m_pad * h.n_pad * esz);
+      h.xt_off[pp] = take(h.m_pad * h.n_pad * esz);
+    }
+    h.a_off = take(h.m_pad * h.m_pad * esz);
+    h.b_off = take(h.m_pad * h.m_pad * esz);
+    h.o_off = take(h.m_pad * h.n_pad * 4);
+    h.partial_off = take(h.ew_tiles * 4);
+    h.ws_bytes = off;  // relative offsets for now, rebased per wave below
+
+    p.ns_flops += 3.0 * double(h.m) * double(h.m) * double(h.n) + double(h.m) * double(h.m) * double(h.m);
+  }
+  p.n_buckets = int32_t(buckets.size());
+
+  // Wave order: largest buckets first, same bucket contiguous, then index.
+  p.order.resize(size_t(n));
+  for (int32_t i = 0; i < n; ++i) p.order[size_t(i)] = i;
+  std::stable_sort(p.order.begin(), p.order.end(), [&](int32_t x, int32_t y) {
+    const MatHost& a = p.mats[size_t(x)];
+    const MatHost& b = p.mats[size_t(y)];
+    const int64_t ca = a.m_pad * a.n_pad, cb = b.m_pad * b.n_pad;
+    if (ca != cb) return ca > cb;
+    if (a.kclass != b.kclass) return a.kclass < b.kclass;
+    return a.bucket < b.bucket;
+  });
+
+  // Waves: split the ordered list into groups whose workspace stays under
+  // the cap, balanced so that the groups carry similar bytes.
+  const int64_t cap = o.wave_bytes > 0 ? o.wave_bytes : kDefaultWaveBytes;
+  int64_t total = 0;
+  for (const auto& h : p.mats) total += h.ws_bytes;
+  const int64_t n_waves_min = std::max<int64_t>(1, (total + cap - 1) / cap);
+  const int64_t target = (total + n_waves_min - 1) / n_waves_min;
+  {
+    int32_t start = 0;
+    int64_t acc = 0;
+    for (int32_t pos = 0; pos < n; ++pos) {
+      const int64_t b = p.mats[size_t(p.order[size_t(pos)])].ws_bytes;
+      if (pos > start && (acc + b > cap || acc + b > target + target / 8)) {
+        WaveHost w{};
+        w.first = start;
+        w.count = pos - start;
+        p.waves.push_back(w);
+        start = pos;
+        acc = 0;
+      }
+      acc += b;
+    }
+    WaveHost w{};
+    w.first = start;
+    w.count = n - start;
+    p.waves.push_back(w);
+  }
+
+  // Per-wave layout, descriptors, EW prefix and tile tables.
+  p.h_matdev.resize(size_t(n));
+  for (int32_t wi = 0; wi < int32_t(p.waves.size()); ++wi) {
+    WaveHost& w = p.waves[size_t(wi)];
+    int64_t off = 0;
+    w.prefix_off = int64_t(p.h_prefix.size());
+    p.h_prefix.push_back(0);
+    int64_t ew = 0;
+    for (int32_t s = 0; s < w.count; ++s) {
+      const int32_t idx = p.order[size_t(w.first + s)];
+      MatHost& h = p.mats[size_t(idx)];
+      h.wave = wi;
+      h.slot = s;
+      for (int pp = 0; pp < 2; ++pp) {
+        h.x_off[pp] += off;
+        h.xt_off[pp] += off;
+      }
+      h.a_off += off;
+      h.b_off += off;
+      h.o_off += off;
+      h.partial_off += off;
+      off += h.ws_bytes;
+      ew += h.ew_tiles;
+      if (ew > int64_t(INT32_MAX)) {
+        err = "too many elementwise tiles in one wave";
+        return MUON_ERR_UNSUPPORTED;
+      }
+      p.h_prefix.push_back(int32_t(ew));
+
+      MatDev& d = p.h_matdev[size_t(w.first + s)];
+      d = MatDev{};
+      // For a tall matrix the stored layout is X^T, so the momentum kernel's
+      // transposed store produces X; for a wide one the roles swap.
+      for (int pp = 0; pp < 2; ++pp) {
+        d.x_off[pp] = h.x_off[pp];
+        d.xt_off[pp] = h.xt_off[pp];
+      }
+      d.a_off = h.a_off;
+      d.b_off = h.b_off;
+      d.o_off = h.o_off;
+      d.partial_off = h.partial_off;
+      d.rows = int32_t(h.rows);
+      d.cols = int32_t(h.cols);
+      d.rows_pad = int32_t(h.rows_pad);
+      d.cols_pad = int32_t(h.cols_pad);
+      d.m_pad = int32_t(h.m_pad);
+      d.n_pad = int32_t(h.n_pad);
+      d.transposed = h.transposed;
+      d.x_f32 = h.fp32_ns;
+      d.param_dtype = h.param_dtype;
+      d.grad_dtype = h.grad_dtype;
+      d.slot = s;
+      d.index = idx;
+      d.ew_tiles_c = int32_t(h.cols_pad / EW_TILE);
+    }
+    w.ew_tiles = ew;
+    w.scale_off = off;
+    off += round_up(int64_t(w.count) * 4, kAlign);
+    w.flag_off = off;
+    off += round_up(int64_t(w.count) * 4, kAlign);
+    w.ws_bytes = off;
+    p.ws_bytes = std::max(p.ws_bytes, off);
+
+    for (int32_t kc = 0; kc < KC_COUNT; ++kc) {
+      std::vector<TileEntry> lower, full;
+      const int64_t tile = kClasses[kc].tile;
+      for (int32_t s = 0; s < w.count; ++s) {
+        const MatHost& h = p.mats[size_t(p.order[size_t(w.first + s)])];
+        if (h.kclass != kc) continue;
+        const int32_t pos = w.first + s;
+        emit_lower(lower, pos, h.m_pad / tile);
+        emit_full(full, pos, h.m_pad / tile, h.n_pad / tile);
+        const double t2 = double(tile) * double(tile);
+        const int64_t tm = h.m_pad / tile;
+        const double nl = double(tm * (tm + 1) / 2);
+        p.padded_flops += nl * 2.0 * t2 * double(h.n_pad) + nl * 2.0 * t2 * double(h.m_pad) +
+                          double(tm * (h.n_pad / tile)) * 2.0 * t2 * double(h.m_pad);
+      }
+      if (full.empty()) continue;
+      xcd_permute(lower);
+      xcd_permute(full);
+      ClassLaunch cl{};
+      cl.kclass = kc;
+      cl.lower_off = int64_t(p.h_tiles.size());
+      cl.n_lower = int32_t(lower.size());
+      p.h_tiles.insert(p.h_tiles.end(), lower.begin(), lower.end());
+      cl.full_off = int64_t(p.h_tiles.size());
+      cl.n_full = int32_t(full.size());
+      p.h_tiles.insert(p.h_tiles.end(), full.begin(), full.end());
+      w.launches.push_back(cl);
+    }
+  }
+  p.h_ptrs.assign(size_t(n), PtrEntry{nullptr, nullptr, nullptr, nullptr});
+  return MUON_OK;
+}
+
+}  // namespace muon

@@ -1,0 +1,189 @@
+"""Python front end of the HIP Muon step: ``MuonPlan`` and ``Muon``.
+
+``MuonPlan`` wraps muon_plan_create / muon_step / muon_step_debug for a fixed
+list of matrix shapes; PyTorch supplies device memory (the tensors and the
+workspace) and the stream.  ``Muon`` is a torch.optim.Optimizer over 2-D
+parameters (DMuon's user surface, Sec. 4: the optimizer keeps the usual
+optimizer protocol; its state is the per-matrix momentum buffer).
+"""
+from __future__ import annotations
+
+import ctypes
+from typing import List, Optional, Sequence
+
+from . import _lib as L
+
+_DT = {"f32": L.MUON_F32, "bf16": L.MUON_BF16}
+
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.float32:
+        return L.MUON_F32
+    if t.dtype == torch.bfloat16:
+        return L.MUON_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}; use float32 or bfloat16")
+
+
+class MuonPlan:
+    """A plan over matrix descriptors ``(rows, cols, param_dtype, grad_dtype)``.
+
+    dtypes are 'f32' or 'bf16'; momentum is always fp32.
+    """
+
+    def __init__(self, descs: Sequence, *, precision: str = "bf16", max_ns_steps: int = 16,
+                 abc: Optional[Sequence[float]] = None, eps: float = 1e-7,
+                 small_m_threshold: int = 64, wave_bytes: int = 0, host_only: bool = False):
+        lib = L.load()
+        n = len(descs)
+        arr = (L.muon_matrix_desc * max(n, 1))()
+        for i, d in enumerate(descs):
+            rows, cols, pd, gd = d
+            arr[i].rows, arr[i].cols = int(rows), int(cols)
+            arr[i].param_dtype = _DT[pd] if isinstance(pd, str) else int(pd)
+            arr[i].grad_dtype = _DT[gd] if isinstance(gd, str) else int(gd)
+            arr[i].momentum_dtype = L.MUON_F32
+        opts = L.muon_plan_opts()
+        L.check(lib.muon_plan_opts_default(ctypes.byref(opts)))
+        opts.precision = {"bf16": L.MUON_NS_BF16, "fp32": L.MUON_NS_FP32}[precision]
+        opts.max_ns_steps = int(max_ns_steps)
+        if abc is not None:
+            opts.a, opts.b, opts.c = (float(v) for v in abc)
+        opts.eps = float(eps)
+        opts.small_m_threshold = int(small_m_threshold)
+        opts.wave_bytes = int(wave_bytes)
+        opts.flags = L.MUON_PLAN_HOST_ONLY if host_only else 0
+        h = ctypes.c_void_p()
+        L.check(lib.muon_plan_create(arr, n, ctypes.byref(opts), ctypes.byref(h)))
+        self._h = h
+        self.n = n
+        self.descs = list(descs)
+        self.precision = precision
+        self._workspace = None
+
+    # ------------------------------------------------------------ inspection
+    @property
+    def handle(self):
+        return self._h
+
+    @property
+    def workspace_bytes(self) -> int:
+        v = ctypes.c_size_t()
+        L.check(L.load().muon_plan_workspace_bytes(self._h, ctypes.byref(v)))
+        return int(v.value)
+
+    def info(self) -> dict:
+        v = L.muon_plan_info()
+        L.check(L.load().muon_plan_get_info(self._h, ctypes.byref(v)))
+        return {f: getattr(v, f) for f, _ in v._fields_}
+
+    def matrix_info(self, i: int) -> dict:
+        v = L.muon_matrix_info()
+        L.check(L.load().muon_plan_matrix_info(self._h, int(i), ctypes.byref(v)))
+        return {f: getattr(v, f) for f, _ in v._fields_}
+
+    # ------------------------------------------------------------ stepping
+    def workspace(self, device=None):
+        """A cached torch uint8 workspace of the plan's size on ``device``."""
+        import torch
+        need = self.workspace_bytes
+        ws = self._workspace
+        if ws is None or ws.numel() < need or (device is not None and ws.device != torch.device(device)):
+            self._workspace = torch.empty(max(need, 256), dtype=torch.uint8,
+                                          device=device if device is not None else "cuda")
+        return self._workspace
+
+    def step(self, params: List, grads: List, moms: List, *, lr: float, momentum: float,
+             weight_decay: float, ns_steps: int = 5, nesterov: bool = True, workspace=None,
+             stream=None, update_out: Optional[List] = None) -> None:
+        """Enqueues one Muon step on ``stream`` (default: torch's current stream)."""
+        import torch
+        n = self.n
+        if not (len(params) == len(grads) == len(moms) == n):
+            raise ValueError(f"expected {n} params, grads and momentum buffers")
+        if workspace is None:
+            workspace = self.workspace(params[0].device)
+        if stream is None:
+            stream = torch.cuda.current_stream(params[0].device)
+        sp = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+        pp = L.ptr_array([t.data_ptr() for t in params])
+        gp = L.ptr_array([t.data_ptr() for t in grads])
+        mp = L.ptr_array([t.data_ptr() for t in moms])
+        args = (self._h, pp, gp, mp, float(lr), float(momentum), float(weight_decay),
+                int(ns_steps), 1 if nesterov else 0, ctypes.c_void_p(workspace.data_ptr()),
+                workspace.numel() * workspace.element_size(), ctypes.c_void_p(sp))
+        lib = L.load()
+        if update_out is None:
+            L.check(lib.muon_step(*args))
+        else:
+            op = L.ptr_array([0 if t is None else t.data_ptr() for t in update_out])
+            L.check(lib.muon_step_debug(*args, op))
+
+    def close(self) -> None:
+        if getattr(self, "_h", None) is not None and self._h.value:
+            L.check(L.load().muon_plan_destroy(self._h))
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def _optimizer_base():
+    import torch
+    return torch.optim.Optimizer
+
+
+class Muon(_optimizer_base()):
+    """torch.optim-style Muon over 2-D parameters (fp32 or bf16).
+
+    Per-parameter state: ``momentum_buffer`` (fp32).  Parameters without a
+    gradient are skipped for that step (a new plan is built when the set of
+    stepped parameters changes).
+    """
+
+    def __init__(self, params, lr: float = 0.02, momentum: float = 0.95, weight_decay: float = 0.01,
+                 ns_steps: int = 5, nesterov: bool = True, precision: str = "bf16"):
+        defaults = dict(lr=lr, momentum=momentum, weight_decay=weight_decay, ns_steps=ns_steps,
+                        nesterov=nesterov, precision=precision)
+        super().__init__(params, defaults)
+        self._plans = {}
+
+    def _plan_for(self, key, descs, precision):
+        plan = self._plans.get(key)
+        if plan is None:
+            plan = MuonPlan(descs, precision=precision)
+            self._plans[key] = plan
+        return plan
+
+    def step(self, closure=None):
+        import torch
+        loss = None
+        if closure is not None:
+            with torch.enable_grad():
+                loss = closure()
+        for group in self.param_groups:
+            ps = [p for p in group["params"] if p.grad is not None]
+            if not ps:
+                continue
+            for p in ps:
+                if p.ndim != 2:
+                    raise ValueError("Muon steps 2-D parameters only")
+            descs = [(p.shape[0], p.shape[1], _dtype_code(p), _dtype_code(p.grad)) for p in ps]
+            key = (id(group), tuple(descs), group["precision"])
+            plan = self._plan_for(key, descs, group["precision"])
+            moms = []
+            for p in ps:
+                st = self.state[p]
+                if "momentum_buffer" not in st:
+                    st["momentum_buffer"] = torch.zeros_like(p, dtype=torch.float32,
+                                                             memory_format=torch.contiguous_format)
+                moms.append(st["momentum_buffer"])
+            params = [p.data for p in ps]
+            grads = [p.grad.contiguous() for p in ps]
+            plan.step(params, grads, moms, lr=group["lr"], momentum=group["momentum"],
+                      weight_decay=group["weight_decay"], ns_steps=group["ns_steps"],
+                      nesterov=group["nesterov"])
+        return loss

@@ -1,0 +1,190 @@
+"""C-ABI checks that need no GPU: exports, struct layout, host-only plans,
+argument validation and error statuses."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from oracle import muon_ref as R
+from paper_2606_27153_amd import _lib as L
+from paper_2606_27153_amd.optim import MuonPlan
+from paper_2606_27153_amd.workloads import WORKLOAD_KEYS, get_workload
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "muon.h")
+
+
+def _declared_functions():
+    txt = open(HEADER).read()
+    return sorted(set(re.findall(r"^MUON_API\s+[\w\s\*]+?\b(muon_\w+)\(", txt, flags=re.M)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = _declared_functions()
+    assert len(names) >= 11
+    for name in names:
+        assert hasattr(lib, name), name
+        assert name in L.SIGNATURES, name
+    assert lib.muon_abi_version() == 1
+
+
+def test_struct_layout_matches_c_compiler(tmp_path):
+    src = tmp_path / "layout.c"
+    structs = {
+        "muon_matrix_desc": L.muon_matrix_desc,
+        "muon_plan_opts": L.muon_plan_opts,
+        "muon_plan_info": L.muon_plan_info,
+        "muon_matrix_info": L.muon_matrix_info,
+    }
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "muon.h"', "int main(void){"]
+    for sname, cls in structs.items():
+        lines.append(f'printf("{sname} size %zu\\n", sizeof({sname}));')
+        for f, _ in cls._fields_:
+            lines.append(f'printf("{sname} {f} %zu\\n", offsetof({sname}, {f}));')
+    lines.append("return 0;}")
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c99", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)],
+                   check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+    for line in out:
+        if not line:
+            continue
+        sname, field, val = line.split()
+        cls = structs[sname]
+        if field == "size":
+            assert ctypes.sizeof(cls) == int(val), sname
+        else:
+            assert getattr(cls, field).offset == int(val), (sname, field)
+
+
+def test_opts_default(lib):
+    o = L.muon_plan_opts()
+    assert lib.muon_plan_opts_default(ctypes.byref(o)) == L.MUON_OK
+    assert (o.precision, o.max_ns_steps, o.small_m_threshold, o.flags, o.wave_bytes) == (0, 16, 64, 0, 0)
+    assert abs(o.a - 3.4445) < 1e-6 and abs(o.b + 4.775) < 1e-6 and abs(o.c - 2.0315) < 1e-6
+    assert abs(o.eps - 1e-7) < 1e-12
+    assert lib.muon_plan_opts_default(None) == L.MUON_ERR_INVALID_ARG
+    assert "NULL" in L.last_error()
+
+
+def _descs(wl):
+    return [(m.rows, m.cols, m.param, m.grad) for m in wl.matrices]
+
+
+@pytest.mark.parametrize("key", WORKLOAD_KEYS)
+def test_host_only_plan_of_each_workload(key):
+    wl = get_workload(key)
+    plan = MuonPlan(_descs(wl), host_only=True)
+    info = plan.info()
+    assert info["n_matrices"] == wl.n
+    assert info["device"] == -1
+    assert info["n_waves"] >= 1
+    want = sum(R.ns_flops(m.rows, m.cols, 1) for m in wl.matrices)
+    assert abs(info["ns_flops_per_ns_step"] - want) <= 1e-9 * want
+    assert info["padded_flops_per_ns_step"] >= info["ns_flops_per_ns_step"]
+    assert plan.workspace_bytes > 0
+    waves = set()
+    for i, m in enumerate(wl.matrices):
+        mi = plan.matrix_info(i)
+        assert mi["m"] == min(m.rows, m.cols) and mi["n"] == max(m.rows, m.cols)
+        assert mi["transposed"] == int(m.rows > m.cols)
+        assert mi["m_pad"] % mi["tile"] == 0 and mi["n_pad"] % mi["tile"] == 0
+        assert mi["m"] <= mi["m_pad"] < mi["m"] + mi["tile"]
+        assert mi["n"] <= mi["n_pad"] < mi["n"] + mi["tile"]
+        assert mi["fp32_ns"] == int(mi["m"] <= 64)
+        waves.add(mi["wave"])
+    assert waves == set(range(info["n_waves"]))
+    plan.close()
+
+
+def test_fp32_precision_uses_fp32_everywhere():
+    wl = get_workload("tiny")
+    plan = MuonPlan(_descs(wl), precision="fp32", host_only=True)
+    assert all(plan.matrix_info(i)["fp32_ns"] == 1 for i in range(wl.n))
+
+
+def test_buckets_of_the_8b_set():
+    wl = get_workload("8b")
+    plan = MuonPlan(_descs(wl), host_only=True)
+    assert plan.info()["n_buckets"] == 3
+    shapes = {(plan.matrix_info(i)["m"], plan.matrix_info(i)["n"]) for i in range(wl.n)}
+    assert shapes == {(4096, 14336), (4096, 4096), (1024, 4096)}
+
+
+def test_wave_cap_splits_work():
+    wl = get_workload("1b")
+    one = MuonPlan(_descs(wl), host_only=True, wave_bytes=1 << 40)
+    many = MuonPlan(_descs(wl), host_only=True, wave_bytes=1 << 30)
+    assert one.info()["n_waves"] == 1
+    assert many.info()["n_waves"] > 1
+    assert many.workspace_bytes < one.workspace_bytes
+
+
+def _create(lib, descs, opts=None):
+    arr = (L.muon_matrix_desc * max(1, len(descs)))()
+    for i, d in enumerate(descs):
+        arr[i].rows, arr[i].cols, arr[i].param_dtype, arr[i].grad_dtype, arr[i].momentum_dtype = d
+    h = ctypes.c_void_p()
+    if opts is None:
+        opts = L.muon_plan_opts()
+        lib.muon_plan_opts_default(ctypes.byref(opts))
+        opts.flags = L.MUON_PLAN_HOST_ONLY
+    st = lib.muon_plan_create(arr, len(descs), ctypes.byref(opts), ctypes.byref(h))
+    return st, h
+
+
+@pytest.mark.parametrize("desc,status", [
+    ((0, 5, 1, 1, 0), L.MUON_ERR_INVALID_ARG),
+    ((5, -1, 1, 1, 0), L.MUON_ERR_INVALID_ARG),
+    ((1 << 31, 5, 1, 1, 0), L.MUON_ERR_INVALID_ARG),
+    ((5, 5, 7, 1, 0), L.MUON_ERR_UNSUPPORTED),
+    ((5, 5, 1, 9, 0), L.MUON_ERR_UNSUPPORTED),
+    ((5, 5, 1, 1, 1), L.MUON_ERR_UNSUPPORTED),   # bf16 momentum
+])
+def test_plan_create_rejects_bad_descriptors(lib, desc, status):
+    st, h = _create(lib, [desc])
+    assert st == status
+    assert h.value is None
+    assert L.last_error()
+
+
+@pytest.mark.parametrize("field,value", [
+    ("precision", 3), ("max_ns_steps", 0), ("max_ns_steps", 65), ("eps", -1.0),
+    ("small_m_threshold", -1), ("flags", 0x10), ("wave_bytes", -5), ("a", float("nan")),
+])
+def test_plan_create_rejects_bad_opts(lib, field, value):
+    opts = L.muon_plan_opts()
+    lib.muon_plan_opts_default(ctypes.byref(opts))
+    opts.flags = L.MUON_PLAN_HOST_ONLY
+    setattr(opts, field, value)
+    st, h = _create(lib, [(8, 8, 1, 1, 0)], opts)
+    assert st == L.MUON_ERR_INVALID_ARG
+    assert field.split("_")[0] in L.last_error() or "opts" in L.last_error()
+
+
+def test_null_arguments(lib):
+    h = ctypes.c_void_p()
+    assert lib.muon_plan_create(None, 1, None, ctypes.byref(h)) == L.MUON_ERR_INVALID_ARG
+    arr = (L.muon_matrix_desc * 1)()
+    assert lib.muon_plan_create(arr, 0, None, ctypes.byref(h)) == L.MUON_ERR_INVALID_ARG
+    assert lib.muon_plan_create(arr, 1, None, None) == L.MUON_ERR_INVALID_ARG
+    assert lib.muon_plan_destroy(None) == L.MUON_OK
+    b = ctypes.c_size_t()
+    assert lib.muon_plan_workspace_bytes(None, ctypes.byref(b)) == L.MUON_ERR_INVALID_ARG
+    for s in range(6):
+        assert lib.muon_status_string(s).decode().startswith("MUON_")
+
+
+def test_step_on_host_only_plan_is_rejected_before_any_device_call(lib):
+    st, h = _create(lib, [(8, 16, 1, 1, 0)])
+    assert st == L.MUON_OK
+    p = L.ptr_array([16])
+    r = lib.muon_step(h, p, p, p, 0.02, 0.95, 0.01, 5, 1, ctypes.c_void_p(256), 1 << 20, None)
+    assert r == L.MUON_ERR_INVALID_ARG
+    assert "host-only" in L.last_error()
+    mi = L.muon_matrix_info()
+    assert lib.muon_plan_matrix_info(h, 5, ctypes.byref(mi)) == L.MUON_ERR_INVALID_ARG
+    assert lib.muon_plan_destroy(h) == L.MUON_OK

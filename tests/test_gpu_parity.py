@@ -1,0 +1,183 @@
+"""GPU parity: the HIP Muon step (through the C ABI) against the fp64 oracle.
+
+Bars: relative Frobenius error of O per matrix <= 2e-2 on the bf16 NS path
+and <= 1e-5 on the fp32 path; momentum <= 1e-6; parameters within the drift
+bound of parity_utils; zero-gradient matrices bitwise unchanged.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2606_27153_amd.optim import MuonPlan
+from paper_2606_27153_amd.workloads import custom_workload, get_workload, make_grads, make_state
+
+from parity_utils import TOL_O, assert_parity, rel, run_parity, to64
+
+pytestmark = pytest.mark.gpu
+
+
+def _banner(msg):
+    print(f"[gpu-test] {msg}", flush=True)
+
+
+@pytest.mark.parametrize("precision", ["bf16", "fp32"])
+def test_tiny_three_steps(precision):
+    wl = get_workload("tiny")
+    _banner(f"tiny {precision}")
+    res = run_parity(wl, precision=precision)
+    _banner(f"tiny {precision}: worst O {res.worst('o_rel'):.3e} M {res.worst('m_rel'):.3e}")
+    assert_parity(res, precision, "tiny")
+
+
+RAGGED = [(1, 1), (1, 300), (300, 1), (7, 13), (65, 200), (200, 65), (130, 700), (700, 130),
+          (257, 513), (513, 257), (1000, 1000), (96, 4304), (1152, 1200), (33, 1030)]
+
+
+@pytest.mark.parametrize("precision", ["bf16", "fp32"])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_ragged_shapes(precision, dtype):
+    wl = custom_workload(RAGGED, param=dtype, grad=dtype, seed=11)
+    _banner(f"ragged {precision} {dtype}")
+    res = run_parity(wl, precision=precision, steps=2)
+    _banner(f"ragged {precision} {dtype}: worst O {res.worst('o_rel'):.3e}")
+    assert_parity(res, precision, "ragged")
+
+
+def test_ragged_shapes_small_waves():
+    # every matrix in a wave of its own: same results as the single-wave plan
+    wl = custom_workload(RAGGED, seed=12)
+    res = run_parity(wl, precision="bf16", steps=1, wave_bytes=1)
+    assert_parity(res, "bf16", "ragged-waves")
+
+
+def test_zero_gradients_leave_bf16_params_bitwise_unchanged():
+    wl = get_workload("moe")
+    # a small slice of the MoE bank: a few experts, some unrouted
+    idx = [i for i, m in enumerate(wl.matrices) if m.name.startswith("l0.e") and int(m.name.split(".")[1][1:]) < 8]
+    sub = [wl.matrices[i] for i in idx]
+    assert any(m.zero_grad for m in sub) and not all(m.zero_grad for m in sub)
+    from dataclasses import replace
+    swl = replace(wl, matrices=sub, key="moe-slice")
+    params, moms = make_state(torch, swl, "cuda:0")
+    w0 = [p.clone() for p in params]
+    plan = MuonPlan([(m.rows, m.cols, m.param, m.grad) for m in sub])
+    for step in range(2):
+        grads = make_grads(torch, swl, step, "cuda:0")
+        outs = [torch.full((m.rows, m.cols), 7.0, device="cuda:0") for m in sub]
+        plan.step(params, grads, moms, lr=0.02, momentum=0.95, weight_decay=0.01, ns_steps=5, update_out=outs)
+        torch.cuda.synchronize()
+        for k, m in enumerate(sub):
+            if m.zero_grad:
+                assert torch.equal(params[k], w0[k]), m.name
+                assert not torch.any(moms[k]) and not torch.any(outs[k]), m.name
+            else:
+                assert not torch.equal(params[k], w0[k]), m.name
+    plan.close()
+
+
+def test_deterministic_and_batching_invariant():
+    wl = custom_workload([(300, 700), (700, 300), (1024, 1024), (130, 520)] * 3, seed=5)
+    g = make_grads(torch, wl, 0, "cuda:0")
+
+    def run(descs_idx, wave_bytes):
+        sub = [wl.matrices[i] for i in descs_idx]
+        plan = MuonPlan([(m.rows, m.cols, m.param, m.grad) for m in sub], wave_bytes=wave_bytes)
+        params, moms = make_state(torch, wl, "cuda:0", descs_idx)
+        outs = [torch.empty(m.rows, m.cols, device="cuda:0") for m in sub]
+        plan.step(params, [g[i] for i in descs_idx], moms, lr=0.02, momentum=0.95, weight_decay=0.01,
+                  ns_steps=5, update_out=outs)
+        torch.cuda.synchronize()
+        plan.close()
+        return params, moms, outs
+
+    full = list(range(wl.n))
+    a = run(full, 0)
+    b = run(full, 0)
+    for x, y in zip(a, b):
+        for s, t in zip(x, y):
+            assert torch.equal(s, t)
+    # the same matrix stepped alone, or in one-matrix waves, gives identical bits
+    for i in (0, 1, 2, 3):
+        alone = run([i], 0)
+        assert torch.equal(alone[2][0], a[2][i]) and torch.equal(alone[0][0], a[0][i])
+    split = run(full, 1)
+    for x, y in zip(a, split):
+        for s, t in zip(x, y):
+            assert torch.equal(s, t)
+
+
+@pytest.mark.parametrize("precision", ["bf16", "fp32"])
+def test_zero_ns_steps_is_normalised_input(precision):
+    wl = custom_workload([(64, 200), (200, 128), (256, 256)], seed=3)
+    res = run_parity(wl, precision=precision, steps=1, ns_steps=0)
+    # with k = 0, O = u/||u||: bf16 storage of u costs at most 2^-9 relative
+    bound = 4e-3 if precision == "bf16" else 1e-6
+    for r in res.reports:
+        assert r.o_rel <= bound, (r.index, r.o_rel)
+
+
+def test_plain_momentum_without_nesterov():
+    wl = custom_workload([(256, 768), (768, 256)], seed=4)
+    res = run_parity(wl, precision="bf16", steps=2, nesterov=False)
+    assert_parity(res, "bf16", "no-nesterov")
+
+
+def test_step_and_debug_step_are_bitwise_identical():
+    wl = custom_workload([(300, 500), (500, 300), (2048, 512)], seed=6)
+    descs = [(m.rows, m.cols, m.param, m.grad) for m in wl.matrices]
+    plan = MuonPlan(descs)
+    pa, ma = make_state(torch, wl, "cuda:0")
+    pb, mb = make_state(torch, wl, "cuda:0")
+    for step in range(2):
+        g = make_grads(torch, wl, step, "cuda:0")
+        plan.step(pa, g, ma, lr=0.02, momentum=0.95, weight_decay=0.01)
+        outs = [torch.empty(m.rows, m.cols, device="cuda:0") for m in wl.matrices]
+        plan.step(pb, g, mb, lr=0.02, momentum=0.95, weight_decay=0.01, update_out=outs)
+    torch.cuda.synchronize()
+    for x, y in zip(pa + ma, pb + mb):
+        assert torch.equal(x, y)
+    plan.close()
+
+
+def test_error_statuses_on_gpu():
+    from paper_2606_27153_amd import _lib as L
+    wl = custom_workload([(64, 128)], seed=1)
+    plan = MuonPlan([(64, 128, "bf16", "bf16")])
+    p, m = make_state(torch, wl, "cuda:0")
+    g = make_grads(torch, wl, 0, "cuda:0")
+    small = torch.empty(256, dtype=torch.uint8, device="cuda:0")
+    with pytest.raises(L.MuonError) as e:
+        plan.step(p, g, m, lr=0.02, momentum=0.95, weight_decay=0.01, workspace=small)
+    assert e.value.status == L.MUON_ERR_WORKSPACE_TOO_SMALL
+    with pytest.raises(L.MuonError) as e:
+        plan.step(p, g, m, lr=0.02, momentum=1.5, weight_decay=0.01)
+    assert e.value.status == L.MUON_ERR_INVALID_ARG
+    with pytest.raises(L.MuonError) as e:
+        plan.step(p, g, m, lr=0.02, momentum=0.9, weight_decay=0.01, ns_steps=17)
+    assert e.value.status == L.MUON_ERR_INVALID_ARG
+    w0 = p[0].clone()
+    torch.cuda.synchronize()
+    assert torch.equal(p[0], w0)   # nothing was launched
+    plan.close()
+
+
+def _sample(wl, per_bucket, extra=()):
+    seen = {}
+    for i, m in enumerate(wl.matrices):
+        key = (min(m.rows, m.cols), max(m.rows, m.cols), m.rows > m.cols, m.zero_grad)
+        seen.setdefault(key, []).append(i)
+    out = set(extra)
+    for key, idx in seen.items():
+        out.update(idx[:per_bucket] if not key[3] else idx[:1])
+        out.add(idx[-1])
+    return sorted(out)
+
+
+@pytest.mark.parametrize("key,per_bucket", [("1b", 1), ("vla", 1), ("moe", 1), ("8b", 1)])
+def test_full_size_workload_sampled(key, per_bucket):
+    wl = get_workload(key)
+    check = _sample(wl, per_bucket)
+    _banner(f"{key}: full plan on GPU, oracle on {len(check)} sampled matrices")
+    res = run_parity(wl, precision="bf16", steps=1, check=check)
+    _banner(f"{key}: worst O {res.worst('o_rel'):.3e} M {res.worst('m_rel'):.3e}")
+    assert_parity(res, "bf16", key)
