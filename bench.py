@@ -1,0 +1,245 @@
+"""Benchmark of the single-GPU Muon optimizer step (one JSON line on stdout).
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 8b]
+
+A step is one muon_step over every matrix of the chosen synthetic set:
+momentum + Nesterov, Frobenius normalisation, 5 Newton-Schulz steps, apply.
+Inputs (params, grads, momentum) are resident in HBM before the timed
+region.  Per-launch durations come from HIP events recorded by the library
+on its stream during the timed steps; the dominant kernel's achieved rate is
+its algorithmic work per launch over its mean launch duration.  The fp64
+oracle is timed on the host cores on a bounded sample as a reference point.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "Muon optimizer-step ms per step (1 GPU) + MFMA util % on Newton–Schulz GEMMs"
+PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 matrix peak: 256 CU x 2.4 GHz x 4096 flop/clk
+PEAK_F32_TFLOPS = 157.3       # MI355X fp32 matrix peak
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+GEMM_KINDS = ("gram", "poly", "bx")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_sources_hash() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2606_27153_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode() + f.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(kernel_key: str):
+    """HBM traffic of the dominant kernel from the committed rocprofv3 --pmc
+    summary, if it was taken on the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", "traffic_summary.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if line.startswith("#") or "=" not in line:
+                continue
+            k, v = line.split("=", 1)
+            vals[k.strip()] = v.strip()
+    if vals.get("sources_sha256_16") != kernel_sources_hash() or vals.get("kernel") != kernel_key:
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(wl, budget_s: float):
+    """Times the fp64 oracle on one matrix per shape bucket and extrapolates
+    to the whole set by bucket counts."""
+    import numpy as np
+    import torch
+
+    from oracle import muon_ref as R
+    from paper_2606_27153_amd.workloads import make_grad, make_param
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([d.get("num_threads", 1) for d in threadpool_info() if d.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    buckets = {}
+    for i, m in enumerate(wl.matrices):
+        buckets.setdefault((min(m.rows, m.cols), max(m.rows, m.cols)), []).append(i)
+    order = sorted(buckets.items(), key=lambda kv: kv[0][0] * kv[0][0] * kv[0][1])
+    total_ms = 0.0
+    sampled = []
+    spent = 0.0
+    lr, mu, wd = wl.lr, wl.momentum, wl.weight_decay
+    per_flop_ms = None
+    for (m, n), idx in order:
+        i = idx[0]
+        flops = R.ns_flops(m, n, wl.ns_steps)
+        if spent < budget_s or per_flop_ms is None:
+            w = make_param(torch, wl, i, "cpu").double().numpy()
+            g = make_grad(torch, wl, i, 0, "cpu").double().numpy()
+            t0 = time.perf_counter()
+            R.muon_step_matrix(w, g, np.zeros_like(g), lr=lr, momentum=mu, weight_decay=wd,
+                               ns_steps=wl.ns_steps, nesterov=wl.nesterov, param_dtype=wl.matrices[i].param)
+            dt = time.perf_counter() - t0
+            spent += dt
+            per_flop_ms = dt * 1e3 / flops
+            sampled.append(f"{wl.matrices[i].rows}x{wl.matrices[i].cols} {dt:.2f}s")
+            total_ms += dt * 1e3 * len(idx)
+        else:
+            total_ms += per_flop_ms * flops * len(idx)
+            sampled.append(f"{m}x{n} extrapolated by flops")
+    return {"value": round(total_ms, 1), "unit": "ms", "cores": int(threads), "kind": "oracle",
+            "sample": ("fp64 numpy oracle, one matrix per shape bucket, one step each ("
+                       + "; ".join(sampled) + "), scaled by bucket counts to the whole set")}
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", default="8b", choices=["tiny", "1b", "8b", "vla", "moe"])
+    ap.add_argument("--precision", default="bf16", choices=["bf16", "fp32"])
+    ap.add_argument("--wave-bytes", type=int, default=0)
+    ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle time to sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: the Muon step here runs on one GPU's matrices with no "
+              f"collectives; --gpus {args.gpus} is not supported", file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_2606_27153_amd.optim import MuonPlan
+    from paper_2606_27153_amd.workloads import get_workload, make_grads, make_state
+
+    if not torch.cuda.is_available():
+        log("bench.py needs a GPU")
+        return 1
+    dev = "cuda:0"
+    wl = get_workload(args.config)
+    log(f"[bench] workload {wl.key}: {wl.description}; {wl.elements() / 1e9:.2f} G elements")
+    plan = MuonPlan([(m.rows, m.cols, m.param, m.grad) for m in wl.matrices], precision=args.precision,
+                    wave_bytes=args.wave_bytes)
+    info = plan.info()
+    log(f"[bench] plan: {info['n_waves']} waves, {info['n_buckets']} buckets, "
+        f"{info['launches_per_step']} launches/step at max steps, workspace {info['workspace_bytes'] / 2**30:.2f} GiB")
+    params, moms = make_state(torch, wl, dev)
+    grads = make_grads(torch, wl, 0, dev)
+    ws = plan.workspace(dev)
+    stream = torch.cuda.current_stream(dev)
+    kw = dict(lr=wl.lr, momentum=wl.momentum, weight_decay=wl.weight_decay, ns_steps=wl.ns_steps,
+              nesterov=wl.nesterov, workspace=ws, stream=stream)
+    torch.cuda.synchronize()
+    for i in range(args.warmup):
+        plan.step(params, grads, moms, **kw)
+        torch.cuda.synchronize()
+        log(f"[bench] warmup step {i + 1}/{args.warmup} done")
+
+    plan.set_timing(True)
+    plan.timing_read(reset=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        plan.step(params, grads, moms, **kw)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    plan.set_timing(False)
+    stats = plan.timing_read(reset=True)
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    log(f"[bench] {args.steps} timed steps: {ms_per_step:.3f} ms/step")
+
+    peak_mm = PEAK_BF16_TFLOPS if args.precision == "bf16" else PEAK_F32_TFLOPS
+    per_kernel = []
+    for s in sorted(stats, key=lambda s: -s["total_ms"]):
+        mean_ms = s["total_ms"] / max(1, s["launches"])
+        row = {"kind": s["kind"], "class": s["kernel_class"], "launches_per_step": s["launches"] / args.steps,
+               "ms_per_step": round(s["total_ms"] / args.steps, 4), "mean_launch_ms": round(mean_ms, 5)}
+        if s["kind"] in GEMM_KINDS and s["total_ms"] > 0:
+            row["tflops"] = round(s["algo_flops"] / (s["total_ms"] * 1e-3) / 1e12, 2)
+        if s["kind"] in ("momentum", "apply") and s["total_ms"] > 0:
+            row["gbs"] = round(s["algo_bytes"] / (s["total_ms"] * 1e-3) / 1e9, 1)
+        per_kernel.append(row)
+        log(f"[bench]   {json.dumps(row)}")
+
+    gemm = [s for s in stats if s["kind"] in GEMM_KINDS]
+    gemm_ms = sum(s["total_ms"] for s in gemm) / args.steps
+    gemm_flops = sum(s["algo_flops"] for s in gemm) / args.steps
+    ew = [s for s in stats if s["kind"] in ("momentum", "apply")]
+    ew_bytes = sum(s["algo_bytes"] for s in ew) / args.steps
+    ns_tflops = gemm_flops / (gemm_ms * 1e-3) / 1e12 if gemm_ms > 0 else 0.0
+    mfma_util = 100.0 * ns_tflops / peak_mm
+
+    dom = max(stats, key=lambda s: s["total_ms"])
+    dom_key = f"{dom['kind']}:{dom['kernel_class']}"
+    dom_mean_s = dom["total_ms"] * 1e-3 / dom["launches"]
+    if dom["kind"] in GEMM_KINDS:
+        achieved = dom["algo_flops"] / dom["launches"] / dom_mean_s / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak_mm, "unit": "TFLOP/s",
+                "frac": round(achieved / peak_mm, 4)}
+    else:
+        achieved = dom["algo_bytes"] / dom["launches"] / dom_mean_s / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBS, 4)}
+    roof["kernel"] = dom_key
+    roof["mean_launch_ms"] = round(dom["total_ms"] / dom["launches"], 4)
+    roof["traffic"] = read_traffic(dom_key)
+
+    floor_ms = (gemm_flops / (peak_mm * 1e12) + ew_bytes / (PEAK_HBM_GBS * 1e9)) * 1e3
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("[bench] timing the fp64 oracle on a sample of the same set ...")
+        cpu = cpu_baseline(wl, args.cpu_budget)
+        log(f"[bench] oracle: {cpu}")
+
+    out = {
+        "metric": METRIC,
+        "value": round(ms_per_step, 3),
+        "unit": "ms",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if args.precision == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.key, "description": wl.description, "matrices": wl.n,
+                   "elements": wl.elements(), "ns_steps": wl.ns_steps,
+                   "params": sorted({m.param for m in wl.matrices}), "momentum": "f32",
+                   "ns_operands": args.precision, "parallelism": "single GPU"},
+        "mfma_util_pct_ns_gemms": round(mfma_util, 2),
+        "ns_gemm_tflops": round(ns_tflops, 2),
+        "ns_gemm_ms_per_step": round(gemm_ms, 3),
+        "step_roofline_floor_ms": round(floor_ms, 3),
+        "step_roofline_frac": round(floor_ms / ms_per_step, 4),
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "kernels": per_kernel,
+    }
+    print(json.dumps(out), flush=True)
+    plan.close()
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

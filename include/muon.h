@@ -176,6 +176,41 @@ MUON_API muon_status muon_step_debug(muon_plan plan, void* const* params, const 
                             void* workspace, size_t workspace_bytes, void* hip_stream,
                             float* const* update_out);
 
+/* Launch timing.  While enabled, muon_step records a pair of HIP events on
+ * its stream around every kernel launch (a few microseconds per launch).
+ * muon_plan_timing_read waits for the recorded events, and aggregates the
+ * launches by (kind, kernel class) into stats[0..capacity), setting *count
+ * to the number of entries; with reset != 0 the records are dropped
+ * afterwards.  Flops and bytes are the algorithmic work of each launch:
+ *   MUON_KERNEL_GRAM  m^2 n flops per matrix (half of the symmetric X X^T)
+ *   MUON_KERNEL_POLY  m^3 flops (half of the symmetric A*A)
+ *   MUON_KERNEL_BX    2 m^2 n flops
+ *   MUON_KERNEL_MOMENTUM  read G, read and write M, write X0 once
+ *   MUON_KERNEL_APPLY     read W and O (fp32), write W
+ * counted for every matrix of the launch, also ones skipped for a zero
+ * gradient.  Timing must be read on the thread that steps the plan. */
+typedef enum muon_kernel_kind {
+  MUON_KERNEL_MOMENTUM = 0,
+  MUON_KERNEL_FINALIZE = 1,
+  MUON_KERNEL_GRAM = 2,
+  MUON_KERNEL_POLY = 3,
+  MUON_KERNEL_BX = 4,
+  MUON_KERNEL_APPLY = 5
+} muon_kernel_kind;
+
+typedef struct muon_kernel_stat {
+  int32_t kind;                      /* muon_kernel_kind */
+  int32_t kernel_class;              /* GEMM class, -1 for elementwise kernels */
+  int64_t launches;
+  double total_ms;                   /* sum of event-measured launch durations */
+  double algo_flops;                 /* summed over the launches */
+  double algo_bytes;
+} muon_kernel_stat;
+
+MUON_API muon_status muon_plan_set_timing(muon_plan plan, int32_t enable);
+MUON_API muon_status muon_plan_timing_read(muon_plan plan, muon_kernel_stat* stats, int32_t capacity,
+                                           int32_t* count, int32_t reset);
+
 MUON_API const char* muon_status_string(muon_status s);
 
 /* Thread-local description of the last failure on this thread ("" if none). */

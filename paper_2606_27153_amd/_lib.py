@@ -61,6 +61,15 @@ class muon_matrix_info(ctypes.Structure):
                 ("wave", ctypes.c_int32), ("bucket", ctypes.c_int32)]
 
 
+class muon_kernel_stat(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("kernel_class", ctypes.c_int32),
+                ("launches", ctypes.c_int64), ("total_ms", ctypes.c_double),
+                ("algo_flops", ctypes.c_double), ("algo_bytes", ctypes.c_double)]
+
+
+KERNEL_KINDS = ("momentum", "finalize", "gram", "poly", "bx", "apply")
+KERNEL_CLASSES = ("bf16_t256", "bf16_t128", "bf16_t64", "f32_t128", "f32_t64")
+
 _VP = ctypes.c_void_p
 _PP = ctypes.POINTER(ctypes.c_void_p)
 _STEP_ARGS = [_VP, _PP, _PP, _PP, ctypes.c_float, ctypes.c_float, ctypes.c_float,
@@ -77,6 +86,9 @@ SIGNATURES = {
     "muon_plan_matrix_info": (ctypes.c_int, [_VP, ctypes.c_int32, ctypes.POINTER(muon_matrix_info)]),
     "muon_step": (ctypes.c_int, _STEP_ARGS),
     "muon_step_debug": (ctypes.c_int, _STEP_ARGS + [_PP]),
+    "muon_plan_set_timing": (ctypes.c_int, [_VP, ctypes.c_int32]),
+    "muon_plan_timing_read": (ctypes.c_int, [_VP, ctypes.POINTER(muon_kernel_stat), ctypes.c_int32,
+                                             ctypes.POINTER(ctypes.c_int32), ctypes.c_int32]),
     "muon_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "muon_last_error": (ctypes.c_char_p, []),
     "muon_abi_version": (ctypes.c_int32, []),

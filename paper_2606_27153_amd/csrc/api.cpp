@@ -146,19 +146,57 @@ muon_status step_impl(muon_plan plan, void* const* params, const void* const* gr
   s.nesterov = nesterov;
   s.ns_steps = ns_steps;
   char* ws = static_cast<char*>(workspace);
+  hipStream_t hs = hipStream_t(stream);
+  // Runs one launch, bracketed by timing events when timing is enabled.
+  auto run = [&](int32_t kind, int32_t kclass, double flops, double bytes, auto&& launch) -> hipError_t {
+    size_t ev = 0;
+    if (p.timing) {
+      ev = p.records.size() * 2;
+      while (p.events.size() < ev + 2) {
+        hipEvent_t e;
+        hipError_t er = hipEventCreate(&e);
+        if (er != hipSuccess) return er;
+        p.events.push_back(e);
+      }
+      hipError_t er = hipEventRecord(hipEvent_t(p.events[ev]), hs);
+      if (er != hipSuccess) return er;
+    }
+    if (launch()) {
+      hipError_t er = hipGetLastError();
+      return er == hipSuccess ? hipErrorLaunchFailure : er;
+    }
+    if (p.timing) {
+      hipError_t er = hipEventRecord(hipEvent_t(p.events[ev + 1]), hs);
+      if (er != hipSuccess) return er;
+      p.records.push_back(TimingRecord{kind, kclass, flops, bytes, ev});
+    }
+    return hipSuccess;
+  };
   for (const WaveHost& w : p.waves) {
-    if (launch_momentum(p, w, ws, s, stream)) return hip_fail(hipGetLastError(), "momentum kernel launch");
-    if (launch_finalize(p, w, ws, s, stream)) return hip_fail(hipGetLastError(), "finalize kernel launch");
+    e = run(MUON_KERNEL_MOMENTUM, -1, 0.0, w.bytes_momentum, [&] { return launch_momentum(p, w, ws, s, stream); });
+    if (e != hipSuccess) return hip_fail(e, "momentum kernel launch");
+    e = run(MUON_KERNEL_FINALIZE, -1, 0.0, 0.0, [&] { return launch_finalize(p, w, ws, s, stream); });
+    if (e != hipSuccess) return hip_fail(e, "finalize kernel launch");
     for (int32_t it = 0; it < ns_steps; ++it) {
       const int32_t last = it == ns_steps - 1;
       for (int32_t stage = ST_GRAM; stage <= ST_BX; ++stage)
-        for (const ClassLaunch& cl : w.launches)
-          if (launch_ns_gemm(p, w, cl, stage, it, last, ws, s, stream))
-            return hip_fail(hipGetLastError(), "NS GEMM launch");
+        for (const ClassLaunch& cl : w.launches) {
+          const int32_t kind = stage == ST_GRAM ? MUON_KERNEL_GRAM : stage == ST_POLY ? MUON_KERNEL_POLY : MUON_KERNEL_BX;
+          const double fl = stage == ST_GRAM ? cl.flops_gram : stage == ST_POLY ? cl.flops_poly : cl.flops_bx;
+          e = run(kind, cl.kclass, fl, 0.0, [&] { return launch_ns_gemm(p, w, cl, stage, it, last, ws, s, stream); });
+          if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
+        }
     }
-    if (launch_apply(p, w, ws, s, stream)) return hip_fail(hipGetLastError(), "apply kernel launch");
+    e = run(MUON_KERNEL_APPLY, -1, 0.0, w.bytes_apply, [&] { return launch_apply(p, w, ws, s, stream); });
+    if (e != hipSuccess) return hip_fail(e, "apply kernel launch");
   }
   return ok();
+}
+
+void release_events(muon::Plan& p) {
+  for (void* e : p.events) (void)hipEventDestroy(hipEvent_t(e));
+  p.events.clear();
+  p.records.clear();
 }
 
 }  // namespace
@@ -253,6 +291,7 @@ muon_status muon_plan_create(const muon_matrix_desc* mats, int32_t n, const muon
 muon_status muon_plan_destroy(muon_plan plan) {
   if (!plan) return ok();
   muon_status st = MUON_OK;
+  release_events(plan->p);
   if (plan->p.d_block) {
     hipError_t e = hipFree(plan->p.d_block);
     if (e != hipSuccess) st = hip_fail(e, "hipFree of plan tables");
@@ -298,6 +337,43 @@ muon_status muon_plan_matrix_info(muon_plan plan, int32_t index, muon_matrix_inf
   info->fp32_ns = h.fp32_ns;
   info->wave = h.wave;
   info->bucket = h.bucket;
+  return ok();
+}
+
+muon_status muon_plan_set_timing(muon_plan plan, int32_t enable) {
+  if (!plan) return fail(MUON_ERR_INVALID_ARG, "plan is NULL");
+  if (!plan->p.d_block) return fail(MUON_ERR_INVALID_ARG, "plan was created host-only");
+  plan->p.timing = enable != 0;
+  return ok();
+}
+
+muon_status muon_plan_timing_read(muon_plan plan, muon_kernel_stat* stats, int32_t capacity, int32_t* count,
+                                  int32_t reset) {
+  if (!plan || !count || (capacity > 0 && !stats) || capacity < 0)
+    return fail(MUON_ERR_INVALID_ARG, "plan, count (and stats when capacity > 0) must be non-NULL");
+  muon::Plan& p = plan->p;
+  std::vector<muon_kernel_stat> agg;
+  for (const muon::TimingRecord& r : p.records) {
+    hipEvent_t e0 = hipEvent_t(p.events[r.event]), e1 = hipEvent_t(p.events[r.event + 1]);
+    hipError_t e = hipEventSynchronize(e1);
+    float ms = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+    if (e != hipSuccess) return hip_fail(e, "reading timing events");
+    muon_kernel_stat* st = nullptr;
+    for (auto& a : agg)
+      if (a.kind == r.kind && a.kernel_class == r.kclass) st = &a;
+    if (!st) {
+      agg.push_back(muon_kernel_stat{r.kind, r.kclass, 0, 0.0, 0.0, 0.0});
+      st = &agg.back();
+    }
+    st->launches += 1;
+    st->total_ms += double(ms);
+    st->algo_flops += r.flops;
+    st->algo_bytes += r.bytes;
+  }
+  *count = int32_t(agg.size());
+  for (int32_t i = 0; i < capacity && size_t(i) < agg.size(); ++i) stats[i] = agg[size_t(i)];
+  if (reset) p.records.clear();
   return ok();
 }
 

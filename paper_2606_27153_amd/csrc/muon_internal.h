@@ -85,6 +85,7 @@ struct MatHost {
 
 struct ClassLaunch {
   int32_t kclass;
+  double flops_gram, flops_poly, flops_bx;  // algorithmic flops of one launch
   int64_t lower_off;   // TileEntry offset of the lower-triangular list
   int32_t n_lower;
   int64_t full_off;    // TileEntry offset of the full list
@@ -99,7 +100,14 @@ struct WaveHost {
   int64_t scale_off;   // workspace byte offset: float scale[count]
   int64_t flag_off;    // workspace byte offset: int32 flag[count]
   int64_t ws_bytes;
+  double bytes_momentum, bytes_apply;  // algorithmic HBM bytes of one launch
   std::vector<ClassLaunch> launches;
+};
+
+struct TimingRecord {
+  int32_t kind, kclass;
+  double flops, bytes;
+  size_t event;  // index of the start event; the stop event follows it
 };
 
 struct Plan {
@@ -123,6 +131,11 @@ struct Plan {
   PtrEntry* d_ptrs = nullptr;
   std::vector<PtrEntry> h_ptrs;     // host shadow of d_ptrs
   bool ptrs_valid = false;
+
+  // launch timing (muon_plan_set_timing)
+  bool timing = false;
+  std::vector<void*> events;        // hipEvent_t pool, start/stop pairs
+  std::vector<TimingRecord> records;
 };
 
 // plan.cpp (host only)

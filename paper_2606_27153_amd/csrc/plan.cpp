@@ -248,6 +248,16 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
       d.ew_tiles_c = int32_t(h.cols_pad / EW_TILE);
     }
     w.ew_tiles = ew;
+    w.bytes_momentum = 0;
+    w.bytes_apply = 0;
+    for (int32_t s = 0; s < w.count; ++s) {
+      const MatHost& h = p.mats[size_t(p.order[size_t(w.first + s)])];
+      const double el = double(h.rows) * double(h.cols);
+      const double gsz = h.grad_dtype == MUON_BF16 ? 2 : 4, psz = h.param_dtype == MUON_BF16 ? 2 : 4;
+      const double xsz = h.fp32_ns ? 4 : 2;
+      w.bytes_momentum += el * (gsz + 4 + 4 + xsz);
+      w.bytes_apply += el * (psz + 4 + psz);
+    }
     w.scale_off = off;
     off += round_up(int64_t(w.count) * 4, kAlign);
     w.flag_off = off;
@@ -258,10 +268,15 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
     for (int32_t kc = 0; kc < KC_COUNT; ++kc) {
       std::vector<TileEntry> lower, full;
       const int64_t tile = kClasses[kc].tile;
+      double fg = 0, fp = 0, fb = 0;
       for (int32_t s = 0; s < w.count; ++s) {
         const MatHost& h = p.mats[size_t(p.order[size_t(w.first + s)])];
         if (h.kclass != kc) continue;
         const int32_t pos = w.first + s;
+        const double m = double(h.m), nn = double(h.n);
+        fg += m * m * nn;
+        fp += m * m * m;
+        fb += 2 * m * m * nn;
         emit_lower(lower, pos, h.m_pad / tile);
         emit_full(full, pos, h.m_pad / tile, h.n_pad / tile);
         const double t2 = double(tile) * double(tile);
@@ -275,6 +290,9 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
       xcd_permute(full);
       ClassLaunch cl{};
       cl.kclass = kc;
+      cl.flops_gram = fg;
+      cl.flops_poly = fp;
+      cl.flops_bx = fb;
       cl.lower_off = int64_t(p.h_tiles.size());
       cl.n_lower = int32_t(lower.size());
       p.h_tiles.insert(p.h_tiles.end(), lower.begin(), lower.end());

@@ -82,6 +82,25 @@ class MuonPlan:
         L.check(L.load().muon_plan_matrix_info(self._h, int(i), ctypes.byref(v)))
         return {f: getattr(v, f) for f, _ in v._fields_}
 
+    def set_timing(self, enable: bool) -> None:
+        L.check(L.load().muon_plan_set_timing(self._h, 1 if enable else 0))
+
+    def timing_read(self, reset: bool = True) -> list:
+        """Event-timed launches aggregated by (kind, kernel class)."""
+        lib = L.load()
+        cap = 64
+        arr = (L.muon_kernel_stat * cap)()
+        cnt = ctypes.c_int32()
+        L.check(lib.muon_plan_timing_read(self._h, arr, cap, ctypes.byref(cnt), 1 if reset else 0))
+        out = []
+        for i in range(min(cnt.value, cap)):
+            s = arr[i]
+            out.append({"kind": L.KERNEL_KINDS[s.kind],
+                        "kernel_class": None if s.kernel_class < 0 else L.KERNEL_CLASSES[s.kernel_class],
+                        "launches": s.launches, "total_ms": s.total_ms,
+                        "algo_flops": s.algo_flops, "algo_bytes": s.algo_bytes})
+        return out
+
     # ------------------------------------------------------------ stepping
     def workspace(self, device=None):
         """A cached torch uint8 workspace of the plan's size on ``device``."""

@@ -37,6 +37,7 @@ def test_struct_layout_matches_c_compiler(tmp_path):
         "muon_plan_opts": L.muon_plan_opts,
         "muon_plan_info": L.muon_plan_info,
         "muon_matrix_info": L.muon_matrix_info,
+        "muon_kernel_stat": L.muon_kernel_stat,
     }
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "muon.h"', "int main(void){"]
     for sname, cls in structs.items():
@@ -187,4 +188,7 @@ def test_step_on_host_only_plan_is_rejected_before_any_device_call(lib):
     assert "host-only" in L.last_error()
     mi = L.muon_matrix_info()
     assert lib.muon_plan_matrix_info(h, 5, ctypes.byref(mi)) == L.MUON_ERR_INVALID_ARG
+    assert lib.muon_plan_set_timing(h, 1) == L.MUON_ERR_INVALID_ARG
+    cnt = ctypes.c_int32()
+    assert lib.muon_plan_timing_read(h, None, 0, ctypes.byref(cnt), 1) == L.MUON_OK and cnt.value == 0
     assert lib.muon_plan_destroy(h) == L.MUON_OK
