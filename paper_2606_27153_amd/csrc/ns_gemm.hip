@@ -22,9 +22,11 @@
 // zeros stay zero through all three products, so the kernels need no bounds
 // checks.
 //
-// Block: 256 threads = 2 x 2 waves, output tile TILE x TILE, each wave owns a
-// (TILE/2)^2 quadrant made of 32 x 32 MFMA blocks.  K advances in 128-byte
-// slabs (64 bf16 / 32 fp32) staged through double-buffered, XOR-swizzled LDS.
+// Block: WGM x WGN waves (2 x 4 for the 256 tile, 2 x 2 otherwise), output
+// tile TILE x TILE, each wave owning a (TILE/WGM) x (TILE/WGN) piece made of
+// 32 x 32 MFMA blocks.  K advances in 128-byte slabs (64 bf16 / 32 fp32)
+// moved straight from global memory into double-buffered, XOR-swizzled LDS
+// by global_load_lds_dwordx4 (no staging registers).
 #include <hip/hip_runtime.h>
 
 #include "muon_internal.h"
@@ -49,47 +51,162 @@ struct GemmArgs {
   int32_t last;    // ST_BX of the last step writes O
 };
 
-// 16-byte chunk c of LDS row r lives at chunk position c ^ (r & 7): the 8
-// rows read together by one MFMA operand fetch land in 8 different bank groups.
-__device__ inline int swz(int row, int chunk) { return chunk ^ (row & 7); }
+// 16-byte chunk c of LDS row r (128-byte rows) lives at chunk position
+// c ^ f(r) with f(r) = (r & 7) ^ ((r >> 3) & 1).  An MFMA operand fetch reads
+// the same logical chunk from consecutive rows; any 8 consecutive rows then
+// hit 8 different 16-byte bank groups, and any 16 consecutive rows hit 16
+// different ones of the 256-byte bank window, so the fetch is conflict-free
+// whether the LDS serves 8 or 16 lanes of a ds_read_b128 per cycle.
+__device__ __forceinline__ int swz(int row) { return (row & 7) ^ ((row >> 3) & 1); }
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) const void gbl_void_t;
 
 template <typename E>
-__device__ inline E to_e(float v);
+__device__ __forceinline__ E to_e(float v);
 template <>
-__device__ inline __bf16 to_e<__bf16>(float v) { return __bf16(v); }
+__device__ __forceinline__ __bf16 to_e<__bf16>(float v) { return __bf16(v); }
 template <>
-__device__ inline float to_e<float>(float v) { return v; }
+__device__ __forceinline__ float to_e<float>(float v) { return v; }
 
 template <typename E>
-__device__ inline void store_vec4(E* p, const float v[4]);
+__device__ __forceinline__ void store_vec4(E* p, float v0, float v1, float v2, float v3);
 template <>
-__device__ inline void store_vec4<__bf16>(__bf16* p, const float v[4]) {
+__device__ __forceinline__ void store_vec4<__bf16>(__bf16* p, float v0, float v1, float v2, float v3) {
   bf16x4 x;
-  x[0] = __bf16(v[0]); x[1] = __bf16(v[1]); x[2] = __bf16(v[2]); x[3] = __bf16(v[3]);
+  x[0] = __bf16(v0); x[1] = __bf16(v1); x[2] = __bf16(v2); x[3] = __bf16(v3);
   *reinterpret_cast<bf16x4*>(p) = x;
 }
 template <>
-__device__ inline void store_vec4<float>(float* p, const float v[4]) {
-  *reinterpret_cast<f32x4*>(p) = f32x4{v[0], v[1], v[2], v[3]};
+__device__ __forceinline__ void store_vec4<float>(float* p, float v0, float v1, float v2, float v3) {
+  *reinterpret_cast<f32x4*>(p) = f32x4{v0, v1, v2, v3};
 }
 
-template <typename E, int TILE, int STAGE>
-__global__ __launch_bounds__(256, 1) void ns_gemm_kernel(GemmArgs args) {
-  constexpr int EPC = 16 / int(sizeof(E));       // elements per 16-byte chunk
-  constexpr int BK = 8 * EPC;                     // elements per 128-byte slab
-  constexpr int WT = TILE / 2;                    // wave quadrant
-  constexpr int NB = WT / 32;                     // 32x32 blocks per quadrant side
-  constexpr int LOADS = TILE * 8 / 256;           // 16-byte chunks per thread per operand
-  constexpr int OPB = TILE * 128;                 // bytes of one operand slab
+// Compile-time shape of one GEMM configuration.
+template <typename E, int TILE, int WGM, int WGN>
+struct Cfg {
+  static constexpr int NW = WGM * WGN;            // waves per block
+  static constexpr int NT = NW * 64;              // threads per block
+  static constexpr int EPC = 16 / int(sizeof(E));  // elements per 16-byte chunk
+  static constexpr int BK = 8 * EPC;              // elements per 128-byte K slab
+  static constexpr int WTM = TILE / WGM, WTN = TILE / WGN;  // wave tile
+  static constexpr int NBM = WTM / 32, NBN = WTN / 32;      // 32x32 MFMA blocks per wave
+  static constexpr int OPB = TILE * 128;          // LDS bytes of one operand slab
+  static constexpr int CPW = TILE / 8 / NW;       // 1 KB LDS chunks per wave per operand
+  static_assert(CPW >= 1 && TILE / 8 % NW == 0, "tile too small for the block");
+};
 
-  __shared__ __attribute__((aligned(16))) char smem[2][2][OPB];
+// Direct-to-LDS loads of one operand slab.  global_load_lds_dwordx4 writes
+// lane l's 16 bytes to LDS offset chunk*1024 + 16*l of the wave's 1 KB chunk,
+// i.e. row 8*chunk + l/8 at physical chunk position l%8; lane l therefore
+// fetches the logical chunk that the swizzle stores in that slot.  The wave's
+// chunks are wid, wid + NW, ...; since NW is even, row & 15 of every row a
+// lane touches is the same, so one per-lane source pointer serves all of
+// them with a uniform offset of 8*NW rows per chunk.
+template <class C, typename E>
+__device__ __forceinline__ const E* lane_src(const E* op, int64_t K, int wid, int lane) {
+  const int row = wid * 8 + (lane >> 3);
+  const int chunk = (lane & 7) ^ swz(row);
+  return op + int64_t(row) * K + chunk * C::EPC;
+}
+
+template <class C, typename E>
+__device__ __forceinline__ void load_slab(const E* src, int64_t K, int kt, char* lds, int wid) {
+#pragma unroll
+  for (int i = 0; i < C::CPW; ++i) {
+    const E* g = src + int64_t(i) * (8 * C::NW) * K + int64_t(kt) * C::BK;
+    __builtin_amdgcn_global_load_lds((gbl_void_t*)(g), (lds_void_t*)(lds + (wid + C::NW * i) * 1024), 16, 0,
+                                     0);
+  }
+}
+
+// Per-lane LDS byte offset of the MFMA operand fragment for K sub-step ks:
+// row (base + lane%32), logical chunk 2*ks + lane/32.  Fragment i of the
+// wave adds i*32 rows = i*4096 bytes, which leaves row & 15 (the swizzle)
+// unchanged.
+__device__ __forceinline__ int frag_off(int row0, int lane, int ks) {
+  const int r = row0 + (lane & 31);
+  return r * 128 + (((2 * ks + (lane >> 5)) ^ swz(r)) << 4);
+}
+
+template <typename E>
+struct Frag;
+template <>
+struct Frag<__bf16> { typedef bf16x8 T; };
+template <>
+struct Frag<float> { typedef f32x4 T; };
+
+template <class C, typename E>
+__device__ __forceinline__ void read_frags(const char* sa, const char* sb, int oa, int ob,
+                                           typename Frag<E>::T (&fa)[C::NBM], typename Frag<E>::T (&fb)[C::NBN]) {
+#pragma unroll
+  for (int i = 0; i < C::NBM; ++i) fa[i] = *reinterpret_cast<const typename Frag<E>::T*>(sa + oa + i * 4096);
+#pragma unroll
+  for (int j = 0; j < C::NBN; ++j) fb[j] = *reinterpret_cast<const typename Frag<E>::T*>(sb + ob + j * 4096);
+}
+
+template <class C, typename E>
+__device__ __forceinline__ void mfma_frags(const typename Frag<E>::T (&fa)[C::NBM],
+                                           const typename Frag<E>::T (&fb)[C::NBN], f32x16 (&acc)[C::NBM][C::NBN]) {
+  if constexpr (sizeof(E) == 2) {
+#pragma unroll
+    for (int i = 0; i < C::NBM; ++i)
+#pragma unroll
+      for (int j = 0; j < C::NBN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+  } else {
+    // fp32: lane half h holds k = 4*(2*ks + h) + q for element q, and the
+    // same mapping on both operands, so the four 32x32x2 MFMAs cover 8 k.
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int i = 0; i < C::NBM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::NBN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[i][q], fb[j][q], acc[i][j], 0, 0, 0);
+  }
+}
+
+// One 128-byte K slab of MFMA work for this wave from LDS operand slabs
+// sa/sb, in four K sub-steps.  The fragments of sub-step ks+1 are read
+// while the MFMAs of sub-step ks run; scheduling barriers keep the compiler
+// from hoisting further reads (which would only add register pressure).
+template <class C, typename E>
+__device__ __forceinline__ void mma_slab(const char* sa, const char* sb, const int (&oa)[4], const int (&ob)[4],
+                                         f32x16 (&acc)[C::NBM][C::NBN]) {
+  typename Frag<E>::T fa0[C::NBM], fb0[C::NBN], fa1[C::NBM], fb1[C::NBN];
+  read_frags<C, E>(sa, sb, oa[0], ob[0], fa0, fb0);
+  __builtin_amdgcn_sched_barrier(0);
+  read_frags<C, E>(sa, sb, oa[1], ob[1], fa1, fb1);
+  mfma_frags<C, E>(fa0, fb0, acc);
+  __builtin_amdgcn_sched_barrier(0);
+  read_frags<C, E>(sa, sb, oa[2], ob[2], fa0, fb0);
+  mfma_frags<C, E>(fa1, fb1, acc);
+  __builtin_amdgcn_sched_barrier(0);
+  read_frags<C, E>(sa, sb, oa[3], ob[3], fa1, fb1);
+  mfma_frags<C, E>(fa0, fb0, acc);
+  __builtin_amdgcn_sched_barrier(0);
+  mfma_frags<C, E>(fa1, fb1, acc);
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+__device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+template <typename E, int TILE, int WGM, int WGN, int STAGE>
+__global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) {
+  using C = Cfg<E, TILE, WGM, WGN>;
+  // Two LDS stages as distinct objects, so that the loads in flight into one
+  // stage are known not to alias the reads of the other.
+  __shared__ __attribute__((aligned(1024))) char stage0[2 * C::OPB];
+  __shared__ __attribute__((aligned(1024))) char stage1[2 * C::OPB];
 
   const TileEntry te = args.tiles[blockIdx.x];
   const MatDev& d = args.mats[te.mat];
   if (args.flag[d.slot]) return;  // all-zero update: O is never read
 
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const int wm = wid >> 1, wn = wid & 1;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
+  const int wm = wid / WGN, wn = wid % WGN;
   const int ti = te.ti, tj = te.tj;
   const int64_t mp = d.m_pad, np = d.n_pad;
 
@@ -114,161 +231,125 @@ __global__ __launch_bounds__(256, 1) void ns_gemm_kernel(GemmArgs args) {
     opb = xt + int64_t(tj) * TILE * K;
   }
 
-  uint4 ra[LOADS], rb[LOADS];
-  auto gload = [&](int kt) {
+  f32x16 acc[C::NBM][C::NBN];
 #pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      const int cid = tid + i * 256;
-      const int row = cid >> 3, ck = cid & 7;
-      const int64_t off = int64_t(row) * K + int64_t(kt) * BK + ck * EPC;
-      ra[i] = *reinterpret_cast<const uint4*>(opa + off);
-      rb[i] = *reinterpret_cast<const uint4*>(opb + off);
-    }
-  };
-  auto lstore = [&](int buf) {
+  for (int i = 0; i < C::NBM; ++i)
 #pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      const int cid = tid + i * 256;
-      const int row = cid >> 3, ck = cid & 7;
-      const int o = row * 128 + (swz(row, ck) << 4);
-      *reinterpret_cast<uint4*>(&smem[buf][0][o]) = ra[i];
-      *reinterpret_cast<uint4*>(&smem[buf][1][o]) = rb[i];
-    }
-  };
-
-  f32x16 acc[NB][NB];
-#pragma unroll
-  for (int i = 0; i < NB; ++i)
-#pragma unroll
-    for (int j = 0; j < NB; ++j)
+    for (int j = 0; j < C::NBN; ++j)
 #pragma unroll
       for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
 
-  auto compute = [&](int buf) {
-    const char* sa = smem[buf][0];
-    const char* sb = smem[buf][1];
+  // K loop, two slabs per trip so that each stage buffer is addressed
+  // statically.  The loads of slab k+1 are in flight while slab k is
+  // multiplied; one barrier per slab publishes the landed stage and retires
+  // the one just read.  (No early exit inside the trip: a second loop exit
+  // would make the compiler copy the accumulators between register files.)
+  const int nk = int(K / C::BK);
+  const E* srca = lane_src<C>(opa, K, wid, lane);
+  const E* srcb = lane_src<C>(opb, K, wid, lane);
+  int oa[4], ob[4];
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const int ck = 2 * ks + (lane >> 5);
-      if constexpr (sizeof(E) == 2) {
-        bf16x8 fa[NB], fb[NB];
-#pragma unroll
-        for (int i = 0; i < NB; ++i) {
-          const int r = wm * WT + i * 32 + (lane & 31);
-          fa[i] = *reinterpret_cast<const bf16x8*>(sa + r * 128 + (swz(r, ck) << 4));
-        }
-#pragma unroll
-        for (int j = 0; j < NB; ++j) {
-          const int r = wn * WT + j * 32 + (lane & 31);
-          fb[j] = *reinterpret_cast<const bf16x8*>(sb + r * 128 + (swz(r, ck) << 4));
-        }
-#pragma unroll
-        for (int i = 0; i < NB; ++i)
-#pragma unroll
-          for (int j = 0; j < NB; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
-      } else {
-        f32x4 fa[NB], fb[NB];
-#pragma unroll
-        for (int i = 0; i < NB; ++i) {
-          const int r = wm * WT + i * 32 + (lane & 31);
-          fa[i] = *reinterpret_cast<const f32x4*>(sa + r * 128 + (swz(r, ck) << 4));
-        }
-#pragma unroll
-        for (int j = 0; j < NB; ++j) {
-          const int r = wn * WT + j * 32 + (lane & 31);
-          fb[j] = *reinterpret_cast<const f32x4*>(sb + r * 128 + (swz(r, ck) << 4));
-        }
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-#pragma unroll
-          for (int i = 0; i < NB; ++i)
-#pragma unroll
-            for (int j = 0; j < NB; ++j)
-              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[i][q], fb[j][q], acc[i][j], 0, 0, 0);
-      }
-    }
-  };
-
-  const int nk = int(K / BK);
-  gload(0);
-  lstore(0);
+  for (int ks = 0; ks < 4; ++ks) {
+    oa[ks] = frag_off(wm * C::WTM, lane, ks);
+    ob[ks] = frag_off(wn * C::WTN, lane, ks);
+  }
+  load_slab<C>(srca, K, 0, stage0, wid);
+  load_slab<C>(srcb, K, 0, stage0 + C::OPB, wid);
+  wait_vm_all();
   __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) gload(kt + 1);
-    compute(kt & 1);
-    if (kt + 1 < nk) lstore((kt + 1) & 1);
+  int kt = 0;
+  for (; kt + 2 <= nk; kt += 2) {
+    load_slab<C>(srca, K, kt + 1, stage1, wid);
+    load_slab<C>(srcb, K, kt + 1, stage1 + C::OPB, wid);
+    mma_slab<C, E>(stage0, stage0 + C::OPB, oa, ob, acc);
+    wait_vm_all();
+    __syncthreads();
+    if (kt + 2 < nk) {
+      load_slab<C>(srca, K, kt + 2, stage0, wid);
+      load_slab<C>(srcb, K, kt + 2, stage0 + C::OPB, wid);
+    }
+    mma_slab<C, E>(stage1, stage1 + C::OPB, oa, ob, acc);
+    wait_vm_all();
     __syncthreads();
   }
+  if (kt < nk) mma_slab<C, E>(stage0, stage0 + C::OPB, oa, ob, acc);  // odd slab count: last slab is in stage 0
 
   // ---------------------------------------------------------------- epilogue
   // Accumulator element q of a 32x32 block sits at row 8*(q/4) + 4*(lane/32)
   // + q%4 and column lane%32 of that block.
   const float sc = args.first ? args.scale[d.slot] : 1.f;
-  const int64_t ld_sq = mp;  // A and B leading dimension
 #pragma unroll
-  for (int i = 0; i < NB; ++i)
+  for (int i = 0; i < C::NBM; ++i)
 #pragma unroll
-    for (int j = 0; j < NB; ++j)
+    for (int j = 0; j < C::NBN; ++j)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int64_t i0 = int64_t(ti) * TILE + wm * WT + i * 32 + 8 * g + 4 * (lane >> 5);
-        const int64_t jc = int64_t(tj) * TILE + wn * WT + j * 32 + (lane & 31);
-        float v[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) v[r] = acc[i][j][4 * g + r];
+        const int64_t i0 = int64_t(ti) * TILE + wm * C::WTM + i * 32 + 8 * g + 4 * (lane >> 5);
+        const int64_t jc = int64_t(tj) * TILE + wn * C::WTN + j * 32 + (lane & 31);
+        float v0 = acc[i][j][4 * g + 0], v1 = acc[i][j][4 * g + 1];
+        float v2 = acc[i][j][4 * g + 2], v3 = acc[i][j][4 * g + 3];
         if (STAGE == ST_GRAM) {
           E* a = reinterpret_cast<E*>(args.ws + d.a_off);
           const float s2 = sc * sc;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            v[r] *= s2;
-            a[(i0 + r) * ld_sq + jc] = to_e<E>(v[r]);
-          }
-          if (ti != tj) store_vec4<E>(a + jc * ld_sq + i0, v);
+          v0 *= s2; v1 *= s2; v2 *= s2; v3 *= s2;
+          a[(i0 + 0) * mp + jc] = to_e<E>(v0);
+          a[(i0 + 1) * mp + jc] = to_e<E>(v1);
+          a[(i0 + 2) * mp + jc] = to_e<E>(v2);
+          a[(i0 + 3) * mp + jc] = to_e<E>(v3);
+          if (ti != tj) store_vec4<E>(a + jc * mp + i0, v0, v1, v2, v3);
         } else if (STAGE == ST_POLY) {
           const E* a = reinterpret_cast<const E*>(args.ws + d.a_off);
           E* b = reinterpret_cast<E*>(args.ws + d.b_off);
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            v[r] = args.b * float(a[(i0 + r) * ld_sq + jc]) + args.c * v[r];
-            b[(i0 + r) * ld_sq + jc] = to_e<E>(v[r]);
-          }
-          if (ti != tj) store_vec4<E>(b + jc * ld_sq + i0, v);
+          v0 = args.b * float(a[(i0 + 0) * mp + jc]) + args.c * v0;
+          v1 = args.b * float(a[(i0 + 1) * mp + jc]) + args.c * v1;
+          v2 = args.b * float(a[(i0 + 2) * mp + jc]) + args.c * v2;
+          v3 = args.b * float(a[(i0 + 3) * mp + jc]) + args.c * v3;
+          b[(i0 + 0) * mp + jc] = to_e<E>(v0);
+          b[(i0 + 1) * mp + jc] = to_e<E>(v1);
+          b[(i0 + 2) * mp + jc] = to_e<E>(v2);
+          b[(i0 + 3) * mp + jc] = to_e<E>(v3);
+          if (ti != tj) store_vec4<E>(b + jc * mp + i0, v0, v1, v2, v3);
         } else {
           const E* x = reinterpret_cast<const E*>(args.ws + d.x_off[args.pin]);
-#pragma unroll
-          for (int r = 0; r < 4; ++r) v[r] = sc * (args.a * float(x[(i0 + r) * np + jc]) + v[r]);
+          v0 = sc * (args.a * float(x[(i0 + 0) * np + jc]) + v0);
+          v1 = sc * (args.a * float(x[(i0 + 1) * np + jc]) + v1);
+          v2 = sc * (args.a * float(x[(i0 + 2) * np + jc]) + v2);
+          v3 = sc * (args.a * float(x[(i0 + 3) * np + jc]) + v3);
           if (!args.last) {
             E* xo = reinterpret_cast<E*>(args.ws + d.x_off[args.pin ^ 1]);
             E* xto = reinterpret_cast<E*>(args.ws + d.xt_off[args.pin ^ 1]);
-#pragma unroll
-            for (int r = 0; r < 4; ++r) xo[(i0 + r) * np + jc] = to_e<E>(v[r]);
-            store_vec4<E>(xto + jc * mp + i0, v);
+            xo[(i0 + 0) * np + jc] = to_e<E>(v0);
+            xo[(i0 + 1) * np + jc] = to_e<E>(v1);
+            xo[(i0 + 2) * np + jc] = to_e<E>(v2);
+            xo[(i0 + 3) * np + jc] = to_e<E>(v3);
+            store_vec4<E>(xto + jc * mp + i0, v0, v1, v2, v3);
           } else {
             float* o = reinterpret_cast<float*>(args.ws + d.o_off);
             if (!d.transposed) {
-#pragma unroll
-              for (int r = 0; r < 4; ++r) o[(i0 + r) * np + jc] = v[r];
+              o[(i0 + 0) * np + jc] = v0;
+              o[(i0 + 1) * np + jc] = v1;
+              o[(i0 + 2) * np + jc] = v2;
+              o[(i0 + 3) * np + jc] = v3;
             } else {
-              store_vec4<float>(o + jc * mp + i0, v);
+              store_vec4<float>(o + jc * mp + i0, v0, v1, v2, v3);
             }
           }
         }
       }
 }
 
-template <typename E, int TILE>
+template <typename E, int TILE, int WGM, int WGN>
 int launch_stage(int32_t stage, unsigned nblocks, const GemmArgs& g, hipStream_t st) {
+  constexpr int NT = WGM * WGN * 64;
   switch (stage) {
     case ST_GRAM:
-      hipLaunchKernelGGL((ns_gemm_kernel<E, TILE, ST_GRAM>), dim3(nblocks), dim3(256), 0, st, g);
+      hipLaunchKernelGGL((ns_gemm_kernel<E, TILE, WGM, WGN, ST_GRAM>), dim3(nblocks), dim3(NT), 0, st, g);
       break;
     case ST_POLY:
-      hipLaunchKernelGGL((ns_gemm_kernel<E, TILE, ST_POLY>), dim3(nblocks), dim3(256), 0, st, g);
+      hipLaunchKernelGGL((ns_gemm_kernel<E, TILE, WGM, WGN, ST_POLY>), dim3(nblocks), dim3(NT), 0, st, g);
       break;
     default:
-      hipLaunchKernelGGL((ns_gemm_kernel<E, TILE, ST_BX>), dim3(nblocks), dim3(256), 0, st, g);
+      hipLaunchKernelGGL((ns_gemm_kernel<E, TILE, WGM, WGN, ST_BX>), dim3(nblocks), dim3(NT), 0, st, g);
       break;
   }
   return hipGetLastError() == hipSuccess ? 0 : -1;
@@ -295,11 +376,11 @@ int launch_ns_gemm(const Plan& p, const WaveHost& w, const ClassLaunch& cl, int3
   if (nblocks == 0) return 0;
   hipStream_t st = hipStream_t(stream);
   switch (cl.kclass) {
-    case KC_BF16_256: return launch_stage<__bf16, 256>(stage, nblocks, g, st);
-    case KC_BF16_128: return launch_stage<__bf16, 128>(stage, nblocks, g, st);
-    case KC_BF16_64: return launch_stage<__bf16, 64>(stage, nblocks, g, st);
-    case KC_F32_128: return launch_stage<float, 128>(stage, nblocks, g, st);
-    case KC_F32_64: return launch_stage<float, 64>(stage, nblocks, g, st);
+    case KC_BF16_256: return launch_stage<__bf16, 256, 2, 4>(stage, nblocks, g, st);
+    case KC_BF16_128: return launch_stage<__bf16, 128, 2, 2>(stage, nblocks, g, st);
+    case KC_BF16_64: return launch_stage<__bf16, 64, 2, 2>(stage, nblocks, g, st);
+    case KC_F32_128: return launch_stage<float, 128, 2, 2>(stage, nblocks, g, st);
+    case KC_F32_64: return launch_stage<float, 64, 2, 2>(stage, nblocks, g, st);
     default: return -1;
   }
 }
