@@ -93,6 +93,7 @@ struct Cfg {
   static constexpr int NBM = WTM / 32, NBN = WTN / 32;      // 32x32 MFMA blocks per wave
   static constexpr int OPB = TILE * 128;          // LDS bytes of one operand slab
   static constexpr int CPW = TILE / 8 / NW;       // 1 KB LDS chunks per wave per operand
+  static constexpr int WAVE_LDS = 4 * OPB / NW;   // LDS bytes per wave for the epilogue
   static_assert(CPW >= 1 && TILE / 8 % NW == 0, "tile too small for the block");
 };
 
@@ -167,30 +168,168 @@ __device__ __forceinline__ void mfma_frags(const typename Frag<E>::T (&fa)[C::NB
   }
 }
 
-// One 128-byte K slab of MFMA work for this wave from LDS operand slabs
-// sa/sb, in four K sub-steps.  The fragments of sub-step ks+1 are read
-// while the MFMAs of sub-step ks run; scheduling barriers keep the compiler
-// from hoisting further reads (which would only add register pressure).
+// Interleaves one LDS fragment read with a group of MFMAs so that the reads
+// for the next K sub-step are spread over the current sub-step's MFMAs.
+template <int NREAD, int NMFMA>
+__device__ __forceinline__ void interleave() {
+  if constexpr (NMFMA >= NREAD && NREAD > 0) {
+#pragma unroll
+    for (int q = 0; q < NREAD; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);              // DS read
+      __builtin_amdgcn_sched_group_barrier(0x008, NMFMA / NREAD, 0);  // MFMA
+    }
+  }
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// MFMA work of one 128-byte K slab held in LDS stage st.  On entry the
+// fragments of sub-step 0 are in (fa0, fb0); each sub-step reads the next
+// sub-step's fragments while its own MFMAs run.
 template <class C, typename E>
-__device__ __forceinline__ void mma_slab(const char* sa, const char* sb, const int (&oa)[4], const int (&ob)[4],
-                                         f32x16 (&acc)[C::NBM][C::NBN]) {
-  typename Frag<E>::T fa0[C::NBM], fb0[C::NBN], fa1[C::NBM], fb1[C::NBN];
-  read_frags<C, E>(sa, sb, oa[0], ob[0], fa0, fb0);
-  __builtin_amdgcn_sched_barrier(0);
-  read_frags<C, E>(sa, sb, oa[1], ob[1], fa1, fb1);
+__device__ __forceinline__ void slab_body(const char* st, const int (&oa)[4], const int (&ob)[4],
+                                          typename Frag<E>::T (&fa0)[C::NBM], typename Frag<E>::T (&fb0)[C::NBN],
+                                          typename Frag<E>::T (&fa1)[C::NBM], typename Frag<E>::T (&fb1)[C::NBN],
+                                          f32x16 (&acc)[C::NBM][C::NBN]) {
+  constexpr int NR = C::NBM + C::NBN;
+  constexpr int NM = C::NBM * C::NBN * (sizeof(E) == 2 ? 1 : 4);
+  read_frags<C, E>(st, st + C::OPB, oa[1], ob[1], fa1, fb1);
   mfma_frags<C, E>(fa0, fb0, acc);
-  __builtin_amdgcn_sched_barrier(0);
-  read_frags<C, E>(sa, sb, oa[2], ob[2], fa0, fb0);
+  interleave<NR, NM>();
+  read_frags<C, E>(st, st + C::OPB, oa[2], ob[2], fa0, fb0);
   mfma_frags<C, E>(fa1, fb1, acc);
-  __builtin_amdgcn_sched_barrier(0);
-  read_frags<C, E>(sa, sb, oa[3], ob[3], fa1, fb1);
+  interleave<NR, NM>();
+  read_frags<C, E>(st, st + C::OPB, oa[3], ob[3], fa1, fb1);
   mfma_frags<C, E>(fa0, fb0, acc);
-  __builtin_amdgcn_sched_barrier(0);
+  interleave<NR, NM>();
   mfma_frags<C, E>(fa1, fb1, acc);
   __builtin_amdgcn_sched_barrier(0);
 }
 
 __device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+template <typename T>
+struct Vec4;
+template <>
+struct Vec4<__bf16> { typedef bf16x4 T; };
+template <>
+struct Vec4<float> { typedef f32x4 T; };
+
+// Writes this wave's (WTM x WTN) result, held in acc, row-major to out
+// (leading dimension ld) through a private LDS region: acc-layout values go
+// to LDS, then whole 16-byte row pieces go to global memory.  Rows are
+// processed in passes that fit the region.
+template <class C, typename OUT>
+__device__ __forceinline__ void store_rows_via_lds(const f32x16 (&acc)[C::NBM][C::NBN], char* region,
+                                                   OUT* out, int64_t ld, int64_t row0, int64_t col0, int lane) {
+  constexpr int ESZ = int(sizeof(OUT));
+  constexpr int ROWB = C::WTN * ESZ;                   // bytes of one sub-tile row in LDS
+  constexpr int PASS = C::WAVE_LDS / ROWB < C::WTM ? C::WAVE_LDS / ROWB : C::WTM;
+  constexpr int CPR = ROWB / 16;                       // 16-byte pieces per row
+  constexpr int EPP = 16 / ESZ;                        // elements per piece
+  static_assert(PASS % 32 == 0 || PASS == C::WTM, "pass must hold whole MFMA blocks");
+#pragma unroll
+  for (int p0 = 0; p0 < C::WTM; p0 += PASS) {
+#pragma unroll
+    for (int i = 0; i < C::NBM; ++i) {
+      if (i * 32 < p0 || i * 32 >= p0 + PASS) continue;
+#pragma unroll
+      for (int j = 0; j < C::NBN; ++j)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          const int r = i * 32 + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3) - p0;
+          const int c = j * 32 + (lane & 31);
+          *reinterpret_cast<OUT*>(region + r * ROWB + c * ESZ) = to_e<OUT>(acc[i][j][q]);
+        }
+    }
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes have landed
+#pragma unroll
+    for (int it = 0; it < PASS * CPR / 64; ++it) {
+      const int piece = lane + 64 * it;
+      const int r = piece / CPR, pc = piece % CPR;
+      const f32x4 v = *reinterpret_cast<const f32x4*>(region + r * ROWB + pc * 16);
+      *reinterpret_cast<f32x4*>(out + (row0 + p0 + r) * ld + col0 + pc * EPP) = v;
+    }
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // reads done before the region is rewritten
+  }
+}
+
+// The wave's tile in "transposed" LDS layout: LDS row j (a column of the
+// output tile) holds the WTM values of that column, so a lane's 4
+// consecutive-row accumulator values are 8 (bf16) or 16 (fp32) contiguous
+// bytes.  16-byte pieces are XOR-swizzled with the row so that the 32 lanes
+// reading one piece column from 32 rows spread over the banks.
+template <class C, typename T, int MAXPASS = C::WTM>
+struct TLay {
+  static constexpr int ESZ = int(sizeof(T));
+  static constexpr int FIT = C::WAVE_LDS / (C::WTN * ESZ) < C::WTM ? C::WAVE_LDS / (C::WTN * ESZ) : C::WTM;
+  static constexpr int PASS = FIT < MAXPASS ? FIT : MAXPASS;
+  static constexpr int ROWB = PASS * ESZ;   // bytes of one LDS row in a pass
+  static constexpr int PPR = ROWB / 16;     // 16-byte pieces per row
+  static_assert(PASS % 32 == 0, "pass must hold whole MFMA blocks");
+  __device__ static __forceinline__ int off(int r, int byte) {
+    const int pc = byte >> 4;
+    return r * ROWB + ((pc ^ (r & (PPR < 16 ? PPR - 1 : 15))) << 4) + (byte & 15);
+  }
+};
+
+// Loads rows [col0, col0 + WTN) x columns [row0 + p0, row0 + p0 + PASS) of
+// src (leading dimension ld) into the wave's LDS region in TLay layout,
+// with 16-byte, full-line global reads.
+template <class L, class C, typename T>
+__device__ __forceinline__ void stage_t_in(char* region, const T* src, int64_t ld, int64_t row0, int64_t col0,
+                                           int p0, int lane) {
+  constexpr int N = C::WTN * L::PPR;
+  constexpr int EPP = 16 / L::ESZ;
+  static_assert(N % 64 == 0, "whole pieces per lane");
+#pragma unroll
+  for (int it = 0; it < N / 64; ++it) {
+    const int piece = lane + 64 * it;
+    const int r = piece / L::PPR, pc = piece % L::PPR;
+    const f32x4 v = *reinterpret_cast<const f32x4*>(src + (col0 + r) * ld + row0 + p0 + pc * EPP);
+    *reinterpret_cast<f32x4*>(region + L::off(r, pc * 16)) = v;
+  }
+}
+
+// Writes this wave's accumulator tile transposed: out[(col0 + j) * ld + row0
+// + i] = acc(i, j), through LDS in TLay layout and full-line 16-byte stores.
+template <class C, typename OUT>
+__device__ __forceinline__ void store_t_via_lds(const f32x16 (&acc)[C::NBM][C::NBN], char* region, OUT* out,
+                                                int64_t ld, int64_t row0, int64_t col0, int lane) {
+  using L = TLay<C, OUT>;
+  constexpr int N = C::WTN * L::PPR;
+  constexpr int EPP = 16 / L::ESZ;
+  static_assert(N % 64 == 0, "whole pieces per lane");
+#pragma unroll
+  for (int p0 = 0; p0 < C::WTM; p0 += L::PASS) {
+#pragma unroll
+    for (int i = 0; i < C::NBM; ++i) {
+      if (i * 32 < p0 || i * 32 >= p0 + L::PASS) continue;
+#pragma unroll
+      for (int j = 0; j < C::NBN; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int r = j * 32 + (lane & 31);
+          const int c = i * 32 + 8 * g + 4 * (lane >> 5) - p0;
+          const float v0 = acc[i][j][4 * g], v1 = acc[i][j][4 * g + 1];
+          const float v2 = acc[i][j][4 * g + 2], v3 = acc[i][j][4 * g + 3];
+          if constexpr (sizeof(OUT) == 2) {
+            bf16x4 x;
+            x[0] = __bf16(v0); x[1] = __bf16(v1); x[2] = __bf16(v2); x[3] = __bf16(v3);
+            *reinterpret_cast<bf16x4*>(region + L::off(r, c * 2)) = x;
+          } else {
+            *reinterpret_cast<f32x4*>(region + L::off(r, c * 4)) = f32x4{v0, v1, v2, v3};
+          }
+        }
+    }
+#pragma unroll
+    for (int it = 0; it < N / 64; ++it) {
+      const int piece = lane + 64 * it;
+      const int r = piece / L::PPR, pc = piece % L::PPR;
+      const f32x4 v = *reinterpret_cast<const f32x4*>(region + L::off(r, pc * 16));
+      *reinterpret_cast<f32x4*>(out + (col0 + r) * ld + row0 + p0 + pc * EPP) = v;
+    }
+  }
+}
 
 template <typename E, int TILE, int WGM, int WGN, int STAGE>
 __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) {
@@ -242,8 +381,10 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
   // K loop, two slabs per trip so that each stage buffer is addressed
   // statically.  The loads of slab k+1 are in flight while slab k is
   // multiplied; one barrier per slab publishes the landed stage and retires
-  // the one just read.  (No early exit inside the trip: a second loop exit
-  // would make the compiler copy the accumulators between register files.)
+  // the one just read, and the first fragments of the next slab are read
+  // right after it while the last MFMAs of the slab still drain.  (No early
+  // exit inside the trip: a second loop exit would make the compiler copy the
+  // accumulators between register files.)
   const int nk = int(K / C::BK);
   const E* srca = lane_src<C>(opa, K, wid, lane);
   const E* srcb = lane_src<C>(opb, K, wid, lane);
@@ -253,89 +394,116 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
     oa[ks] = frag_off(wm * C::WTM, lane, ks);
     ob[ks] = frag_off(wn * C::WTN, lane, ks);
   }
+  typename Frag<E>::T fa0[C::NBM], fb0[C::NBN], fa1[C::NBM], fb1[C::NBN];
   load_slab<C>(srca, K, 0, stage0, wid);
   load_slab<C>(srcb, K, 0, stage0 + C::OPB, wid);
   wait_vm_all();
   __syncthreads();
+  read_frags<C, E>(stage0, stage0 + C::OPB, oa[0], ob[0], fa0, fb0);
   int kt = 0;
   for (; kt + 2 <= nk; kt += 2) {
     load_slab<C>(srca, K, kt + 1, stage1, wid);
     load_slab<C>(srcb, K, kt + 1, stage1 + C::OPB, wid);
-    mma_slab<C, E>(stage0, stage0 + C::OPB, oa, ob, acc);
+    slab_body<C, E>(stage0, oa, ob, fa0, fb0, fa1, fb1, acc);
     wait_vm_all();
     __syncthreads();
+    read_frags<C, E>(stage1, stage1 + C::OPB, oa[0], ob[0], fa0, fb0);
+    __builtin_amdgcn_sched_barrier(0);
     if (kt + 2 < nk) {
       load_slab<C>(srca, K, kt + 2, stage0, wid);
       load_slab<C>(srcb, K, kt + 2, stage0 + C::OPB, wid);
     }
-    mma_slab<C, E>(stage1, stage1 + C::OPB, oa, ob, acc);
+    slab_body<C, E>(stage1, oa, ob, fa0, fb0, fa1, fb1, acc);
     wait_vm_all();
     __syncthreads();
+    if (kt + 2 < nk) read_frags<C, E>(stage0, stage0 + C::OPB, oa[0], ob[0], fa0, fb0);
+    __builtin_amdgcn_sched_barrier(0);
   }
-  if (kt < nk) mma_slab<C, E>(stage0, stage0 + C::OPB, oa, ob, acc);  // odd slab count: last slab is in stage 0
+  if (kt < nk) {  // odd slab count: the last slab is in stage 0
+    slab_body<C, E>(stage0, oa, ob, fa0, fb0, fa1, fb1, acc);
+    __syncthreads();
+  }
 
   // ---------------------------------------------------------------- epilogue
   // Accumulator element q of a 32x32 block sits at row 8*(q/4) + 4*(lane/32)
-  // + q%4 and column lane%32 of that block.
+  // + q%4 and column lane%32 of that block, so a lane holds 4 consecutive
+  // rows of one column.  The epilogue input comes from the transposed (X^T)
+  // or symmetric (A) copy and the outputs go out in both layouts; all three
+  // pass through the wave's private LDS region (the stages are free after
+  // the K loop), so that every global access is a full-line, 16-byte-per-lane
+  // row access.
   const float sc = args.first ? args.scale[d.slot] : 1.f;
+  const int64_t row0 = int64_t(ti) * TILE + wm * C::WTM;
+  const int64_t col0 = int64_t(tj) * TILE + wn * C::WTN;
+  char* region = (wid < C::NW / 2 ? stage0 : stage1) + (wid % (C::NW / 2)) * C::WAVE_LDS;
+  const E* in = nullptr;     // input read at the transposed position (X^T, or A which is symmetric)
+  E* out_t = nullptr;        // transposed output (leading dimension mp)
+  E* out_r = nullptr;        // row-major output
+  int64_t ld_r = mp;
+  bool rows_needed = true;
+  if (STAGE == ST_GRAM) {
+    out_t = reinterpret_cast<E*>(args.ws + d.a_off);
+    out_r = out_t;
+    rows_needed = ti != tj;  // a diagonal tile is complete with one store
+  } else if (STAGE == ST_POLY) {
+    in = reinterpret_cast<const E*>(args.ws + d.a_off);
+    out_t = reinterpret_cast<E*>(args.ws + d.b_off);
+    out_r = out_t;
+    rows_needed = ti != tj;
+  } else {
+    in = reinterpret_cast<const E*>(args.ws + d.xt_off[args.pin]);
+    out_t = reinterpret_cast<E*>(args.ws + d.xt_off[args.pin ^ 1]);
+    out_r = reinterpret_cast<E*>(args.ws + d.x_off[args.pin ^ 1]);
+    ld_r = np;
+  }
+  if (STAGE == ST_GRAM) {
+    const float s2 = sc * sc;
 #pragma unroll
-  for (int i = 0; i < C::NBM; ++i)
+    for (int i = 0; i < C::NBM; ++i)
 #pragma unroll
-    for (int j = 0; j < C::NBN; ++j)
+      for (int j = 0; j < C::NBN; ++j)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int64_t i0 = int64_t(ti) * TILE + wm * C::WTM + i * 32 + 8 * g + 4 * (lane >> 5);
-        const int64_t jc = int64_t(tj) * TILE + wn * C::WTN + j * 32 + (lane & 31);
-        float v0 = acc[i][j][4 * g + 0], v1 = acc[i][j][4 * g + 1];
-        float v2 = acc[i][j][4 * g + 2], v3 = acc[i][j][4 * g + 3];
-        if (STAGE == ST_GRAM) {
-          E* a = reinterpret_cast<E*>(args.ws + d.a_off);
-          const float s2 = sc * sc;
-          v0 *= s2; v1 *= s2; v2 *= s2; v3 *= s2;
-          a[(i0 + 0) * mp + jc] = to_e<E>(v0);
-          a[(i0 + 1) * mp + jc] = to_e<E>(v1);
-          a[(i0 + 2) * mp + jc] = to_e<E>(v2);
-          a[(i0 + 3) * mp + jc] = to_e<E>(v3);
-          if (ti != tj) store_vec4<E>(a + jc * mp + i0, v0, v1, v2, v3);
-        } else if (STAGE == ST_POLY) {
-          const E* a = reinterpret_cast<const E*>(args.ws + d.a_off);
-          E* b = reinterpret_cast<E*>(args.ws + d.b_off);
-          v0 = args.b * float(a[(i0 + 0) * mp + jc]) + args.c * v0;
-          v1 = args.b * float(a[(i0 + 1) * mp + jc]) + args.c * v1;
-          v2 = args.b * float(a[(i0 + 2) * mp + jc]) + args.c * v2;
-          v3 = args.b * float(a[(i0 + 3) * mp + jc]) + args.c * v3;
-          b[(i0 + 0) * mp + jc] = to_e<E>(v0);
-          b[(i0 + 1) * mp + jc] = to_e<E>(v1);
-          b[(i0 + 2) * mp + jc] = to_e<E>(v2);
-          b[(i0 + 3) * mp + jc] = to_e<E>(v3);
-          if (ti != tj) store_vec4<E>(b + jc * mp + i0, v0, v1, v2, v3);
-        } else {
-          const E* x = reinterpret_cast<const E*>(args.ws + d.x_off[args.pin]);
-          v0 = sc * (args.a * float(x[(i0 + 0) * np + jc]) + v0);
-          v1 = sc * (args.a * float(x[(i0 + 1) * np + jc]) + v1);
-          v2 = sc * (args.a * float(x[(i0 + 2) * np + jc]) + v2);
-          v3 = sc * (args.a * float(x[(i0 + 3) * np + jc]) + v3);
-          if (!args.last) {
-            E* xo = reinterpret_cast<E*>(args.ws + d.x_off[args.pin ^ 1]);
-            E* xto = reinterpret_cast<E*>(args.ws + d.xt_off[args.pin ^ 1]);
-            xo[(i0 + 0) * np + jc] = to_e<E>(v0);
-            xo[(i0 + 1) * np + jc] = to_e<E>(v1);
-            xo[(i0 + 2) * np + jc] = to_e<E>(v2);
-            xo[(i0 + 3) * np + jc] = to_e<E>(v3);
-            store_vec4<E>(xto + jc * mp + i0, v0, v1, v2, v3);
-          } else {
-            float* o = reinterpret_cast<float*>(args.ws + d.o_off);
-            if (!d.transposed) {
-              o[(i0 + 0) * np + jc] = v0;
-              o[(i0 + 1) * np + jc] = v1;
-              o[(i0 + 2) * np + jc] = v2;
-              o[(i0 + 3) * np + jc] = v3;
-            } else {
-              store_vec4<float>(o + jc * mp + i0, v0, v1, v2, v3);
+        for (int q = 0; q < 16; ++q) acc[i][j][q] *= s2;
+  } else {
+    // Row jc of X^T (or of A) holds the 4 consecutive rows a lane needs;
+    // the input tile is staged through LDS in passes of at most 64 rows,
+    // which bounds the registers held by the loads in flight.
+    using L = TLay<C, E, 64>;
+#pragma unroll
+    for (int p0 = 0; p0 < C::WTM; p0 += L::PASS) {
+      __builtin_amdgcn_sched_barrier(0);
+      stage_t_in<L, C, E>(region, in, mp, row0, col0, p0, lane);
+#pragma unroll
+      for (int i = 0; i < C::NBM; ++i) {
+        if (i * 32 < p0 || i * 32 >= p0 + L::PASS) continue;
+#pragma unroll
+        for (int j = 0; j < C::NBN; ++j)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const int r = j * 32 + (lane & 31);
+            const int c = i * 32 + 8 * g + 4 * (lane >> 5) - p0;
+            const typename Vec4<E>::T x =
+                *reinterpret_cast<const typename Vec4<E>::T*>(region + L::off(r, c * L::ESZ));
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const float v = acc[i][j][4 * g + q];
+              acc[i][j][4 * g + q] =
+                  STAGE == ST_POLY ? args.b * float(x[q]) + args.c * v : sc * (args.a * float(x[q]) + v);
             }
           }
-        }
       }
+    }
+  }
+  if (STAGE == ST_BX && args.last) {
+    float* o = reinterpret_cast<float*>(args.ws + d.o_off);
+    if (d.transposed)
+      store_t_via_lds<C, float>(acc, region, o, mp, row0, col0, lane);
+    else
+      store_rows_via_lds<C, float>(acc, region, o, np, row0, col0, lane);
+  } else {
+    store_t_via_lds<C, E>(acc, region, out_t, mp, row0, col0, lane);
+    if (rows_needed) store_rows_via_lds<C, E>(acc, region, out_r, ld_r, row0, col0, lane);
+  }
 }
 
 template <typename E, int TILE, int WGM, int WGN>

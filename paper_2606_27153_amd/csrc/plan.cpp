@@ -27,7 +27,10 @@ constexpr ClassInfo kClasses[KC_COUNT] = {
 
 // Relative throughput assumed for each class when choosing a tile: larger
 // tiles re-use each loaded byte more often.
-constexpr double kClassEfficiency[KC_COUNT] = {1.0, 0.8, 0.45, 1.0, 0.6};
+#ifndef MUON_EFF128
+#define MUON_EFF128 0.8
+#endif
+constexpr double kClassEfficiency[KC_COUNT] = {1.0, MUON_EFF128, 0.45, 1.0, 0.6};
 
 constexpr int64_t kDefaultWaveBytes = int64_t(12) << 30;  // 12 GiB
 constexpr int64_t kAlign = 256;
@@ -59,8 +62,13 @@ int32_t choose_class(int64_t m, int64_t n, const muon_plan_opts& o) {
 // the XCD owning it: blocks are dispatched round-robin over the 8 XCDs, so
 // block b runs on XCD b % 8.  Each XCD receives a contiguous range of the
 // grouped tile order and therefore shares operand panels in its own L2.
+#ifndef MUON_XCD_PERMUTE
+#define MUON_XCD_PERMUTE 0
+#endif
+
 void xcd_permute(std::vector<TileEntry>& tiles) {
   constexpr int64_t kXcd = 8;
+  if (!MUON_XCD_PERMUTE) return;
   const int64_t n = int64_t(tiles.size());
   if (n < 2 * kXcd) return;
   std::vector<TileEntry> out(tiles.size());
@@ -73,8 +81,12 @@ void xcd_permute(std::vector<TileEntry>& tiles) {
   tiles.swap(out);
 }
 
+#ifndef MUON_TILE_GROUP
+#define MUON_TILE_GROUP 4
+#endif
+
 void emit_full(std::vector<TileEntry>& t, int32_t mat, int64_t tm, int64_t tn) {
-  constexpr int64_t kGroup = 4;  // output row panels that advance together
+  constexpr int64_t kGroup = MUON_TILE_GROUP;  // output row panels that advance together
   for (int64_t g0 = 0; g0 < tm; g0 += kGroup) {
     const int64_t g1 = std::min(tm, g0 + kGroup);
     for (int64_t tj = 0; tj < tn; ++tj)
