@@ -64,6 +64,124 @@ def read_traffic(kernel_key: str):
         return None
 
 
+KERNEL_RE = [
+    # (regex on the mangled or plain kernel name, readable key)
+    (r"ns_gemm_kernelIDF16bLi256ELi2ELi4ELi0E", "gram:bf16_t256"),
+    (r"ns_gemm_kernelIDF16bLi256ELi2ELi4ELi1E", "poly:bf16_t256"),
+    (r"ns_gemm_kernelIDF16bLi256ELi2ELi4ELi2E", "bx:bf16_t256"),
+    (r"ns_gemm_kernelIDF16bLi128ELi2ELi2ELi0E", "gram:bf16_t128"),
+    (r"ns_gemm_kernelIDF16bLi128ELi2ELi2ELi1E", "poly:bf16_t128"),
+    (r"ns_gemm_kernelIDF16bLi128ELi2ELi2ELi2E", "bx:bf16_t128"),
+    (r"ns_gemm_kernelIDF16bLi64ELi2ELi2ELi0E", "gram:bf16_t64"),
+    (r"ns_gemm_kernelIDF16bLi64ELi2ELi2ELi1E", "poly:bf16_t64"),
+    (r"ns_gemm_kernelIDF16bLi64ELi2ELi2ELi2E", "bx:bf16_t64"),
+    (r"ns_gemm_kernelIfLi128ELi2ELi2ELi0E", "gram:f32_t128"),
+    (r"ns_gemm_kernelIfLi128ELi2ELi2ELi1E", "poly:f32_t128"),
+    (r"ns_gemm_kernelIfLi128ELi2ELi2ELi2E", "bx:f32_t128"),
+    (r"ns_gemm_kernelIfLi64ELi2ELi2ELi0E", "gram:f32_t64"),
+    (r"ns_gemm_kernelIfLi64ELi2ELi2ELi1E", "poly:f32_t64"),
+    (r"ns_gemm_kernelIfLi64ELi2ELi2ELi2E", "bx:f32_t64"),
+    (r"momentum_kernel", "momentum"),
+    (r"finalize_kernel", "finalize"),
+    (r"apply_kernel", "apply"),
+    (r"__amd_rocclr_copyBuffer", "copy (device copy)"),
+]
+
+
+def kernel_key(name: str) -> str:
+    import re
+    for pat, key in KERNEL_RE:
+        if re.search(pat, name):
+            return key
+    return "other: " + name[:60]
+
+
+def rocprof_summary(root: str) -> str:
+    """Markdown summary of rocprofv3 CSV output found under ``root``:
+    kernel statistics (--kernel-trace --stats) and per-dispatch FETCH_SIZE /
+    WRITE_SIZE counters (--pmc), scaled by the device-copy calibration."""
+    import csv
+    import glob
+    lines = []
+    for path in sorted(glob.glob(os.path.join(root, "**", "*kernel_stats.csv"), recursive=True)):
+        rows = list(csv.DictReader(open(path)))
+        agg = {}
+        for r in rows:
+            k = kernel_key(r["Name"])
+            a = agg.setdefault(k, [0, 0.0])
+            a[0] += int(r["Calls"])
+            a[1] += float(r["TotalDurationNs"])
+        total = sum(v[1] for v in agg.values())
+        lines += [f"### kernel statistics ({os.path.relpath(path, root)})", "",
+                  "| kernel | calls | total ms | mean ms | share |", "|---|---|---|---|---|"]
+        for k, (calls, ns) in sorted(agg.items(), key=lambda kv: -kv[1][1]):
+            lines.append(f"| {k} | {calls} | {ns / 1e6:.3f} | {ns / 1e6 / max(1, calls):.4f} | "
+                         f"{100 * ns / total:.1f}% |")
+        lines.append("")
+    counters = {}
+    for path in sorted(glob.glob(os.path.join(root, "**", "*counter_collection.csv"), recursive=True)):
+        for r in csv.DictReader(open(path)):
+            k = kernel_key(r["Kernel_Name"])
+            c = counters.setdefault(r["Counter_Name"], {}).setdefault(k, [0, 0.0])
+            c[0] += 1
+            c[1] += float(r["Counter_Value"])
+    if counters:
+        copy = "copy (device copy)"
+        lines += ["### HBM traffic per dispatch (rocprofv3 --pmc, KiB per dispatch)", ""]
+        cal = {}
+        for cname in ("FETCH_SIZE", "WRITE_SIZE"):
+            if cname in counters and copy in counters[cname]:
+                n, v = counters[cname][copy]
+                cal[cname] = v / n
+        lines.append(f"device-copy calibration (mean KiB per copy dispatch): {cal}")
+        lines += ["", "| kernel | counter | dispatches | mean KiB | mean GB |", "|---|---|---|---|---|"]
+        for cname, per in sorted(counters.items()):
+            for k, (n, v) in sorted(per.items()):
+                lines.append(f"| {k} | {cname} | {n} | {v / n:.0f} | {v / n * 1024 / 1e9:.4f} |")
+        lines.append("")
+    return "\n".join(lines)
+
+
+def write_traffic_summary(root: str, kernel: str, copy_mib: int, command: str) -> str:
+    """Writes profiles/traffic_summary.txt for ``kernel`` from the FETCH_SIZE
+    and WRITE_SIZE passes under ``root``.  Each counter is scaled by the
+    ratio of the known size of the calibration copy to what the same counter
+    read for it."""
+    import csv
+    import glob
+    per = {}
+    for path in sorted(glob.glob(os.path.join(root, "**", "*counter_collection.csv"), recursive=True)):
+        for r in csv.DictReader(open(path)):
+            k = kernel_key(r["Kernel_Name"])
+            c = per.setdefault(r["Counter_Name"], {}).setdefault(k, [0, 0.0])
+            c[0] += 1
+            c[1] += float(r["Counter_Value"])
+    known_kib = copy_mib * 1024.0
+    out = {}
+    for cname in ("FETCH_SIZE", "WRITE_SIZE"):
+        copy_total = per[cname]["copy (device copy)"][1]
+        factor = known_kib / copy_total
+        n, v = per[cname][kernel]
+        out[cname] = (v / n, factor)
+    total = sum(kib * f * 1024.0 for kib, f in out.values())
+    lines = [
+        "# HBM traffic of one launch of the dominant kernel (rocprofv3 --pmc, one counter per run)",
+        f"# command: {command}",
+        f"# FETCH_SIZE and WRITE_SIZE scaled by a {copy_mib} MiB device-to-device copy in the same run",
+        f"kernel = {kernel}",
+        f"sources_sha256_16 = {kernel_sources_hash()}",
+        f"fetch_kib_per_launch = {out['FETCH_SIZE'][0]:.0f}",
+        f"fetch_scale = {out['FETCH_SIZE'][1]:.4f}",
+        f"write_kib_per_launch = {out['WRITE_SIZE'][0]:.0f}",
+        f"write_scale = {out['WRITE_SIZE'][1]:.4f}",
+        f"hbm_bytes_per_launch = {total:.0f}",
+    ]
+    path = os.path.join(ROOT, "profiles", "traffic_summary.txt")
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    return path
+
+
 def cpu_baseline(wl, budget_s: float):
     """Times the fp64 oracle on one matrix per shape bucket and extrapolates
     to the whole set by bucket counts."""
@@ -119,7 +237,20 @@ def main(argv=None) -> int:
     ap.add_argument("--wave-bytes", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle time to sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="run one device-to-device copy of this size first (HBM counter calibration)")
+    ap.add_argument("--rocprof-summary", metavar="DIR", help="summarise rocprofv3 CSV output and exit")
+    ap.add_argument("--write-traffic", metavar="KERNEL",
+                    help="with --rocprof-summary: write profiles/traffic_summary.txt for this kernel key")
+    ap.add_argument("--traffic-command", default="", help="command recorded in the traffic summary")
     args = ap.parse_args(argv)
+
+    if args.rocprof_summary:
+        print(rocprof_summary(args.rocprof_summary))
+        if args.write_traffic:
+            print(write_traffic_summary(args.rocprof_summary, args.write_traffic, args.copy_calibration_mib or 1024,
+                                        args.traffic_command))
+        return 0
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the Muon step here runs on one GPU's matrices with no "
@@ -142,6 +273,15 @@ def main(argv=None) -> int:
     info = plan.info()
     log(f"[bench] plan: {info['n_waves']} waves, {info['n_buckets']} buckets, "
         f"{info['launches_per_step']} launches/step at max steps, workspace {info['workspace_bytes'] / 2**30:.2f} GiB")
+    if args.copy_calibration_mib > 0:
+        nb = args.copy_calibration_mib << 20
+        src = torch.ones(nb, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy of {nb} bytes done")
+        del src, dst
     params, moms = make_state(torch, wl, dev)
     grads = make_grads(torch, wl, 0, dev)
     ws = plan.workspace(dev)
@@ -201,7 +341,15 @@ def main(argv=None) -> int:
                 "frac": round(achieved / PEAK_HBM_GBS, 4)}
     roof["kernel"] = dom_key
     roof["mean_launch_ms"] = round(dom["total_ms"] / dom["launches"], 4)
-    roof["traffic"] = read_traffic(dom_key)
+    traffic = read_traffic(dom_key)
+    roof["traffic"] = None if traffic is None else round(traffic)
+    if dom["kind"] == "bx":
+        # algorithmic bytes of one B*X launch: read B and X once, write X' once (bf16)
+        launches_per_step = dom["launches"] / args.steps
+        alg = sum(2.0 * min(m.rows, m.cols) ** 2 + 4.0 * m.rows * m.cols for m in wl.matrices)
+        roof["algorithmic_bytes"] = round(alg * wl.ns_steps / launches_per_step)
+        if traffic is not None:
+            roof["traffic_vs_algorithmic"] = round(traffic / roof["algorithmic_bytes"], 2)
 
     floor_ms = (gemm_flops / (peak_mm * 1e12) + ew_bytes / (PEAK_HBM_GBS * 1e9)) * 1e3
     cpu = None

@@ -24,7 +24,7 @@ decay form, orientation) are listed in the design notes of the repository.
 Pins (tests/test_oracle_pins.py): SVD closed form U p^{ok}(s/||s||) V^T,
 transpose / sign / scale / orthogonal equivariance, rank-1 closed form,
 2x2 and 3x3 brute force against numpy.linalg.svd, the Gram-space identity of
-Eq. 3, the momentum closed form under constant gradients, the apply special
+Eq. 4, the momentum closed form under constant gradients, the apply special
 cases, and the bf16 rounding against torch's conversion.
 
 Every floating-point operation is fp64.  Narrowing to the stored dtype is a
@@ -137,7 +137,7 @@ def newton_schulz(x, steps: int, abc=QUINTIC_ABC):
 
 
 def newton_schulz_gram(x, steps: int, abc=QUINTIC_ABC):
-    """The same iteration carried in Gram space (Eq. 3).
+    """The same iteration carried in Gram space (Eq. 4).
 
     With G_0 = X_0 X_0^T and P_i = a I + b G_i + c G_i^2, the Gram matrix
     obeys G_{i+1} = P_i G_i P_i and X_k = P_{k-1} ... P_0 X_0.  In exact

@@ -3,7 +3,7 @@
 None of these re-types the oracle's iteration.  They compare it with the SVD
 closed form of Eq. 2 (each step maps a singular value x to
 p(x) = a x + b x^3 + c x^5), with brute force through numpy.linalg.svd, with
-the Gram-space recurrence of Eq. 3, with symmetry invariants, with the
+the Gram-space recurrence of Eq. 4, with symmetry invariants, with the
 closed form of the momentum recurrence under a constant gradient, and with
 torch's own bfloat16 conversion.  The last test plants mistakes in copies of
 the oracle and shows the pins catch each one.
