@@ -273,21 +273,26 @@ struct TLay {
 };
 
 // Loads rows [col0, col0 + WTN) x columns [row0 + p0, row0 + p0 + PASS) of
-// src (leading dimension ld) into the wave's LDS region in TLay layout,
-// with 16-byte, full-line global reads.
+// src (leading dimension ld) into the wave's LDS region in TLay layout with
+// direct-to-LDS 16-byte loads: instruction i fills LDS pieces 64*i .. 64*i+63
+// (lane l -> piece 64*i + l), so each lane fetches the logical piece that
+// the swizzle places in that slot.  Full-line global reads, no registers.
 template <class L, class C, typename T>
 __device__ __forceinline__ void stage_t_in(char* region, const T* src, int64_t ld, int64_t row0, int64_t col0,
                                            int p0, int lane) {
   constexpr int N = C::WTN * L::PPR;
   constexpr int EPP = 16 / L::ESZ;
+  constexpr int SW = L::PPR < 16 ? L::PPR - 1 : 15;
   static_assert(N % 64 == 0, "whole pieces per lane");
 #pragma unroll
   for (int it = 0; it < N / 64; ++it) {
     const int piece = lane + 64 * it;
-    const int r = piece / L::PPR, pc = piece % L::PPR;
-    const f32x4 v = *reinterpret_cast<const f32x4*>(src + (col0 + r) * ld + row0 + p0 + pc * EPP);
-    *reinterpret_cast<f32x4*>(region + L::off(r, pc * 16)) = v;
+    const int r = piece / L::PPR, phys = piece % L::PPR;
+    const int pc = phys ^ (r & SW);
+    const T* g = src + (col0 + r) * ld + row0 + p0 + pc * EPP;
+    __builtin_amdgcn_global_load_lds((gbl_void_t*)(g), (lds_void_t*)(region + it * 1024), 16, 0, 0);
   }
+  wait_vm_all();
 }
 
 // Writes this wave's accumulator tile transposed: out[(col0 + j) * ld + row0
@@ -466,12 +471,10 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
         for (int q = 0; q < 16; ++q) acc[i][j][q] *= s2;
   } else {
     // Row jc of X^T (or of A) holds the 4 consecutive rows a lane needs;
-    // the input tile is staged through LDS in passes of at most 64 rows,
-    // which bounds the registers held by the loads in flight.
-    using L = TLay<C, E, 64>;
+    // the input tile is staged through LDS.
+    using L = TLay<C, E>;
 #pragma unroll
     for (int p0 = 0; p0 < C::WTM; p0 += L::PASS) {
-      __builtin_amdgcn_sched_barrier(0);
       stage_t_in<L, C, E>(region, in, mp, row0, col0, p0, lane);
 #pragma unroll
       for (int i = 0; i < C::NBM; ++i) {

@@ -58,36 +58,40 @@ int32_t choose_class(int64_t m, int64_t n, const muon_plan_opts& o) {
   return best;
 }
 
-// Places logical tile i of a launch at the block index the hardware sends to
-// the XCD owning it: blocks are dispatched round-robin over the 8 XCDs, so
-// block b runs on XCD b % 8.  Each XCD receives a contiguous range of the
-// grouped tile order and therefore shares operand panels in its own L2.
-#ifndef MUON_XCD_PERMUTE
-#define MUON_XCD_PERMUTE 0
+#ifndef MUON_TILE_ORDER
+#define MUON_TILE_ORDER 1
 #endif
 
-void xcd_permute(std::vector<TileEntry>& tiles) {
-  constexpr int64_t kXcd = 8;
-  if (!MUON_XCD_PERMUTE) return;
-  const int64_t n = int64_t(tiles.size());
-  if (n < 2 * kXcd) return;
-  std::vector<TileEntry> out(tiles.size());
-  int64_t start = 0;
-  for (int64_t x = 0; x < kXcd; ++x) {
-    const int64_t cnt = (n - x + kXcd - 1) / kXcd;
-    for (int64_t i = 0; i < cnt; ++i) out[size_t(x + kXcd * i)] = tiles[size_t(start + i)];
-    start += cnt;
-  }
-  tiles.swap(out);
-}
-
-#ifndef MUON_TILE_GROUP
-#define MUON_TILE_GROUP 4
-#endif
-
+// Full tile list of one matrix (tm x tn output tiles) in dispatch order.
+//
+// Blocks are dispatched round-robin over the 8 XCDs (block b runs on XCD
+// b % 8), and about 256 of them (one per CU) run at a time.  Tiles are
+// taken in chunks of 8 row panels x up to 32 column panels; within a chunk
+// XCD x receives the 4 x W/4 sub-block at rows 4*(x%2), columns (x/2)*W/4.
+// The blocks running together thus read 8 + 32 operand panels chip-wide
+// (shared through the MALL) and 4 + 8 within each XCD's L2.  Chunks that do
+// not fit that pattern fall back to column-major order in groups of 4 rows.
 void emit_full(std::vector<TileEntry>& t, int32_t mat, int64_t tm, int64_t tn) {
-  constexpr int64_t kGroup = MUON_TILE_GROUP;  // output row panels that advance together
-  for (int64_t g0 = 0; g0 < tm; g0 += kGroup) {
+  int64_t g0 = 0;
+  if (MUON_TILE_ORDER == 1) {
+    for (; g0 + 8 <= tm; g0 += 8) {
+      for (int64_t c0 = 0; c0 < tn; c0 += 32) {
+        const int64_t w = std::min<int64_t>(32, tn - c0);
+        if (w % 4 != 0 || t.size() % 8 != 0) {
+          for (int64_t tj = c0; tj < c0 + w; ++tj)
+            for (int64_t ti = g0; ti < g0 + 8; ++ti) t.push_back(TileEntry{mat, uint16_t(ti), uint16_t(tj)});
+          continue;
+        }
+        for (int64_t b = 0; b < 8 * w; ++b) {
+          const int64_t x = b % 8, k = b / 8;
+          const int64_t r = 4 * (x % 2) + k % 4, c = (x / 2) * (w / 4) + k / 4;
+          t.push_back(TileEntry{mat, uint16_t(g0 + r), uint16_t(c0 + c)});
+        }
+      }
+    }
+  }
+  constexpr int64_t kGroup = 4;  // remaining row panels: column-major in groups of 4
+  for (; g0 < tm; g0 += kGroup) {
     const int64_t g1 = std::min(tm, g0 + kGroup);
     for (int64_t tj = 0; tj < tn; ++tj)
       for (int64_t ti = g0; ti < g1; ++ti) t.push_back(TileEntry{mat, uint16_t(ti), uint16_t(tj)});
@@ -298,8 +302,6 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
                           double(tm * (h.n_pad / tile)) * 2.0 * t2 * double(h.m_pad);
       }
       if (full.empty()) continue;
-      xcd_permute(lower);
-      xcd_permute(full);
       ClassLaunch cl{};
       cl.kclass = kc;
       cl.flops_gram = fg;

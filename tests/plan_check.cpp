@@ -1,0 +1,112 @@
+// Host-only checks of the planner (built with g++ from csrc/plan.cpp by
+// tests/test_plan_host.py).  Reads "rows cols" pairs from stdin, builds a
+// plan, and verifies: every matrix is in exactly one wave; each wave's
+// lower-triangular tile lists cover {(i, j): j <= i} and its full lists
+// cover every output tile of each of its matrices exactly once; workspace
+// regions inside a wave are 256-byte aligned and disjoint; the elementwise
+// tile prefix matches the matrices' tile counts.  Prints "OK" or the first
+// violation.
+#include <algorithm>
+#include <cstdio>
+#include <cstdlib>
+#include <map>
+#include <set>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "../paper_2606_27153_amd/csrc/muon_internal.h"
+
+using namespace muon;
+
+static int fail(const std::string& m) {
+  std::printf("FAIL %s\n", m.c_str());
+  return 1;
+}
+
+int main(int argc, char** argv) {
+  const int precision = argc > 1 ? std::atoi(argv[1]) : 0;
+  const long long wave_bytes = argc > 2 ? std::atoll(argv[2]) : 0;
+  std::vector<muon_matrix_desc> descs;
+  long long r, c;
+  while (std::scanf("%lld %lld", &r, &c) == 2) descs.push_back(muon_matrix_desc{r, c, MUON_BF16, MUON_BF16, MUON_F32, 0});
+  muon_plan_opts o{};
+  o.precision = precision;
+  o.max_ns_steps = 16;
+  o.a = 3.4445f;
+  o.b = -4.775f;
+  o.c = 2.0315f;
+  o.eps = 1e-7f;
+  o.small_m_threshold = 64;
+  o.wave_bytes = wave_bytes;
+  Plan p;
+  std::string err;
+  if (build_plan(descs.data(), int32_t(descs.size()), o, p, err) != MUON_OK) return fail("build_plan: " + err);
+  std::vector<int> seen(descs.size(), 0);
+  for (size_t wi = 0; wi < p.waves.size(); ++wi) {
+    const WaveHost& w = p.waves[wi];
+    std::vector<std::pair<long long, long long>> regions;
+    long long ew = 0;
+    for (int s = 0; s < w.count; ++s) {
+      const int idx = p.order[size_t(w.first + s)];
+      const MatHost& h = p.mats[size_t(idx)];
+      seen[size_t(idx)]++;
+      if (h.wave != int(wi) || h.slot != s) return fail("wave/slot bookkeeping");
+      const MatDev& d = p.h_matdev[size_t(w.first + s)];
+      if (d.index != idx) return fail("descriptor index");
+      if (p.h_prefix[size_t(w.prefix_off + s)] != ew) return fail("ew prefix");
+      ew += h.ew_tiles;
+      const long long esz = h.fp32_ns ? 4 : 2;
+      const long long xb = h.m_pad * h.n_pad * esz;
+      const long long ab = h.m_pad * h.m_pad * esz;
+      const std::pair<long long, long long> rs[] = {
+          {h.x_off[0], xb}, {h.x_off[1], xb}, {h.xt_off[0], xb}, {h.xt_off[1], xb},
+          {h.a_off, ab},    {h.b_off, ab},    {h.o_off, h.m_pad * h.n_pad * 4}, {h.partial_off, h.ew_tiles * 4}};
+      for (const auto& rg : rs) {
+        if (rg.first % 256 != 0) return fail("unaligned region");
+        regions.push_back(rg);
+      }
+    }
+    if (p.h_prefix[size_t(w.prefix_off + w.count)] != ew || ew != w.ew_tiles) return fail("ew total");
+    regions.push_back({w.scale_off, w.count * 4});
+    regions.push_back({w.flag_off, w.count * 4});
+    std::sort(regions.begin(), regions.end());
+    for (size_t i = 0; i < regions.size(); ++i) {
+      if (i + 1 < regions.size() && regions[i].first + regions[i].second > regions[i + 1].first)
+        return fail("overlapping workspace regions");
+      if (regions[i].first + regions[i].second > w.ws_bytes) return fail("region past wave end");
+    }
+    if (w.ws_bytes > p.ws_bytes) return fail("wave larger than plan workspace");
+    for (const ClassLaunch& cl : w.launches) {
+      const int tile = class_info(cl.kclass).tile;
+      std::map<int, std::set<std::pair<int, int>>> lower, full;
+      for (int t = 0; t < cl.n_lower; ++t) {
+        const TileEntry& e = p.h_tiles[size_t(cl.lower_off + t)];
+        if (!lower[e.mat].insert({e.ti, e.tj}).second) return fail("duplicate lower tile");
+      }
+      for (int t = 0; t < cl.n_full; ++t) {
+        const TileEntry& e = p.h_tiles[size_t(cl.full_off + t)];
+        if (!full[e.mat].insert({e.ti, e.tj}).second) return fail("duplicate full tile");
+      }
+      for (int s = 0; s < w.count; ++s) {
+        const int pos = w.first + s;
+        const MatHost& h = p.mats[size_t(p.order[size_t(pos)])];
+        if (h.kclass != cl.kclass) {
+          if (lower.count(pos) || full.count(pos)) return fail("tile of another class");
+          continue;
+        }
+        const int tm = int(h.m_pad / tile), tn = int(h.n_pad / tile);
+        if (int(full[pos].size()) != tm * tn) return fail("full tile count");
+        if (int(lower[pos].size()) != tm * (tm + 1) / 2) return fail("lower tile count");
+        for (const auto& t : full[pos])
+          if (t.first >= tm || t.second >= tn) return fail("full tile out of range");
+        for (const auto& t : lower[pos])
+          if (t.first >= tm || t.second > t.first) return fail("lower tile out of range");
+      }
+    }
+  }
+  for (size_t i = 0; i < seen.size(); ++i)
+    if (seen[i] != 1) return fail("matrix not in exactly one wave");
+  std::printf("OK %zu matrices %zu waves %zu tiles\n", descs.size(), p.waves.size(), p.h_tiles.size());
+  return 0;
+}
