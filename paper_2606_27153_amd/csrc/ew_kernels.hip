@@ -2,8 +2,8 @@
 //
 //  momentum_kernel  one pass over G and M: M <- mu*M + G, the Nesterov input
 //                   u = G + mu*M, a per-tile sum of u^2, and u stored as the
-//                   NS operand in both layouts (stored and transposed), so the
-//                   Gram and B*X products can both read K-contiguous rows.
+//                   oriented NS operand X (transposed through LDS for a tall
+//                   matrix); the fp32 classes also keep X^T.
 //  finalize_kernel  per matrix, a fixed-order sum of the tile partials and the
 //                   Frobenius scale 1 / (||u||_F + eps) (deterministic; no
 //                   float atomics).  A zero sum marks the matrix as skipped.
@@ -100,9 +100,11 @@ __global__ __launch_bounds__(256) void momentum_kernel(const MatDev* __restrict_
   const int r0 = tr * EW_TILE, c0 = tc * EW_TILE;
   const int rows = d.rows, cols = d.cols;
   const bool vec = (cols & 3) == 0;
-  // Stored-layout and transposed operand buffers of ping-pong pair 0.
-  char* ubuf = ws + (d.transposed ? d.xt_off[0] : d.x_off[0]);
-  char* utbuf = ws + (d.transposed ? d.x_off[0] : d.xt_off[0]);
+  // Stored-layout and transposed operand buffers of ping-pong pair 0: X is
+  // the stored layout for a wide matrix and the transposed one for a tall
+  // matrix.  X^T exists only for the fp32 classes (null otherwise).
+  char* ubuf = d.transposed ? (d.x_f32 ? ws + d.xt_off[0] : nullptr) : ws + d.x_off[0];
+  char* utbuf = d.transposed ? ws + d.x_off[0] : (d.x_f32 ? ws + d.xt_off[0] : nullptr);
 
   float ss = 0.f;
 #pragma unroll
@@ -127,18 +129,20 @@ __global__ __launch_bounds__(256) void momentum_kernel(const MatDev* __restrict_
       }
       store4(pe.mom, idx, MUON_F32, vec, valid, m);
     }
-    store_x4(ubuf, int64_t(r) * d.cols_pad + c, d.x_f32, u);
+    if (ubuf) store_x4(ubuf, int64_t(r) * d.cols_pad + c, d.x_f32, u);
 #pragma unroll
     for (int e = 0; e < 4; ++e) tile_t[rl][4 * cg + e] = u[e];
   }
   __syncthreads();
+  if (utbuf) {
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int oc = rr + 16 * q;   // stored column = row of the transposed buffer
-    float v[4];
+    for (int q = 0; q < 4; ++q) {
+      const int oc = rr + 16 * q;   // stored column = row of the transposed buffer
+      float v[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) v[e] = tile_t[4 * cg + e][oc];
-    store_x4(utbuf, int64_t(c0 + oc) * d.rows_pad + r0 + 4 * cg, d.x_f32, v);
+      for (int e = 0; e < 4; ++e) v[e] = tile_t[4 * cg + e][oc];
+      store_x4(utbuf, int64_t(c0 + oc) * d.rows_pad + r0 + 4 * cg, d.x_f32, v);
+    }
   }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
@@ -191,7 +195,10 @@ __global__ __launch_bounds__(256) void apply_kernel(const MatDev* __restrict__ m
   const float sc = scale[s];
   const float lrs = lr * sqrtf(fmaxf(1.f, float(rows) / float(cols)));
   const char* obuf = ws + d.o_off;
-  const char* ubuf = ws + (d.transposed ? d.xt_off[0] : d.x_off[0]);
+  // ns_steps == 0: O = s*u, read from X (transposed for a tall bf16 matrix,
+  // whose stored-layout copy does not exist) or from the fp32 X^T.
+  const bool u_transposed = d.transposed && !d.x_f32;
+  const char* ubuf = ws + (d.transposed && d.x_f32 ? d.xt_off[0] : d.x_off[0]);
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int r = tr * EW_TILE + rr + 16 * q;
@@ -207,9 +214,13 @@ __global__ __launch_bounds__(256) void apply_kernel(const MatDev* __restrict__ m
       } else if (d.x_f32) {
         const f32x4 x = *reinterpret_cast<const f32x4*>(reinterpret_cast<const float*>(ubuf) + pidx);
         o[0] = sc * x[0]; o[1] = sc * x[1]; o[2] = sc * x[2]; o[3] = sc * x[3];
-      } else {
+      } else if (!u_transposed) {
         const bf16x4 x = *reinterpret_cast<const bf16x4*>(reinterpret_cast<const __bf16*>(ubuf) + pidx);
         o[0] = sc * float(x[0]); o[1] = sc * float(x[1]); o[2] = sc * float(x[2]); o[3] = sc * float(x[3]);
+      } else {
+        const __bf16* xb = reinterpret_cast<const __bf16*>(ubuf);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = sc * float(xb[int64_t(c + e) * d.rows_pad + r]);
       }
     }
     const int64_t idx = int64_t(r) * cols + c;

@@ -41,7 +41,7 @@ constexpr int32_t EW_TILE = 64;
 // offsets into the caller's workspace.
 struct MatDev {
   int64_t x_off[2];    // oriented X, m_pad x n_pad (ping-pong pair p)
-  int64_t xt_off[2];   // X^T, n_pad x m_pad
+  int64_t xt_off[2];   // X^T, n_pad x m_pad (fp32 classes only; -1 otherwise)
   int64_t a_off;       // Gram A, m_pad x m_pad
   int64_t b_off;       // polynomial B, m_pad x m_pad
   int64_t o_off;       // fp32 O in stored layout, rows_pad x cols_pad

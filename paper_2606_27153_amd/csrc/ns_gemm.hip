@@ -83,18 +83,19 @@ __device__ __forceinline__ void store_vec4<float>(float* p, float v0, float v1, 
 }
 
 // Compile-time shape of one GEMM configuration.
-template <typename E, int TILE, int WGM, int WGN>
+template <typename E, int TILE_, int WGM, int WGN>
 struct Cfg {
+  static constexpr int TILE = TILE_;
   static constexpr int NW = WGM * WGN;            // waves per block
   static constexpr int NT = NW * 64;              // threads per block
   static constexpr int EPC = 16 / int(sizeof(E));  // elements per 16-byte chunk
   static constexpr int BK = 8 * EPC;              // elements per 128-byte K slab
-  static constexpr int WTM = TILE / WGM, WTN = TILE / WGN;  // wave tile
+  static constexpr int WTM = TILE_ / WGM, WTN = TILE_ / WGN;  // wave tile
   static constexpr int NBM = WTM / 32, NBN = WTN / 32;      // 32x32 MFMA blocks per wave
-  static constexpr int OPB = TILE * 128;          // LDS bytes of one operand slab
-  static constexpr int CPW = TILE / 8 / NW;       // 1 KB LDS chunks per wave per operand
+  static constexpr int OPB = TILE_ * 128;          // LDS bytes of one operand slab
+  static constexpr int CPW = TILE_ / 8 / NW;       // 1 KB LDS chunks per wave per operand
   static constexpr int WAVE_LDS = 4 * OPB / NW;   // LDS bytes per wave for the epilogue
-  static_assert(CPW >= 1 && TILE / 8 % NW == 0, "tile too small for the block");
+  static_assert(CPW >= 1 && TILE_ / 8 % NW == 0, "tile too small for the block");
 };
 
 // Direct-to-LDS loads of one operand slab.  global_load_lds_dwordx4 writes
@@ -216,7 +217,9 @@ struct Vec4<float> { typedef f32x4 T; };
 
 // Writes this wave's (WTM x WTN) result, held in acc, row-major to out
 // (leading dimension ld) through a private LDS region: acc-layout values go
-// to LDS, then whole 16-byte row pieces go to global memory.  Rows are
+// to LDS, then whole 16-byte row pieces go to global memory with
+// non-temporal stores (full lines; the outputs are far larger than the
+// caches and would otherwise evict operand panels other blocks still read).  Rows are
 // processed in passes that fit the region.
 template <class C, typename OUT>
 __device__ __forceinline__ void store_rows_via_lds(const f32x16 (&acc)[C::NBM][C::NBN], char* region,
@@ -247,7 +250,7 @@ __device__ __forceinline__ void store_rows_via_lds(const f32x16 (&acc)[C::NBM][C
       const int piece = lane + 64 * it;
       const int r = piece / CPR, pc = piece % CPR;
       const f32x4 v = *reinterpret_cast<const f32x4*>(region + r * ROWB + pc * 16);
-      *reinterpret_cast<f32x4*>(out + (row0 + p0 + r) * ld + col0 + pc * EPP) = v;
+      __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(out + (row0 + p0 + r) * ld + col0 + pc * EPP));
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);  // reads done before the region is rewritten
   }
@@ -331,14 +334,148 @@ __device__ __forceinline__ void store_t_via_lds(const f32x16 (&acc)[C::NBM][C::N
       const int piece = lane + 64 * it;
       const int r = piece / L::PPR, pc = piece % L::PPR;
       const f32x4 v = *reinterpret_cast<const f32x4*>(region + L::off(r, pc * 16));
-      *reinterpret_cast<f32x4*>(out + (col0 + r) * ld + row0 + p0 + pc * EPP) = v;
+      __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(out + (col0 + r) * ld + row0 + p0 + pc * EPP));
     }
   }
+}
+
+// ---------------------------------------------------------------------------
+// bf16 B*X reads its second operand straight from row-major X.  The slab of
+// X (64 K-rows x TILE columns) sits in LDS row-major; ds_read_b64_tr_b16
+// then assembles the MFMA operand: within each 16-lane group, if lane j
+// points at 4 consecutive elements S[j][0..3], lane i receives
+// S[4e + i/4][i%4] for e = 0..3.  Pointing lane j at row k0 + j/4, columns
+// c0 + 4*(j%4) .. +3 therefore hands lane i the 4 consecutive K values
+// k0..k0+3 of column c0 + i; two such reads give the 8 K values of a
+// 32x32x16 operand fragment, in the same K order as the row-operand
+// fragments.  32-byte segments of each LDS row are XOR-swizzled with the
+// row so that the 4 rows one 16-lane group touches fall in different banks.
+// ---------------------------------------------------------------------------
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ i16x4 lds_tr16(const char* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p));
+}
+
+// Segment swizzle for row-major LDS rows of ROWB bytes.
+template <int ROWB>
+__device__ __forceinline__ int seg_swz(int row) {
+  constexpr int RPW = ROWB >= 256 ? 1 : 256 / ROWB;        // rows per 256-byte bank window
+  constexpr int SEGW = ROWB / 32 < 8 ? ROWB / 32 : 8;      // swizzle span in segments
+  return (row / RPW) & (SEGW - 1);
+}
+
+// Per-lane source of the direct-to-LDS loads of a row-major X slab: the
+// wave's chunk q covers rows q*RPC .. q*RPC + RPC - 1 (RPC = 1024 / ROWB);
+// lane l fills 16-byte slot l of the chunk, i.e. row l / LPR, slot l % LPR,
+// and fetches the logical segment the swizzle stores there.  Across the
+// wave's chunks (q + NW*i) the swizzle of a lane's row is unchanged.
+template <class C>
+__device__ __forceinline__ const __bf16* lane_src_rows(const __bf16* xcol, int64_t ld, int wid, int lane) {
+  constexpr int ROWB = C::TILE * 2, RPC = 1024 / ROWB, LPR = ROWB / 16;
+  const int row = wid * RPC + lane / LPR;
+  const int slot = lane % LPR;
+  const int seg = (slot >> 1) ^ seg_swz<ROWB>(row);
+  return xcol + int64_t(row) * ld + seg * 16 + (slot & 1) * 8;
+}
+
+template <class C>
+__device__ __forceinline__ void load_slab_rows(const __bf16* src, int64_t ld, int kt, char* lds, int wid) {
+  constexpr int ROWB = C::TILE * 2, RPC = 1024 / ROWB;
+#pragma unroll
+  for (int i = 0; i < C::CPW; ++i) {
+    const __bf16* g = src + int64_t(i) * (RPC * C::NW) * ld + int64_t(kt) * 64 * ld;
+    __builtin_amdgcn_global_load_lds((gbl_void_t*)(g), (lds_void_t*)(lds + (wid + C::NW * i) * 1024), 16, 0, 0);
+  }
+}
+
+// Per-lane byte offsets (within a slab, K sub-step 0) of the two transposing
+// reads that make column block jb's operand fragment.
+template <class C>
+__device__ __forceinline__ void tr_offsets(int wn, int lane, int (&ot)[2 * C::NBN]) {
+  constexpr int ROWB = C::TILE * 2;
+  const int h = lane >> 5, g = (lane >> 4) & 1, i = lane & 15;
+#pragma unroll
+  for (int jb = 0; jb < C::NBN; ++jb)
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+      const int row = 8 * h + 4 * r + (i >> 2);
+      const int seg = (wn * C::WTN) / 16 + 2 * jb + g;
+      ot[2 * jb + r] = row * ROWB + ((seg ^ seg_swz<ROWB>(row)) << 5) + 8 * (i & 3);
+    }
+}
+
+template <class C>
+__device__ __forceinline__ void read_frags_tr(const char* sa, const char* sb, int oa, const int (&ot)[2 * C::NBN],
+                                              int ks, bf16x8 (&fa)[C::NBM], bf16x8 (&fb)[C::NBN]) {
+  constexpr int KSB = 16 * C::TILE * 2;  // bytes of 16 K-rows
+#pragma unroll
+  for (int i = 0; i < C::NBM; ++i) fa[i] = *reinterpret_cast<const bf16x8*>(sa + oa + i * 4096);
+#pragma unroll
+  for (int j = 0; j < C::NBN; ++j) {
+    const i16x4 lo = lds_tr16(sb + ot[2 * j] + ks * KSB);
+    const i16x4 hi = lds_tr16(sb + ot[2 * j + 1] + ks * KSB);
+    const i16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    fb[j] = __builtin_bit_cast(bf16x8, v);
+  }
+}
+
+template <class C>
+__device__ __forceinline__ void slab_body_tr(const char* st, const int (&oa)[4], const int (&ot)[2 * C::NBN],
+                                             bf16x8 (&fa0)[C::NBM], bf16x8 (&fb0)[C::NBN], bf16x8 (&fa1)[C::NBM],
+                                             bf16x8 (&fb1)[C::NBN], f32x16 (&acc)[C::NBM][C::NBN]) {
+  constexpr int NR = C::NBM + 2 * C::NBN;
+  constexpr int NM = C::NBM * C::NBN;
+  read_frags_tr<C>(st, st + C::OPB, oa[1], ot, 1, fa1, fb1);
+  mfma_frags<C, __bf16>(fa0, fb0, acc);
+  interleave<NR, NM>();
+  read_frags_tr<C>(st, st + C::OPB, oa[2], ot, 2, fa0, fb0);
+  mfma_frags<C, __bf16>(fa1, fb1, acc);
+  interleave<NR, NM>();
+  read_frags_tr<C>(st, st + C::OPB, oa[3], ot, 3, fa1, fb1);
+  mfma_frags<C, __bf16>(fa0, fb0, acc);
+  interleave<NR, NM>();
+  mfma_frags<C, __bf16>(fa1, fb1, acc);
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// Stages the wave's (WTM x WTN) tile of row-major src (rows row0.., columns
+// col0..) into its LDS region, row-major and segment-swizzled, with
+// direct-to-LDS loads; lane l of instruction it fills 16-byte slot 64*it + l.
+template <class C>
+__device__ __forceinline__ void stage_rows_in(char* region, const __bf16* src, int64_t ld, int64_t row0,
+                                              int64_t col0, int lane) {
+  constexpr int ROWB = C::WTN * 2, LPR = ROWB / 16;
+  constexpr int N = C::WTM * LPR;
+  static_assert(N % 64 == 0, "whole slots per lane");
+#pragma unroll
+  for (int it = 0; it < N / 64; ++it) {
+    const int slot = 64 * it + lane;
+    const int row = slot / LPR, s16 = slot % LPR;
+    const int seg = (s16 >> 1) ^ seg_swz<ROWB>(row);
+    const __bf16* g = src + (row0 + row) * ld + col0 + seg * 16 + (s16 & 1) * 8;
+    __builtin_amdgcn_global_load_lds((gbl_void_t*)(g), (lds_void_t*)(region + it * 1024), 16, 0, 0);
+  }
+  wait_vm_all();
+}
+
+// Reads, in accumulator layout, the 4 consecutive rows i0..i0+3 of column j
+// of the tile staged by stage_rows_in (block i, j, group g).
+template <class C>
+__device__ __forceinline__ i16x4 read_rows_tr(const char* region, int i, int j, int g, int lane) {
+  constexpr int ROWB = C::WTN * 2;
+  const int jj = lane & 15;
+  const int row = 32 * i + 8 * g + 4 * (lane >> 5) + (jj >> 2);
+  const int seg = 2 * j + ((lane >> 4) & 1);
+  return lds_tr16(region + row * ROWB + ((seg ^ seg_swz<ROWB>(row)) << 5) + 8 * (jj & 3));
 }
 
 template <typename E, int TILE, int WGM, int WGN, int STAGE>
 __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) {
   using C = Cfg<E, TILE, WGM, WGN>;
+  // bf16 B*X takes its second operand from row-major X via transposing reads
+  constexpr bool TRB = STAGE == ST_BX && sizeof(E) == 2;
   // Two LDS stages as distinct objects, so that the loads in flight into one
   // stage are known not to alias the reads of the other.
   __shared__ __attribute__((aligned(1024))) char stage0[2 * C::OPB];
@@ -369,10 +506,14 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
     opb = a + int64_t(tj) * TILE * K;
   } else {
     const E* b = reinterpret_cast<const E*>(args.ws + d.b_off);
-    const E* xt = reinterpret_cast<const E*>(args.ws + d.xt_off[args.pin]);
     K = mp;
     opa = b + int64_t(ti) * TILE * K;
-    opb = xt + int64_t(tj) * TILE * K;
+    if (TRB) {
+      // columns tj*TILE.. of row-major X (m_pad x n_pad)
+      opb = reinterpret_cast<const E*>(args.ws + d.x_off[args.pin]) + int64_t(tj) * TILE;
+    } else {
+      opb = reinterpret_cast<const E*>(args.ws + d.xt_off[args.pin]) + int64_t(tj) * TILE * K;
+    }
   }
 
   f32x16 acc[C::NBM][C::NBN];
@@ -391,42 +532,80 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
   // exit inside the trip: a second loop exit would make the compiler copy the
   // accumulators between register files.)
   const int nk = int(K / C::BK);
-  const E* srca = lane_src<C>(opa, K, wid, lane);
-  const E* srcb = lane_src<C>(opb, K, wid, lane);
-  int oa[4], ob[4];
+  if constexpr (TRB) {
+    const E* srca = lane_src<C>(opa, K, wid, lane);
+    const __bf16* srcb = lane_src_rows<C>(reinterpret_cast<const __bf16*>(opb), np, wid, lane);
+    int oa[4], ot[2 * C::NBN];
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) {
-    oa[ks] = frag_off(wm * C::WTM, lane, ks);
-    ob[ks] = frag_off(wn * C::WTN, lane, ks);
-  }
-  typename Frag<E>::T fa0[C::NBM], fb0[C::NBN], fa1[C::NBM], fb1[C::NBN];
-  load_slab<C>(srca, K, 0, stage0, wid);
-  load_slab<C>(srcb, K, 0, stage0 + C::OPB, wid);
-  wait_vm_all();
-  __syncthreads();
-  read_frags<C, E>(stage0, stage0 + C::OPB, oa[0], ob[0], fa0, fb0);
-  int kt = 0;
-  for (; kt + 2 <= nk; kt += 2) {
-    load_slab<C>(srca, K, kt + 1, stage1, wid);
-    load_slab<C>(srcb, K, kt + 1, stage1 + C::OPB, wid);
-    slab_body<C, E>(stage0, oa, ob, fa0, fb0, fa1, fb1, acc);
+    for (int ks = 0; ks < 4; ++ks) oa[ks] = frag_off(wm * C::WTM, lane, ks);
+    tr_offsets<C>(wn, lane, ot);
+    bf16x8 fa0[C::NBM], fb0[C::NBN], fa1[C::NBM], fb1[C::NBN];
+    load_slab<C>(srca, K, 0, stage0, wid);
+    load_slab_rows<C>(srcb, np, 0, stage0 + C::OPB, wid);
     wait_vm_all();
     __syncthreads();
-    read_frags<C, E>(stage1, stage1 + C::OPB, oa[0], ob[0], fa0, fb0);
-    __builtin_amdgcn_sched_barrier(0);
-    if (kt + 2 < nk) {
-      load_slab<C>(srca, K, kt + 2, stage0, wid);
-      load_slab<C>(srcb, K, kt + 2, stage0 + C::OPB, wid);
+    read_frags_tr<C>(stage0, stage0 + C::OPB, oa[0], ot, 0, fa0, fb0);
+    int kt = 0;
+    for (; kt + 2 <= nk; kt += 2) {
+      load_slab<C>(srca, K, kt + 1, stage1, wid);
+      load_slab_rows<C>(srcb, np, kt + 1, stage1 + C::OPB, wid);
+      slab_body_tr<C>(stage0, oa, ot, fa0, fb0, fa1, fb1, acc);
+      wait_vm_all();
+      __syncthreads();
+      read_frags_tr<C>(stage1, stage1 + C::OPB, oa[0], ot, 0, fa0, fb0);
+      __builtin_amdgcn_sched_barrier(0);
+      if (kt + 2 < nk) {
+        load_slab<C>(srca, K, kt + 2, stage0, wid);
+        load_slab_rows<C>(srcb, np, kt + 2, stage0 + C::OPB, wid);
+      }
+      slab_body_tr<C>(stage1, oa, ot, fa0, fb0, fa1, fb1, acc);
+      wait_vm_all();
+      __syncthreads();
+      if (kt + 2 < nk) read_frags_tr<C>(stage0, stage0 + C::OPB, oa[0], ot, 0, fa0, fb0);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    slab_body<C, E>(stage1, oa, ob, fa0, fb0, fa1, fb1, acc);
+    if (kt < nk) {  // odd slab count: the last slab is in stage 0
+      slab_body_tr<C>(stage0, oa, ot, fa0, fb0, fa1, fb1, acc);
+      __syncthreads();
+    }
+  } else {
+    const E* srca = lane_src<C>(opa, K, wid, lane);
+    const E* srcb = lane_src<C>(opb, K, wid, lane);
+    int oa[4], ob[4];
+  #pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      oa[ks] = frag_off(wm * C::WTM, lane, ks);
+      ob[ks] = frag_off(wn * C::WTN, lane, ks);
+    }
+    typename Frag<E>::T fa0[C::NBM], fb0[C::NBN], fa1[C::NBM], fb1[C::NBN];
+    load_slab<C>(srca, K, 0, stage0, wid);
+    load_slab<C>(srcb, K, 0, stage0 + C::OPB, wid);
     wait_vm_all();
     __syncthreads();
-    if (kt + 2 < nk) read_frags<C, E>(stage0, stage0 + C::OPB, oa[0], ob[0], fa0, fb0);
-    __builtin_amdgcn_sched_barrier(0);
-  }
-  if (kt < nk) {  // odd slab count: the last slab is in stage 0
-    slab_body<C, E>(stage0, oa, ob, fa0, fb0, fa1, fb1, acc);
-    __syncthreads();
+    read_frags<C, E>(stage0, stage0 + C::OPB, oa[0], ob[0], fa0, fb0);
+    int kt = 0;
+    for (; kt + 2 <= nk; kt += 2) {
+      load_slab<C>(srca, K, kt + 1, stage1, wid);
+      load_slab<C>(srcb, K, kt + 1, stage1 + C::OPB, wid);
+      slab_body<C, E>(stage0, oa, ob, fa0, fb0, fa1, fb1, acc);
+      wait_vm_all();
+      __syncthreads();
+      read_frags<C, E>(stage1, stage1 + C::OPB, oa[0], ob[0], fa0, fb0);
+      __builtin_amdgcn_sched_barrier(0);
+      if (kt + 2 < nk) {
+        load_slab<C>(srca, K, kt + 2, stage0, wid);
+        load_slab<C>(srcb, K, kt + 2, stage0 + C::OPB, wid);
+      }
+      slab_body<C, E>(stage1, oa, ob, fa0, fb0, fa1, fb1, acc);
+      wait_vm_all();
+      __syncthreads();
+      if (kt + 2 < nk) read_frags<C, E>(stage0, stage0 + C::OPB, oa[0], ob[0], fa0, fb0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (kt < nk) {  // odd slab count: the last slab is in stage 0
+      slab_body<C, E>(stage0, oa, ob, fa0, fb0, fa1, fb1, acc);
+      __syncthreads();
+    }
   }
 
   // ---------------------------------------------------------------- epilogue
@@ -456,8 +635,8 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
     out_r = out_t;
     rows_needed = ti != tj;
   } else {
-    in = reinterpret_cast<const E*>(args.ws + d.xt_off[args.pin]);
-    out_t = reinterpret_cast<E*>(args.ws + d.xt_off[args.pin ^ 1]);
+    in = TRB ? nullptr : reinterpret_cast<const E*>(args.ws + d.xt_off[args.pin]);
+    out_t = TRB ? nullptr : reinterpret_cast<E*>(args.ws + d.xt_off[args.pin ^ 1]);
     out_r = reinterpret_cast<E*>(args.ws + d.x_off[args.pin ^ 1]);
     ld_r = np;
   }
@@ -469,6 +648,20 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
       for (int j = 0; j < C::NBN; ++j)
 #pragma unroll
         for (int q = 0; q < 16; ++q) acc[i][j][q] *= s2;
+  } else if constexpr (TRB) {
+    // a*X from row-major X: the wave's tile is staged in LDS and read in
+    // accumulator layout with transposing reads.
+    stage_rows_in<C>(region, reinterpret_cast<const __bf16*>(args.ws + d.x_off[args.pin]), np, row0, col0, lane);
+#pragma unroll
+    for (int i = 0; i < C::NBM; ++i)
+#pragma unroll
+      for (int j = 0; j < C::NBN; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const bf16x4 x = __builtin_bit_cast(bf16x4, read_rows_tr<C>(region, i, j, g, lane));
+#pragma unroll
+          for (int q = 0; q < 4; ++q) acc[i][j][4 * g + q] = sc * (args.a * float(x[q]) + acc[i][j][4 * g + q]);
+        }
   } else {
     // Row jc of X^T (or of A) holds the 4 consecutive rows a lane needs;
     // the input tile is staged through LDS.
@@ -504,7 +697,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
     else
       store_rows_via_lds<C, float>(acc, region, o, np, row0, col0, lane);
   } else {
-    store_t_via_lds<C, E>(acc, region, out_t, mp, row0, col0, lane);
+    if (!TRB) store_t_via_lds<C, E>(acc, region, out_t, mp, row0, col0, lane);
     if (rows_needed) store_rows_via_lds<C, E>(acc, region, out_r, ld_r, row0, col0, lane);
   }
 }

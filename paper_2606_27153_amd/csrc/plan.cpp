@@ -154,9 +154,11 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
       off += round_up(bytes, kAlign);
       return at;
     };
+    // X in both layouts for the fp32 classes; the bf16 classes read X^T
+    // straight from X with LDS transposing reads and keep X only.
     for (int pp = 0; pp < 2; ++pp) {
       h.x_off[pp] = take(h.m_pad * h.n_pad * esz);
-      h.xt_off[pp] = take(h.m_pad * h.n_pad * esz);
+      h.xt_off[pp] = ci.fp32 ? take(h.m_pad * h.n_pad * esz) : -1;
     }
     h.a_off = take(h.m_pad * h.m_pad * esz);
     h.b_off = take(h.m_pad * h.m_pad * esz);
@@ -223,7 +225,7 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
       h.slot = s;
       for (int pp = 0; pp < 2; ++pp) {
         h.x_off[pp] += off;
-        h.xt_off[pp] += off;
+        if (h.xt_off[pp] >= 0) h.xt_off[pp] += off;
       }
       h.a_off += off;
       h.b_off += off;

@@ -62,7 +62,10 @@ int main(int argc, char** argv) {
       const std::pair<long long, long long> rs[] = {
           {h.x_off[0], xb}, {h.x_off[1], xb}, {h.xt_off[0], xb}, {h.xt_off[1], xb},
           {h.a_off, ab},    {h.b_off, ab},    {h.o_off, h.m_pad * h.n_pad * 4}, {h.partial_off, h.ew_tiles * 4}};
+      if ((h.xt_off[0] < 0) != (h.fp32_ns == 0) || (h.xt_off[1] < 0) != (h.fp32_ns == 0))
+        return fail("X^T buffers must exist exactly for the fp32 classes");
       for (const auto& rg : rs) {
+        if (rg.first < 0) continue;  // absent X^T buffer
         if (rg.first % 256 != 0) return fail("unaligned region");
         regions.push_back(rg);
       }
