@@ -1,0 +1,103 @@
+"""GPU checks of the Python front end and the ABI extras: the torch.optim
+wrapper, checkpoint/resume equivalence, launch timing, and the pointer-table
+refresh when buffers move."""
+import pytest
+import torch
+
+from paper_2606_27153_amd.optim import Muon, MuonPlan
+from paper_2606_27153_amd.workloads import custom_workload, make_grads, make_state
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [(256, 768), (768, 256), (512, 512), (64, 300)]
+
+
+def test_optimizer_wrapper_matches_plan_step():
+    wl = custom_workload(SHAPES, seed=21)
+    pa, ma = make_state(torch, wl, "cuda:0")
+    pb, _ = make_state(torch, wl, "cuda:0")
+    params = [torch.nn.Parameter(p) for p in pb]
+    opt = Muon(params, lr=0.02, momentum=0.95, weight_decay=0.01, ns_steps=5)
+    plan = MuonPlan([(m.rows, m.cols, m.param, m.grad) for m in wl.matrices])
+    for step in range(3):
+        g = make_grads(torch, wl, step, "cuda:0")
+        plan.step(pa, g, ma, lr=0.02, momentum=0.95, weight_decay=0.01, ns_steps=5)
+        for p, gi in zip(params, g):
+            p.grad = gi.clone()
+        opt.step()
+    torch.cuda.synchronize()
+    for x, y in zip(pa, params):
+        assert torch.equal(x, y.data)
+    for x, p in zip(ma, params):
+        assert torch.equal(x, opt.state[p]["momentum_buffer"])
+    plan.close()
+
+
+def test_checkpoint_resume_is_bitwise_identical():
+    wl = custom_workload(SHAPES, seed=22)
+    descs = [(m.rows, m.cols, m.param, m.grad) for m in wl.matrices]
+    kw = dict(lr=0.02, momentum=0.95, weight_decay=0.01, ns_steps=5)
+    # uninterrupted run of 3 steps
+    plan = MuonPlan(descs)
+    p, m = make_state(torch, wl, "cuda:0")
+    for step in range(3):
+        plan.step(p, make_grads(torch, wl, step, "cuda:0"), m, **kw)
+    torch.cuda.synchronize()
+    # 2 steps, save W and M to host, new plan and new buffers, 3rd step
+    plan2 = MuonPlan(descs)
+    q, n = make_state(torch, wl, "cuda:0")
+    for step in range(2):
+        plan2.step(q, make_grads(torch, wl, step, "cuda:0"), n, **kw)
+    torch.cuda.synchronize()
+    saved = [(x.cpu(), y.cpu()) for x, y in zip(q, n)]
+    plan2.close()
+    del q, n
+    plan3 = MuonPlan(descs)
+    q = [x.cuda() for x, _ in saved]
+    n = [y.cuda() for _, y in saved]
+    plan3.step(q, make_grads(torch, wl, 2, "cuda:0"), n, **kw)
+    torch.cuda.synchronize()
+    for a, b in zip(p + m, q + n):
+        assert torch.equal(a, b)
+    plan.close()
+    plan3.close()
+
+
+def test_moved_buffers_refresh_the_pointer_table():
+    wl = custom_workload(SHAPES, seed=23)
+    plan = MuonPlan([(mm.rows, mm.cols, mm.param, mm.grad) for mm in wl.matrices])
+    kw = dict(lr=0.02, momentum=0.95, weight_decay=0.01, ns_steps=5)
+    p, m = make_state(torch, wl, "cuda:0")
+    p2 = [x.clone() for x in p]
+    m2 = [x.clone() for x in m]
+    g = make_grads(torch, wl, 0, "cuda:0")
+    plan.step(p, g, m, **kw)       # table holds p, m
+    plan.step(p2, g, m2, **kw)     # different buffers: must be refreshed
+    torch.cuda.synchronize()
+    for a, b in zip(p + m, p2 + m2):
+        assert torch.equal(a, b)
+    plan.close()
+
+
+def test_launch_timing_reports_every_kind():
+    wl = custom_workload([(1024, 4096), (96, 300)] * 2, seed=24)
+    plan = MuonPlan([(mm.rows, mm.cols, mm.param, mm.grad) for mm in wl.matrices])
+    p, m = make_state(torch, wl, "cuda:0")
+    g = make_grads(torch, wl, 0, "cuda:0")
+    plan.set_timing(True)
+    plan.step(p, g, m, lr=0.02, momentum=0.95, weight_decay=0.01, ns_steps=5)
+    plan.set_timing(False)
+    stats = plan.timing_read()
+    kinds = {s["kind"] for s in stats}
+    assert kinds == {"momentum", "finalize", "gram", "poly", "bx", "apply"}
+    info = plan.info()
+    assert sum(s["launches"] for s in stats) <= info["launches_per_step"]
+    for s in stats:
+        assert s["total_ms"] > 0
+        if s["kind"] in ("gram", "poly", "bx"):
+            assert s["algo_flops"] > 0
+    want = sum(3 * min(r, c) ** 2 * max(r, c) + min(r, c) ** 3 for r, c in ((1024, 4096), (96, 300))) * 2 * 5
+    got = sum(s["algo_flops"] for s in stats)
+    assert abs(got - want) <= 1e-9 * want
+    assert plan.timing_read() == []     # records were dropped by the first read
+    plan.close()
