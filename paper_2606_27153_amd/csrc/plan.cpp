@@ -98,9 +98,36 @@ void emit_full(std::vector<TileEntry>& t, int32_t mat, int64_t tm, int64_t tn) {
   }
 }
 
+#ifndef MUON_LOWER_ORDER
+#define MUON_LOWER_ORDER 1
+#endif
+
+// Lower-triangular tile list (tj <= ti) of one matrix in dispatch order:
+// 8 x 8 blocks of output tiles, row-block by row-block.  In a full
+// off-diagonal block XCD x receives the 2 x 4 sub-block at rows 2*(x%4),
+// columns 4*(x/4), so each XCD's blocks share 6 operand panels; diagonal
+// and partial blocks are emitted row by row.
 void emit_lower(std::vector<TileEntry>& t, int32_t mat, int64_t tm) {
-  for (int64_t ti = 0; ti < tm; ++ti)
-    for (int64_t tj = 0; tj <= ti; ++tj) t.push_back(TileEntry{mat, uint16_t(ti), uint16_t(tj)});
+  if (MUON_LOWER_ORDER == 0) {
+    for (int64_t ti = 0; ti < tm; ++ti)
+      for (int64_t tj = 0; tj <= ti; ++tj) t.push_back(TileEntry{mat, uint16_t(ti), uint16_t(tj)});
+    return;
+  }
+  for (int64_t r0 = 0; r0 < tm; r0 += 8) {
+    const int64_t r1 = std::min(tm, r0 + 8);
+    for (int64_t c0 = 0; c0 <= r0; c0 += 8) {
+      if (c0 < r0 && r1 - r0 == 8 && t.size() % 8 == 0) {
+        for (int64_t b = 0; b < 64; ++b) {
+          const int64_t x = b % 8, k = b / 8;
+          t.push_back(TileEntry{mat, uint16_t(r0 + 2 * (x % 4) + k / 4), uint16_t(c0 + 4 * (x / 4) + k % 4)});
+        }
+      } else {
+        for (int64_t ti = r0; ti < r1; ++ti)
+          for (int64_t tj = c0; tj < std::min(c0 + 8, ti + 1); ++tj)
+            t.push_back(TileEntry{mat, uint16_t(ti), uint16_t(tj)});
+      }
+    }
+  }
 }
 
 }  // namespace
