@@ -83,7 +83,9 @@ typedef struct muon_matrix_desc {
 typedef struct muon_plan_opts {
   int32_t precision;                 /* muon_ns_precision */
   int32_t max_ns_steps;              /* largest ns_steps muon_step accepts, 1..64 */
-  float a, b, c;                     /* NS coefficients of Eq. 2, used for every step */
+  float a, b, c;                     /* NS coefficients of Eq. 2, used for every step.  c = 0 gives the
+                                        cubic iteration (the A*A product is skipped); otherwise b / c must
+                                        be finite in fp32, else muon_plan_create returns INVALID_ARG */
   float eps;                         /* added to ||X||_F before dividing */
   int32_t small_m_threshold;         /* bf16 plans: min(rows,cols) <= this -> fp32 NS */
   uint32_t flags;                    /* MUON_PLAN_* */

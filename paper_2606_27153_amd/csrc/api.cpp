@@ -41,6 +41,8 @@ muon_status check_opts(const muon_plan_opts& o) {
     return fail(MUON_ERR_INVALID_ARG, "opts.max_ns_steps must be in [1, 64]");
   if (!std::isfinite(o.a) || !std::isfinite(o.b) || !std::isfinite(o.c))
     return fail(MUON_ERR_INVALID_ARG, "opts.a, opts.b, opts.c must be finite");
+  if (o.c != 0.f && !std::isfinite(o.b / o.c))
+    return fail(MUON_ERR_INVALID_ARG, "opts.c must be 0 or large enough that b / c is finite in fp32");
   if (!std::isfinite(o.eps) || o.eps < 0.f) return fail(MUON_ERR_INVALID_ARG, "opts.eps must be finite and >= 0");
   if (o.small_m_threshold < 0) return fail(MUON_ERR_INVALID_ARG, "opts.small_m_threshold must be >= 0");
   if (o.flags & ~uint32_t(MUON_PLAN_HOST_ONLY)) return fail(MUON_ERR_INVALID_ARG, "opts.flags has unknown bits");
@@ -179,13 +181,15 @@ muon_status step_impl(muon_plan plan, void* const* params, const void* const* gr
     if (e != hipSuccess) return hip_fail(e, "finalize kernel launch");
     for (int32_t it = 0; it < ns_steps; ++it) {
       const int32_t last = it == ns_steps - 1;
-      for (int32_t stage = ST_GRAM; stage <= ST_BX; ++stage)
+      for (int32_t stage = ST_GRAM; stage <= ST_BX; ++stage) {
+        if (stage == ST_POLY && s.c == 0.f) continue;  // cubic iteration: the Gram stage wrote B = b*A
         for (const ClassLaunch& cl : w.launches) {
           const int32_t kind = stage == ST_GRAM ? MUON_KERNEL_GRAM : stage == ST_POLY ? MUON_KERNEL_POLY : MUON_KERNEL_BX;
           const double fl = stage == ST_GRAM ? cl.flops_gram : stage == ST_POLY ? cl.flops_poly : cl.flops_bx;
           e = run(kind, cl.kclass, fl, 0.0, [&] { return launch_ns_gemm(p, w, cl, stage, it, last, ws, s, stream); });
           if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
         }
+      }
     }
     e = run(MUON_KERNEL_APPLY, -1, 0.0, w.bytes_apply, [&] { return launch_apply(p, w, ws, s, stream); });
     if (e != hipSuccess) return hip_fail(e, "apply kernel launch");

@@ -275,29 +275,6 @@ struct TLay {
   }
 };
 
-// Loads rows [col0, col0 + WTN) x columns [row0 + p0, row0 + p0 + PASS) of
-// src (leading dimension ld) into the wave's LDS region in TLay layout with
-// direct-to-LDS 16-byte loads: instruction i fills LDS pieces 64*i .. 64*i+63
-// (lane l -> piece 64*i + l), so each lane fetches the logical piece that
-// the swizzle places in that slot.  Full-line global reads, no registers.
-template <class L, class C, typename T>
-__device__ __forceinline__ void stage_t_in(char* region, const T* src, int64_t ld, int64_t row0, int64_t col0,
-                                           int p0, int lane) {
-  constexpr int N = C::WTN * L::PPR;
-  constexpr int EPP = 16 / L::ESZ;
-  constexpr int SW = L::PPR < 16 ? L::PPR - 1 : 15;
-  static_assert(N % 64 == 0, "whole pieces per lane");
-#pragma unroll
-  for (int it = 0; it < N / 64; ++it) {
-    const int piece = lane + 64 * it;
-    const int r = piece / L::PPR, phys = piece % L::PPR;
-    const int pc = phys ^ (r & SW);
-    const T* g = src + (col0 + r) * ld + row0 + p0 + pc * EPP;
-    __builtin_amdgcn_global_load_lds((gbl_void_t*)(g), (lds_void_t*)(region + it * 1024), 16, 0, 0);
-  }
-  wait_vm_all();
-}
-
 // Writes this wave's accumulator tile transposed: out[(col0 + j) * ld + row0
 // + i] = acc(i, j), through LDS in TLay layout and full-line 16-byte stores.
 template <class C, typename OUT>
@@ -440,35 +417,52 @@ __device__ __forceinline__ void slab_body_tr(const char* st, const int (&oa)[4],
   __builtin_amdgcn_sched_barrier(0);
 }
 
-// Stages the wave's (WTM x WTN) tile of row-major src (rows row0.., columns
-// col0..) into its LDS region, row-major and segment-swizzled, with
-// direct-to-LDS loads; lane l of instruction it fills 16-byte slot 64*it + l.
-template <class C>
-__device__ __forceinline__ void stage_rows_in(char* region, const __bf16* src, int64_t ld, int64_t row0,
-                                              int64_t col0, int lane) {
-  constexpr int ROWB = C::WTN * 2, LPR = ROWB / 16;
-  constexpr int N = C::WTM * LPR;
-  static_assert(N % 64 == 0, "whole slots per lane");
+// Adds coef * IN[i][j] to the accumulators for the output rows i that K
+// slab kt covers.  IN is X (B*X) or A (polynomial step), and those values
+// are already in LDS: the second operand's slab holds column j of X for
+// k = i (B*X) or row j of the symmetric A at k = i (A*A), for every output
+// row i of the tile whose index falls in the slab.  Each accumulator block
+// of 32 rows sits in exactly one slab, so every term is added once.
+//   TRB: the slab is row-major X (rows k); transposing reads hand each lane
+//        the 4 consecutive rows of its column.
+//   otherwise: the slab holds K-contiguous rows (the operand's row = the
+//        output column j); a lane's 4 consecutive k are 8 or 16 contiguous
+//        bytes of one swizzled chunk.
+template <class C, typename E, bool TRB>
+__device__ __forceinline__ void fuse_input(const char* sb, int kt, int row0, int wn, int lane, float coef,
+                                           f32x16 (&acc)[C::NBM][C::NBN]) {
+  const int h = lane >> 5;
 #pragma unroll
-  for (int it = 0; it < N / 64; ++it) {
-    const int slot = 64 * it + lane;
-    const int row = slot / LPR, s16 = slot % LPR;
-    const int seg = (s16 >> 1) ^ seg_swz<ROWB>(row);
-    const __bf16* g = src + (row0 + row) * ld + col0 + seg * 16 + (s16 & 1) * 8;
-    __builtin_amdgcn_global_load_lds((gbl_void_t*)(g), (lds_void_t*)(region + it * 1024), 16, 0, 0);
+  for (int i = 0; i < C::NBM; ++i) {
+    const int kb = row0 + 32 * i;  // first row (= k) of block i within the matrix
+    if (kb / C::BK != kt) continue;
+    const int kl0 = kb - kt * C::BK;
+#pragma unroll
+    for (int j = 0; j < C::NBN; ++j)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int k4 = kl0 + 8 * g + 4 * h;
+        float x[4];
+        if constexpr (TRB) {
+          constexpr int ROWB = C::TILE * 2;
+          const int jj = lane & 15;
+          const int row = k4 + (jj >> 2);
+          const int col = wn * C::WTN + 32 * j + 16 * ((lane >> 4) & 1) + 4 * (jj & 3);
+          const bf16x4 v = __builtin_bit_cast(
+              bf16x4, lds_tr16(sb + row * ROWB + (((col >> 4) ^ seg_swz<ROWB>(row)) << 5) + (col & 15) * 2));
+#pragma unroll
+          for (int e = 0; e < 4; ++e) x[e] = float(v[e]);
+        } else {
+          const int row = wn * C::WTN + 32 * j + (lane & 31);
+          const char* p = sb + row * 128 + (((k4 / C::EPC) ^ swz(row)) << 4) + (k4 % C::EPC) * int(sizeof(E));
+          const typename Vec4<E>::T v = *reinterpret_cast<const typename Vec4<E>::T*>(p);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) x[e] = float(v[e]);
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[i][j][4 * g + e] = fmaf(coef, x[e], acc[i][j][4 * g + e]);
+      }
   }
-  wait_vm_all();
-}
-
-// Reads, in accumulator layout, the 4 consecutive rows i0..i0+3 of column j
-// of the tile staged by stage_rows_in (block i, j, group g).
-template <class C>
-__device__ __forceinline__ i16x4 read_rows_tr(const char* region, int i, int j, int g, int lane) {
-  constexpr int ROWB = C::WTN * 2;
-  const int jj = lane & 15;
-  const int row = 32 * i + 8 * g + 4 * (lane >> 5) + (jj >> 2);
-  const int seg = 2 * j + ((lane >> 4) & 1);
-  return lds_tr16(region + row * ROWB + ((seg ^ seg_swz<ROWB>(row)) << 5) + 8 * (jj & 3));
 }
 
 template <typename E, int TILE, int WGM, int WGN, int STAGE>
@@ -532,6 +526,11 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
   // exit inside the trip: a second loop exit would make the compiler copy the
   // accumulators between register files.)
   const int nk = int(K / C::BK);
+  // a*X (B*X) and b*A (A*A, as b/c * A, the product is scaled by c at the
+  // end) are folded in while the slab holding them is in LDS.
+  constexpr bool FUSE = STAGE != ST_GRAM;
+  const float fcoef = STAGE == ST_BX ? args.a : args.b / args.c;
+  const int frow0 = ti * TILE + wm * C::WTM;
   if constexpr (TRB) {
     const E* srca = lane_src<C>(opa, K, wid, lane);
     const __bf16* srcb = lane_src_rows<C>(reinterpret_cast<const __bf16*>(opb), np, wid, lane);
@@ -550,6 +549,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
       load_slab<C>(srca, K, kt + 1, stage1, wid);
       load_slab_rows<C>(srcb, np, kt + 1, stage1 + C::OPB, wid);
       slab_body_tr<C>(stage0, oa, ot, fa0, fb0, fa1, fb1, acc);
+      fuse_input<C, E, true>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
       wait_vm_all();
       __syncthreads();
       read_frags_tr<C>(stage1, stage1 + C::OPB, oa[0], ot, 0, fa0, fb0);
@@ -559,6 +559,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
         load_slab_rows<C>(srcb, np, kt + 2, stage0 + C::OPB, wid);
       }
       slab_body_tr<C>(stage1, oa, ot, fa0, fb0, fa1, fb1, acc);
+      fuse_input<C, E, true>(stage1 + C::OPB, kt + 1, frow0, wn, lane, fcoef, acc);
       wait_vm_all();
       __syncthreads();
       if (kt + 2 < nk) read_frags_tr<C>(stage0, stage0 + C::OPB, oa[0], ot, 0, fa0, fb0);
@@ -566,6 +567,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
     }
     if (kt < nk) {  // odd slab count: the last slab is in stage 0
       slab_body_tr<C>(stage0, oa, ot, fa0, fb0, fa1, fb1, acc);
+      fuse_input<C, E, true>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
       __syncthreads();
     }
   } else {
@@ -588,6 +590,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
       load_slab<C>(srca, K, kt + 1, stage1, wid);
       load_slab<C>(srcb, K, kt + 1, stage1 + C::OPB, wid);
       slab_body<C, E>(stage0, oa, ob, fa0, fb0, fa1, fb1, acc);
+      if (FUSE) fuse_input<C, E, false>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
       wait_vm_all();
       __syncthreads();
       read_frags<C, E>(stage1, stage1 + C::OPB, oa[0], ob[0], fa0, fb0);
@@ -597,6 +600,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
         load_slab<C>(srcb, K, kt + 2, stage0 + C::OPB, wid);
       }
       slab_body<C, E>(stage1, oa, ob, fa0, fb0, fa1, fb1, acc);
+      if (FUSE) fuse_input<C, E, false>(stage1 + C::OPB, kt + 1, frow0, wn, lane, fcoef, acc);
       wait_vm_all();
       __syncthreads();
       if (kt + 2 < nk) read_frags<C, E>(stage0, stage0 + C::OPB, oa[0], ob[0], fa0, fb0);
@@ -604,6 +608,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
     }
     if (kt < nk) {  // odd slab count: the last slab is in stage 0
       slab_body<C, E>(stage0, oa, ob, fa0, fb0, fa1, fb1, acc);
+      if (FUSE) fuse_input<C, E, false>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
       __syncthreads();
     }
   }
@@ -611,85 +616,41 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
   // ---------------------------------------------------------------- epilogue
   // Accumulator element q of a 32x32 block sits at row 8*(q/4) + 4*(lane/32)
   // + q%4 and column lane%32 of that block, so a lane holds 4 consecutive
-  // rows of one column.  The epilogue input comes from the transposed (X^T)
-  // or symmetric (A) copy and the outputs go out in both layouts; all three
-  // pass through the wave's private LDS region (the stages are free after
-  // the K loop), so that every global access is a full-line, 16-byte-per-lane
-  // row access.
+  // rows of one column.  The outputs pass through the wave's private LDS
+  // region (the stages are free after the K loop), so that every global
+  // access is a full-line, 16-byte-per-lane row access.
   const float sc = args.first ? args.scale[d.slot] : 1.f;
   const int64_t row0 = int64_t(ti) * TILE + wm * C::WTM;
   const int64_t col0 = int64_t(tj) * TILE + wn * C::WTN;
   char* region = (wid < C::NW / 2 ? stage0 : stage1) + (wid % (C::NW / 2)) * C::WAVE_LDS;
-  const E* in = nullptr;     // input read at the transposed position (X^T, or A which is symmetric)
   E* out_t = nullptr;        // transposed output (leading dimension mp)
   E* out_r = nullptr;        // row-major output
   int64_t ld_r = mp;
   bool rows_needed = true;
   if (STAGE == ST_GRAM) {
-    out_t = reinterpret_cast<E*>(args.ws + d.a_off);
+    // With c = 0 (the cubic iteration) B = b*A is written here and the A*A
+    // product is not launched.
+    out_t = reinterpret_cast<E*>(args.ws + (args.c == 0.f ? d.b_off : d.a_off));
     out_r = out_t;
     rows_needed = ti != tj;  // a diagonal tile is complete with one store
   } else if (STAGE == ST_POLY) {
-    in = reinterpret_cast<const E*>(args.ws + d.a_off);
     out_t = reinterpret_cast<E*>(args.ws + d.b_off);
     out_r = out_t;
     rows_needed = ti != tj;
   } else {
-    in = TRB ? nullptr : reinterpret_cast<const E*>(args.ws + d.xt_off[args.pin]);
     out_t = TRB ? nullptr : reinterpret_cast<E*>(args.ws + d.xt_off[args.pin ^ 1]);
     out_r = reinterpret_cast<E*>(args.ws + d.x_off[args.pin ^ 1]);
     ld_r = np;
   }
-  if (STAGE == ST_GRAM) {
-    const float s2 = sc * sc;
+  // Gram: s^2 * acc (times b when c = 0);  A*A: c * (acc + b/c * A);
+  // B*X: s * (acc + a * X)
+  const float mul = STAGE == ST_GRAM ? (args.c == 0.f ? args.b * sc * sc : sc * sc) : STAGE == ST_POLY ? args.c : sc;
 #pragma unroll
-    for (int i = 0; i < C::NBM; ++i)
+  for (int i = 0; i < C::NBM; ++i)
 #pragma unroll
-      for (int j = 0; j < C::NBN; ++j)
+    for (int j = 0; j < C::NBN; ++j)
 #pragma unroll
-        for (int q = 0; q < 16; ++q) acc[i][j][q] *= s2;
-  } else if constexpr (TRB) {
-    // a*X from row-major X: the wave's tile is staged in LDS and read in
-    // accumulator layout with transposing reads.
-    stage_rows_in<C>(region, reinterpret_cast<const __bf16*>(args.ws + d.x_off[args.pin]), np, row0, col0, lane);
-#pragma unroll
-    for (int i = 0; i < C::NBM; ++i)
-#pragma unroll
-      for (int j = 0; j < C::NBN; ++j)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const bf16x4 x = __builtin_bit_cast(bf16x4, read_rows_tr<C>(region, i, j, g, lane));
-#pragma unroll
-          for (int q = 0; q < 4; ++q) acc[i][j][4 * g + q] = sc * (args.a * float(x[q]) + acc[i][j][4 * g + q]);
-        }
-  } else {
-    // Row jc of X^T (or of A) holds the 4 consecutive rows a lane needs;
-    // the input tile is staged through LDS.
-    using L = TLay<C, E>;
-#pragma unroll
-    for (int p0 = 0; p0 < C::WTM; p0 += L::PASS) {
-      stage_t_in<L, C, E>(region, in, mp, row0, col0, p0, lane);
-#pragma unroll
-      for (int i = 0; i < C::NBM; ++i) {
-        if (i * 32 < p0 || i * 32 >= p0 + L::PASS) continue;
-#pragma unroll
-        for (int j = 0; j < C::NBN; ++j)
-#pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const int r = j * 32 + (lane & 31);
-            const int c = i * 32 + 8 * g + 4 * (lane >> 5) - p0;
-            const typename Vec4<E>::T x =
-                *reinterpret_cast<const typename Vec4<E>::T*>(region + L::off(r, c * L::ESZ));
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const float v = acc[i][j][4 * g + q];
-              acc[i][j][4 * g + q] =
-                  STAGE == ST_POLY ? args.b * float(x[q]) + args.c * v : sc * (args.a * float(x[q]) + v);
-            }
-          }
-      }
-    }
-  }
+      for (int q = 0; q < 16; ++q) acc[i][j][q] *= mul;
   if (STAGE == ST_BX && args.last) {
     float* o = reinterpret_cast<float*>(args.ws + d.o_off);
     if (d.transposed)

@@ -69,7 +69,7 @@ class ParityResult:
 def run_parity(wl: Workload, *, precision: str = "bf16", steps: Optional[int] = None,
                check: Optional[Sequence[int]] = None, ns_steps: Optional[int] = None,
                nesterov: Optional[bool] = None, wave_bytes: int = 0, device: str = "cuda:0",
-               plan: Optional[MuonPlan] = None) -> ParityResult:
+               plan: Optional[MuonPlan] = None, abc: Optional[Sequence[float]] = None) -> ParityResult:
     """Runs ``steps`` HIP Muon steps over the whole workload and checks the
     matrices in ``check`` against the free-running oracle after every step."""
     steps = wl.steps if steps is None else steps
@@ -80,7 +80,8 @@ def run_parity(wl: Workload, *, precision: str = "bf16", steps: Optional[int] = 
     descs = [(m.rows, m.cols, m.param, m.grad) for m in wl.matrices]
     own_plan = plan is None
     if own_plan:
-        plan = MuonPlan(descs, precision=precision, wave_bytes=wave_bytes)
+        plan = MuonPlan(descs, precision=precision, wave_bytes=wave_bytes, abc=abc)
+    abc = R.QUINTIC_ABC if abc is None else tuple(float(np.float32(v)) for v in abc)
     params, moms = make_state(torch, wl, device)
     torch.cuda.synchronize()
     # oracle state: its own stored values, starting from the same seeded ones
@@ -100,7 +101,7 @@ def run_parity(wl: Workload, *, precision: str = "bf16", steps: Optional[int] = 
             spec = wl.matrices[i]
             g = to64(grads[i])
             ref = R.muon_step_matrix(ow[i], g, om[i], lr=lr, momentum=mu, weight_decay=wd, ns_steps=ns,
-                                     nesterov=nest, param_dtype=spec.param)
+                                     nesterov=nest, param_dtype=spec.param, abc=abc)
             o_gpu = to64(outs[i])
             m_gpu = to64(moms[i])
             w_gpu = to64(params[i])

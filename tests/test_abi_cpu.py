@@ -155,6 +155,7 @@ def test_plan_create_rejects_bad_descriptors(lib, desc, status):
 @pytest.mark.parametrize("field,value", [
     ("precision", 3), ("max_ns_steps", 0), ("max_ns_steps", 65), ("eps", -1.0),
     ("small_m_threshold", -1), ("flags", 0x10), ("wave_bytes", -5), ("a", float("nan")),
+    ("c", 1e-39),
 ])
 def test_plan_create_rejects_bad_opts(lib, field, value):
     opts = L.muon_plan_opts()
@@ -164,6 +165,16 @@ def test_plan_create_rejects_bad_opts(lib, field, value):
     st, h = _create(lib, [(8, 8, 1, 1, 0)], opts)
     assert st == L.MUON_ERR_INVALID_ARG
     assert field.split("_")[0] in L.last_error() or "opts" in L.last_error()
+
+
+def test_plan_create_accepts_cubic_coefficients(lib):
+    opts = L.muon_plan_opts()
+    lib.muon_plan_opts_default(ctypes.byref(opts))
+    opts.flags = L.MUON_PLAN_HOST_ONLY
+    opts.a, opts.b, opts.c = 1.5, -0.5, 0.0
+    st, h = _create(lib, [(8, 8, 1, 1, 0)], opts)
+    assert st == L.MUON_OK
+    assert lib.muon_plan_destroy(h) == L.MUON_OK
 
 
 def test_null_arguments(lib):

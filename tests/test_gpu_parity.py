@@ -122,6 +122,16 @@ def test_plain_momentum_without_nesterov():
     assert_parity(res, "bf16", "no-nesterov")
 
 
+@pytest.mark.parametrize("precision", ["bf16", "fp32"])
+@pytest.mark.parametrize("abc", [(15 / 8, -10 / 8, 3 / 8), (1.5, -0.5, 0.0)], ids=["quintic-classic", "cubic"])
+def test_other_ns_coefficients(precision, abc):
+    # Eq. 2 with other (a, b, c): the textbook quintic and, with c = 0, the
+    # cubic iteration (for which the A*A product is not launched).
+    wl = custom_workload([(64, 200), (200, 128), (256, 768), (768, 256), (300, 300)], seed=6)
+    res = run_parity(wl, precision=precision, steps=2, abc=abc)
+    assert_parity(res, precision, f"abc={abc}")
+
+
 def test_step_and_debug_step_are_bitwise_identical():
     wl = custom_workload([(300, 500), (500, 300), (2048, 512)], seed=6)
     descs = [(m.rows, m.cols, m.param, m.grad) for m in wl.matrices]
