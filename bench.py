@@ -27,7 +27,7 @@ METRIC = "Muon optimizer-step ms per step (1 GPU) + MFMA util % on Newton–Schu
 PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 matrix peak: 256 CU x 2.4 GHz x 4096 flop/clk
 PEAK_F32_TFLOPS = 157.3       # MI355X fp32 matrix peak
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
-GEMM_KINDS = ("gram", "poly", "bx")
+GEMM_KINDS = ("gram", "poly", "bx", "symm")
 
 
 def log(*a):
@@ -227,6 +227,32 @@ def cpu_baseline(wl, budget_s: float):
                        + "; ".join(sampled) + "), scaled by bucket counts to the whole set")}
 
 
+def gemm_algorithmic_bytes(plan, k: int, kind: str, kclass: str) -> float:
+    """HBM bytes one muon_step must move for the launches of one GEMM kind and
+    kernel class, each operand read once and each output written once:
+      Eq. 2, per step:  Gram  read X, write A;  A*A  read A, write B;
+                        B*X   read B and X, write X' (O, fp32, on the last step)
+      Gram space:       Gram  read X0, write G (once);  P_i  read G, write P (k times);
+                        m^3 products  read two, write one (3 (k - 1) times);
+                        B*X   read Q and X0, write O (once)."""
+    from paper_2606_27153_amd import _lib as L
+    total = 0.0
+    for i in range(plan.n):
+        mi = plan.matrix_info(i)
+        if L.KERNEL_CLASSES[mi["kernel_class"]] != kclass:
+            continue
+        m, n = float(mi["m"]), float(mi["n"])
+        e = 4.0 if mi["fp32_ns"] else 2.0
+        if mi["gram_space"]:
+            per = {"gram": e * (m * n + m * m), "poly": k * 2 * e * m * m, "symm": (k - 1) * 3 * 3 * e * m * m,
+                   "bx": e * (m * m + m * n) + 4.0 * m * n}
+        else:
+            per = {"gram": k * e * (m * n + m * m), "poly": k * 2 * e * m * m, "symm": 0.0,
+                   "bx": k * e * (m * m + m * n) + (k - 1) * e * m * n + 4.0 * m * n}
+        total += per[kind]
+    return total
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -235,6 +261,8 @@ def main(argv=None) -> int:
     ap.add_argument("--config", default="8b", choices=["tiny", "1b", "8b", "vla", "moe"])
     ap.add_argument("--precision", default="bf16", choices=["bf16", "fp32"])
     ap.add_argument("--wave-bytes", type=int, default=0)
+    ap.add_argument("--gram-min-aspect", type=float, default=2.0,
+                    help="Gram-space recurrence (Eq. 4) for matrices with n >= this * m; 0 = Eq. 2 only")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle time to sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -269,7 +297,7 @@ def main(argv=None) -> int:
     wl = get_workload(args.config)
     log(f"[bench] workload {wl.key}: {wl.description}; {wl.elements() / 1e9:.2f} G elements")
     plan = MuonPlan([(m.rows, m.cols, m.param, m.grad) for m in wl.matrices], precision=args.precision,
-                    wave_bytes=args.wave_bytes)
+                    wave_bytes=args.wave_bytes, gram_min_aspect=args.gram_min_aspect)
     info = plan.info()
     log(f"[bench] plan: {info['n_waves']} waves, {info['n_buckets']} buckets, "
         f"{info['launches_per_step']} launches/step at max steps, workspace {info['workspace_bytes'] / 2**30:.2f} GiB")
@@ -343,11 +371,11 @@ def main(argv=None) -> int:
     roof["mean_launch_ms"] = round(dom["total_ms"] / dom["launches"], 4)
     traffic = read_traffic(dom_key)
     roof["traffic"] = None if traffic is None else round(traffic)
-    if dom["kind"] == "bx":
-        # algorithmic bytes of one B*X launch: read B and X once, write X' once (bf16)
+    if dom["kind"] in GEMM_KINDS:
         launches_per_step = dom["launches"] / args.steps
-        alg = sum(2.0 * min(m.rows, m.cols) ** 2 + 4.0 * m.rows * m.cols for m in wl.matrices)
-        roof["algorithmic_bytes"] = round(alg * wl.ns_steps / launches_per_step)
+        alg = gemm_algorithmic_bytes(plan, wl.ns_steps, dom["kind"], dom["kernel_class"])
+        roof["algorithmic_bytes"] = round(alg / launches_per_step)
+        roof["flop_per_byte"] = round(dom["algo_flops"] / dom["launches"] / roof["algorithmic_bytes"], 1)
         if traffic is not None:
             roof["traffic_vs_algorithmic"] = round(traffic / roof["algorithmic_bytes"], 2)
 
@@ -374,7 +402,8 @@ def main(argv=None) -> int:
         "config": {"workload": wl.key, "description": wl.description, "matrices": wl.n,
                    "elements": wl.elements(), "ns_steps": wl.ns_steps,
                    "params": sorted({m.param for m in wl.matrices}), "momentum": "f32",
-                   "ns_operands": args.precision, "parallelism": "single GPU"},
+                   "ns_operands": args.precision, "gram_space_matrices": info["n_gram"],
+                   "gram_min_aspect": args.gram_min_aspect, "parallelism": "single GPU"},
         "mfma_util_pct_ns_gemms": round(mfma_util, 2),
         "ns_gemm_tflops": round(ns_tflops, 2),
         "ns_gemm_ms_per_step": round(gemm_ms, 3),

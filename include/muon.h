@@ -11,7 +11,12 @@
  *        A = X X^T,  B = b*A + c*A*A,  X <- a*X + B*X
  *      with the Gram product computed on lower-triangular tiles only and
  *      mirrored (the symmetric kernel of Sec. 3.3), the polynomial fused into
- *      the epilogue of the A*A product and a*X fused into the epilogue of B*X
+ *      the A*A product and a*X fused into B*X.  Wide enough matrices
+ *      (n >= gram_min_aspect * m) instead carry the iteration in Gram space
+ *      (Sec. 3.3, Eq. 4): G0 = X0 X0^T, P_i = a I + b G_i + c G_i^2,
+ *      G_{i+1} = P_i (G_i P_i), Q = P_{k-1} ... P_0, X_k = Q X0 -- every
+ *      m x m product symmetric (lower tiles, mirrored), one m x n product at
+ *      each end: 3 m^2 n + (4k - 3) m^3 flops instead of k (3 m^2 n + m^3)
  *   5. O = X^T (tall) or X (wide) -- the orthogonalised update NS_k(M_t)
  *   6. Eq. 1 with decoupled weight decay and the shape scale:
  *        W <- W*(1 - lr*wd) - lr*sqrt(max(1, rows/cols))*O
@@ -40,7 +45,7 @@
 extern "C" {
 #endif
 
-#define MUON_ABI_VERSION 1
+#define MUON_ABI_VERSION 2
 
 #if defined(__GNUC__)
 #define MUON_API __attribute__((visibility("default")))
@@ -91,6 +96,10 @@ typedef struct muon_plan_opts {
   uint32_t flags;                    /* MUON_PLAN_* */
   int64_t wave_bytes;                /* cap on the NS working set of one group ("wave")
                                         of matrices processed together; 0 = default */
+  float gram_min_aspect;             /* bf16 NS matrices with n >= gram_min_aspect * m run the
+                                        Gram-space recurrence (Eq. 4); 0 = never.  Must be 0 or
+                                        >= 1; ignored when c = 0 */
+  int32_t reserved;                  /* must be 0 */
 } muon_plan_opts;
 
 typedef struct muon_plan_s* muon_plan;
@@ -103,9 +112,15 @@ typedef struct muon_plan_info {
   int32_t device;                    /* HIP device the plan lives on, -1 if host-only */
   int64_t workspace_bytes;           /* bytes muon_step needs */
   int64_t launches_per_step;         /* kernel launches of one muon_step at max_ns_steps */
-  double ns_flops_per_ns_step;       /* algorithmic flops of one NS step over all matrices:
-                                        sum of 3 m^2 n + m^3 (symmetry-aware) */
-  double padded_flops_per_ns_step;   /* flops the kernels issue on padded tiles */
+  double ns_flops_per_ns_step;       /* algorithmic flops of one NS step of Eq. 2 over all
+                                        matrices: sum of 3 m^2 n + m^3 (symmetry-aware) */
+  double padded_flops_per_ns_step;   /* flops those steps issue on padded tiles */
+  double ns_flops_fixed;             /* the plan's own algorithmic NS flops for k >= 1 steps
+                                        are ns_flops_fixed + k * ns_flops_step: Eq. 2 matrices */
+  double ns_flops_step;              /*   add 3 m^2 n + m^3 per step, Gram-space ones
+                                          3 m^2 n - 3 m^3 once and 4 m^3 per step */
+  int32_t n_gram;                    /* matrices that run the Gram-space recurrence */
+  int32_t reserved;
 } muon_plan_info;
 
 /* Placement of one matrix in the plan. */
@@ -118,11 +133,14 @@ typedef struct muon_matrix_info {
   int32_t fp32_ns;                   /* 1 if the NS GEMMs run in fp32 */
   int32_t wave;                      /* group the matrix is stepped in */
   int32_t bucket;
+  int32_t gram_space;                /* 1 if it runs the Gram-space recurrence (Eq. 4) */
+  int32_t reserved;
 } muon_matrix_info;
 
 /* Fills *o with the defaults: precision BF16, max_ns_steps 16,
  * (a,b,c) = (3.4445, -4.7750, 2.0315), eps 1e-7, small_m_threshold 64,
- * flags 0, wave_bytes 0.  Returns INVALID_ARG if o is NULL. */
+ * flags 0, wave_bytes 0, gram_min_aspect 2.  Returns INVALID_ARG if o is
+ * NULL. */
 MUON_API muon_status muon_plan_opts_default(muon_plan_opts* o);
 
 /* Builds a plan for n matrices (orientation, buckets, kernel classes, tile
@@ -187,6 +205,9 @@ MUON_API muon_status muon_step_debug(muon_plan plan, void* const* params, const 
  *   MUON_KERNEL_GRAM  m^2 n flops per matrix (half of the symmetric X X^T)
  *   MUON_KERNEL_POLY  m^3 flops (half of the symmetric A*A)
  *   MUON_KERNEL_BX    2 m^2 n flops
+ *   MUON_KERNEL_SYMM  m^3 flops (a symmetric m x m product of the Gram-space
+ *                     recurrence: G P, P (G P) or P Q; the P_i product itself
+ *                     counts as MUON_KERNEL_POLY)
  *   MUON_KERNEL_MOMENTUM  read G, read and write M, write X0 once
  *   MUON_KERNEL_APPLY     read W and O (fp32), write W
  * counted for every matrix of the launch, also ones skipped for a zero
@@ -197,7 +218,8 @@ typedef enum muon_kernel_kind {
   MUON_KERNEL_GRAM = 2,
   MUON_KERNEL_POLY = 3,
   MUON_KERNEL_BX = 4,
-  MUON_KERNEL_APPLY = 5
+  MUON_KERNEL_APPLY = 5,
+  MUON_KERNEL_SYMM = 6
 } muon_kernel_kind;
 
 typedef struct muon_kernel_stat {

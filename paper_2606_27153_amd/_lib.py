@@ -42,7 +42,8 @@ class muon_plan_opts(ctypes.Structure):
     _fields_ = [("precision", ctypes.c_int32), ("max_ns_steps", ctypes.c_int32),
                 ("a", ctypes.c_float), ("b", ctypes.c_float), ("c", ctypes.c_float),
                 ("eps", ctypes.c_float), ("small_m_threshold", ctypes.c_int32),
-                ("flags", ctypes.c_uint32), ("wave_bytes", ctypes.c_int64)]
+                ("flags", ctypes.c_uint32), ("wave_bytes", ctypes.c_int64),
+                ("gram_min_aspect", ctypes.c_float), ("reserved", ctypes.c_int32)]
 
 
 class muon_plan_info(ctypes.Structure):
@@ -50,7 +51,9 @@ class muon_plan_info(ctypes.Structure):
                 ("n_buckets", ctypes.c_int32), ("device", ctypes.c_int32),
                 ("workspace_bytes", ctypes.c_int64), ("launches_per_step", ctypes.c_int64),
                 ("ns_flops_per_ns_step", ctypes.c_double),
-                ("padded_flops_per_ns_step", ctypes.c_double)]
+                ("padded_flops_per_ns_step", ctypes.c_double),
+                ("ns_flops_fixed", ctypes.c_double), ("ns_flops_step", ctypes.c_double),
+                ("n_gram", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class muon_matrix_info(ctypes.Structure):
@@ -58,7 +61,8 @@ class muon_matrix_info(ctypes.Structure):
                 ("m_pad", ctypes.c_int64), ("n_pad", ctypes.c_int64),
                 ("transposed", ctypes.c_int32), ("kernel_class", ctypes.c_int32),
                 ("tile", ctypes.c_int32), ("fp32_ns", ctypes.c_int32),
-                ("wave", ctypes.c_int32), ("bucket", ctypes.c_int32)]
+                ("wave", ctypes.c_int32), ("bucket", ctypes.c_int32),
+                ("gram_space", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class muon_kernel_stat(ctypes.Structure):
@@ -67,7 +71,7 @@ class muon_kernel_stat(ctypes.Structure):
                 ("algo_flops", ctypes.c_double), ("algo_bytes", ctypes.c_double)]
 
 
-KERNEL_KINDS = ("momentum", "finalize", "gram", "poly", "bx", "apply")
+KERNEL_KINDS = ("momentum", "finalize", "gram", "poly", "bx", "apply", "symm")
 KERNEL_CLASSES = ("bf16_t256", "bf16_t128", "bf16_t64", "f32_t128", "f32_t64")
 
 _VP = ctypes.c_void_p

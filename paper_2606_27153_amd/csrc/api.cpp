@@ -47,6 +47,9 @@ muon_status check_opts(const muon_plan_opts& o) {
   if (o.small_m_threshold < 0) return fail(MUON_ERR_INVALID_ARG, "opts.small_m_threshold must be >= 0");
   if (o.flags & ~uint32_t(MUON_PLAN_HOST_ONLY)) return fail(MUON_ERR_INVALID_ARG, "opts.flags has unknown bits");
   if (o.wave_bytes < 0) return fail(MUON_ERR_INVALID_ARG, "opts.wave_bytes must be >= 0");
+  if (!std::isfinite(o.gram_min_aspect) || (o.gram_min_aspect != 0.f && o.gram_min_aspect < 1.f))
+    return fail(MUON_ERR_INVALID_ARG, "opts.gram_min_aspect must be 0 or a finite value >= 1");
+  if (o.reserved != 0) return fail(MUON_ERR_INVALID_ARG, "opts.reserved must be 0");
   return MUON_OK;
 }
 
@@ -179,17 +182,56 @@ muon_status step_impl(muon_plan plan, void* const* params, const void* const* gr
     if (e != hipSuccess) return hip_fail(e, "momentum kernel launch");
     e = run(MUON_KERNEL_FINALIZE, -1, 0.0, 0.0, [&] { return launch_finalize(p, w, ws, s, stream); });
     if (e != hipSuccess) return hip_fail(e, "finalize kernel launch");
+    auto gemm = [&](const ClassLaunch& cl, int32_t stage, int32_t kind, const GemmStep& g) {
+      const double fl = kind == MUON_KERNEL_GRAM ? cl.flops_gram : kind == MUON_KERNEL_BX ? cl.flops_bx : cl.flops_poly;
+      return run(kind, cl.kclass, fl, 0.0, [&] { return launch_ns_gemm(p, w, cl, stage, g, ws, stream); });
+    };
+    // Eq. 2: per step A = s^2 X X^T, B = b A + c A A, X' = s (a X + B X).
+    // With c = 0 (the cubic iteration) the Gram stage writes B = b A itself.
     for (int32_t it = 0; it < ns_steps; ++it) {
-      const int32_t last = it == ns_steps - 1;
-      for (int32_t stage = ST_GRAM; stage <= ST_BX; ++stage) {
-        if (stage == ST_POLY && s.c == 0.f) continue;  // cubic iteration: the Gram stage wrote B = b*A
+      const int32_t first = it == 0, pin = it & 1, last = it == ns_steps - 1;
+      for (const ClassLaunch& cl : w.launches) {
+        if (cl.gram) continue;
+        const bool cubic = s.c == 0.f;
+        e = gemm(cl, ST_GRAM, MUON_KERNEL_GRAM,
+                 GemmStep{first, pin, last, SQ_A, SQ_A, cubic ? SQ_B : SQ_A, 0.f, 0.f, cubic ? s.b : 1.f});
+        if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
+      }
+      if (s.c != 0.f)
         for (const ClassLaunch& cl : w.launches) {
-          const int32_t kind = stage == ST_GRAM ? MUON_KERNEL_GRAM : stage == ST_POLY ? MUON_KERNEL_POLY : MUON_KERNEL_BX;
-          const double fl = stage == ST_GRAM ? cl.flops_gram : stage == ST_POLY ? cl.flops_poly : cl.flops_bx;
-          e = run(kind, cl.kclass, fl, 0.0, [&] { return launch_ns_gemm(p, w, cl, stage, it, last, ws, s, stream); });
+          if (cl.gram) continue;
+          e = gemm(cl, ST_POLY, MUON_KERNEL_POLY, GemmStep{first, pin, last, SQ_A, SQ_A, SQ_B, s.b / s.c, 0.f, s.c});
           if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
         }
+      for (const ClassLaunch& cl : w.launches) {
+        if (cl.gram) continue;
+        e = gemm(cl, ST_BX, MUON_KERNEL_BX, GemmStep{first, pin, last, SQ_B, SQ_B, SQ_B, s.a, 0.f, 1.f});
+        if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
       }
+    }
+    // Gram space (Eq. 4): G0 = s^2 X0 X0^T; per step P_i = a I + b G + c G^2
+    // (as c (G G + b/c G + a/c I)); Q_{i+1} = P_i Q_i (Q_1 = P_0, which is
+    // written straight into Q0); R = G P_i and G <- P_i R except after the
+    // last step; finally O = s Q_k X0.
+    for (const ClassLaunch& cl : w.launches) {
+      if (!cl.gram || ns_steps == 0) continue;
+      e = gemm(cl, ST_GRAM, MUON_KERNEL_GRAM, GemmStep{1, 0, 0, SQ_A, SQ_A, SQ_A, 0.f, 0.f, 1.f});
+      if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
+      for (int32_t it = 0; it < ns_steps; ++it) {
+        const int32_t pbuf = it == 0 ? SQ_Q0 : SQ_B;
+        e = gemm(cl, ST_POLY, MUON_KERNEL_POLY, GemmStep{0, 0, 0, SQ_A, SQ_A, pbuf, s.b / s.c, s.a / s.c, s.c});
+        if (e == hipSuccess && it > 0)
+          e = gemm(cl, ST_SYM, MUON_KERNEL_SYMM,
+                   GemmStep{0, 0, 0, SQ_B, (it - 1) & 1 ? SQ_Q1 : SQ_Q0, it & 1 ? SQ_Q1 : SQ_Q0, 0.f, 0.f, 1.f});
+        if (e == hipSuccess && it + 1 < ns_steps) {
+          e = gemm(cl, ST_SYM, MUON_KERNEL_SYMM, GemmStep{0, 0, 0, SQ_A, pbuf, SQ_R, 0.f, 0.f, 1.f});
+          if (e == hipSuccess) e = gemm(cl, ST_SYM, MUON_KERNEL_SYMM, GemmStep{0, 0, 0, pbuf, SQ_R, SQ_A, 0.f, 0.f, 1.f});
+        }
+        if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
+      }
+      const int32_t qk = (ns_steps - 1) & 1 ? SQ_Q1 : SQ_Q0;
+      e = gemm(cl, ST_BX, MUON_KERNEL_BX, GemmStep{1, 0, 1, qk, qk, qk, 0.f, 0.f, 1.f});
+      if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
     }
     e = run(MUON_KERNEL_APPLY, -1, 0.0, w.bytes_apply, [&] { return launch_apply(p, w, ws, s, stream); });
     if (e != hipSuccess) return hip_fail(e, "apply kernel launch");
@@ -235,6 +277,7 @@ muon_status muon_plan_opts_default(muon_plan_opts* o) {
   o->small_m_threshold = 64;
   o->flags = 0;
   o->wave_bytes = 0;
+  o->gram_min_aspect = 2.f;
   return ok();
 }
 
@@ -322,6 +365,9 @@ muon_status muon_plan_get_info(muon_plan plan, muon_plan_info* info) {
   info->launches_per_step = muon::launches_per_step(p, p.opts.max_ns_steps);
   info->ns_flops_per_ns_step = p.ns_flops;
   info->padded_flops_per_ns_step = p.padded_flops;
+  info->ns_flops_fixed = p.ns_flops_fixed;
+  info->ns_flops_step = p.ns_flops_step;
+  info->n_gram = p.n_gram;
   return ok();
 }
 
@@ -341,6 +387,7 @@ muon_status muon_plan_matrix_info(muon_plan plan, int32_t index, muon_matrix_inf
   info->fp32_ns = h.fp32_ns;
   info->wave = h.wave;
   info->bucket = h.bucket;
+  info->gram_space = h.gram;
   return ok();
 }
 

@@ -37,24 +37,30 @@ const ClassInfo& class_info(int32_t kc);
 // layout, padded to the GEMM tile; every padded extent is a multiple of 64.
 constexpr int32_t EW_TILE = 64;
 
+// The m_pad x m_pad buffers of a matrix.  Eq. 2 uses A (Gram) and B
+// (polynomial); the Gram-space recurrence of Eq. 4 uses G in A, P_i in B,
+// the running product Q in a ping-pong pair and R = G P.
+enum SqBuf : int32_t { SQ_A = 0, SQ_B = 1, SQ_Q0 = 2, SQ_Q1 = 3, SQ_R = 4, SQ_COUNT = 5 };
+
 // Device descriptor of one matrix inside a wave.  All *_off fields are byte
-// offsets into the caller's workspace.
+// offsets into the caller's workspace (-1 for a buffer the matrix lacks).
 struct MatDev {
-  int64_t x_off[2];    // oriented X, m_pad x n_pad (ping-pong pair p)
-  int64_t xt_off[2];   // X^T, n_pad x m_pad (fp32 classes only; -1 otherwise)
-  int64_t a_off;       // Gram A, m_pad x m_pad
-  int64_t b_off;       // polynomial B, m_pad x m_pad
+  int64_t x_off[2];    // oriented X, m_pad x n_pad (ping-pong pair p; Gram-space: X0 only)
+  int64_t xt_off[2];   // X^T, n_pad x m_pad (fp32 classes only)
+  int64_t sq_off[SQ_COUNT];
   int64_t o_off;       // fp32 O in stored layout, rows_pad x cols_pad
   int64_t partial_off; // fp32 partial sums of squares, one per EW tile
   int32_t rows, cols;          // stored shape
   int32_t rows_pad, cols_pad;  // stored shape padded to the tile
   int32_t m_pad, n_pad;        // oriented padded shape
   int32_t transposed;          // rows > cols
-  int32_t x_f32;               // X/A/B are fp32 (else bf16)
+  int32_t x_f32;               // X and the square buffers are fp32 (else bf16)
   int32_t param_dtype, grad_dtype;
   int32_t slot;                // position in its wave (scale / flag index)
   int32_t index;               // descriptor index (pointer table index)
   int32_t ew_tiles_c;          // cols_pad / 64
+  int32_t gram;                // runs the Gram-space recurrence
+  int32_t m;                   // oriented unpadded m
   int32_t pad0;
 };
 
@@ -75,17 +81,21 @@ struct PtrEntry {
 struct MatHost {
   int64_t rows, cols, m, n;
   int64_t m_pad, n_pad, rows_pad, cols_pad;
-  int32_t transposed, kclass, fp32_ns;
+  int32_t transposed, kclass, fp32_ns, gram;
   int32_t param_dtype, grad_dtype, momentum_dtype;
   int32_t wave, slot, bucket;
   int64_t ew_tiles;
-  int64_t x_off[2], xt_off[2], a_off, b_off, o_off, partial_off;
+  int64_t x_off[2], xt_off[2], sq_off[SQ_COUNT], o_off, partial_off;
   int64_t ws_bytes;    // workspace bytes of this matrix within its wave
 };
 
+// The matrices of one kernel class and one iteration form (Eq. 2 or the
+// Gram-space recurrence) within a wave, and their tile lists.
 struct ClassLaunch {
   int32_t kclass;
-  double flops_gram, flops_poly, flops_bx;  // algorithmic flops of one launch
+  int32_t gram;
+  double flops_gram, flops_poly, flops_bx;  // algorithmic flops of one launch (an m^3
+                                            // product of the recurrence counts as poly)
   int64_t lower_off;   // TileEntry offset of the lower-triangular list
   int32_t n_lower;
   int64_t full_off;    // TileEntry offset of the full list
@@ -118,9 +128,10 @@ struct Plan {
   std::vector<MatDev> h_matdev;     // wave order
   std::vector<int32_t> h_prefix;
   std::vector<TileEntry> h_tiles;
-  int32_t n_buckets = 0;
+  int32_t n_buckets = 0, n_gram = 0;
   int64_t ws_bytes = 0;
-  double ns_flops = 0, padded_flops = 0;
+  double ns_flops = 0, padded_flops = 0;     // per NS step of Eq. 2 over all matrices
+  double ns_flops_fixed = 0, ns_flops_step = 0;  // the plan's own: fixed + k * step
 
   // device side
   int32_t device = -1;
@@ -155,10 +166,20 @@ int launch_momentum(const Plan& p, const WaveHost& w, char* ws, const StepScalar
 int launch_finalize(const Plan& p, const WaveHost& w, char* ws, const StepScalars& s, void* stream);
 int launch_apply(const Plan& p, const WaveHost& w, char* ws, const StepScalars& s, void* stream);
 
-// ns_gemm.hip.  stage: 0 Gram (lower tiles), 1 A*A + polynomial (lower tiles),
-// 2 B*X + a*X (all tiles).  iter: NS step index; last: write O.
-enum Stage : int32_t { ST_GRAM = 0, ST_POLY = 1, ST_BX = 2 };
-int launch_ns_gemm(const Plan& p, const WaveHost& w, const ClassLaunch& cl, int32_t stage, int32_t iter,
-                   int32_t last, char* ws, const StepScalars& s, void* stream);
+// ns_gemm.hip.  Stages (lower tiles, mirrored, unless noted):
+//   ST_GRAM  sq[out] = oscale * s^2 * X X^T            (X = x[pin])
+//   ST_POLY  sq[out] = oscale * (L L + fcoef * L + diag * I),  L = sq[l]
+//   ST_BX    X' or O = s * (sq[l] X + fcoef * X)        (all tiles)
+//   ST_SYM   sq[out] = sq[l] sq[r]                      (a product known to be symmetric)
+// s is the Frobenius scale when `first` is set, else 1; `last` makes ST_BX
+// write O instead of x[pin ^ 1].
+enum Stage : int32_t { ST_GRAM = 0, ST_POLY = 1, ST_BX = 2, ST_SYM = 3 };
+struct GemmStep {
+  int32_t first, pin, last;
+  int32_t l, r, out;          // SqBuf indices
+  float fcoef, diag, oscale;
+};
+int launch_ns_gemm(const Plan& p, const WaveHost& w, const ClassLaunch& cl, int32_t stage, const GemmStep& g,
+                   char* ws, void* stream);
 
 }  // namespace muon

@@ -1,26 +1,32 @@
-// Grouped Newton-Schulz GEMMs on the gfx950 matrix cores (Eq. 2, Sec. 3.3).
+// Grouped Newton-Schulz GEMMs on the gfx950 matrix cores (Eq. 2, Eq. 4,
+// Sec. 3.3).
 //
-// One NS step X <- a*X + (b*A + c*A*A)*X with A = X X^T is three grouped
-// launches over every matrix of a wave:
+// Every product is C[i][j] = sum_k L[i][k] R[j][k] with both operands
+// K-contiguous rows (X, X^T or a square buffer; a symmetric right factor is
+// its own transpose), which is the layout the MFMA operand fetch wants.  The
+// stages (Stage in muon_internal.h):
 //
-//   ST_GRAM  A = s^2 * X X^T          lower-triangular output tiles only; each
-//                                     off-diagonal tile is also stored mirrored
-//                                     (the symmetric Gram kernel of Sec. 3.3)
-//   ST_POLY  B = b*A + c*A A^T        A is symmetric, so A*A = A*A^T: again
-//                                     lower tiles + mirror, and the polynomial
-//                                     is fused into the epilogue (it reads the
-//                                     same rounded A the matrix cores used)
-//   ST_BX    X' = s*(a*X + B X)       all tiles; a*X fused into the epilogue;
-//                                     X' is stored in both layouts, or, on the
-//                                     last step, O is stored in fp32 in the
-//                                     matrix's own (un-oriented) layout
+//   ST_GRAM  s^2 X X^T            lower-triangular output tiles only; each
+//                                 off-diagonal tile is also stored mirrored
+//                                 (the symmetric Gram kernel of Sec. 3.3)
+//   ST_POLY  c (L L + b/c L + a/c I)  L symmetric, so L L = L L^T: lower
+//                                 tiles + mirror; the b/c L term is folded in
+//                                 from the operand slab already in LDS (the
+//                                 same rounded L the matrix cores use)
+//   ST_SYM   L R                  a product of two commuting symmetric
+//                                 matrices (Gram-space recurrence), itself
+//                                 symmetric: lower tiles + mirror
+//   ST_BX    s (a X + B X)        all tiles; a X folded in from the resident
+//                                 slab of X; X' in the next ping-pong buffer,
+//                                 or, on the last step, O in fp32 in the
+//                                 matrix's own (un-oriented) layout
 //
-// s = 1/(||u||_F + eps) is applied in the first step only (X0 = s*u is never
-// materialised).  Every product is C[i][j] = sum_k P[i][k] Q[j][k] with both
-// operands K-contiguous (X, A, B and X^T rows), which is the layout the MFMA
-// operand fetch wants.  Buffers are padded to the tile with zeros, and the
-// zeros stay zero through all three products, so the kernels need no bounds
-// checks.
+// Eq. 2 runs GRAM, POLY, BX per NS step; the Gram-space recurrence runs GRAM
+// once, then POLY (P_i = a I + b G + c G^2) and SYM (P Q, G P, P (G P)) per
+// step, and BX (O = s Q X0) once.  s = 1/(||u||_F + eps) is applied where X0
+// = s*u would first enter (X0 is never materialised).  Buffers are padded to
+// the tile with zeros, and the zeros stay zero through all products, so the
+// kernels need no bounds checks.
 //
 // Block: WGM x WGN waves (2 x 4 for the 256 tile, 2 x 2 otherwise), output
 // tile TILE x TILE, each wave owning a (TILE/WGM) x (TILE/WGN) piece made of
@@ -45,10 +51,13 @@ struct GemmArgs {
   char* ws;
   const float* scale;
   const int32_t* flag;
-  float a, b, c;
-  int32_t first;   // NS step 0: fold the Frobenius scale
-  int32_t pin;     // ping-pong pair read by ST_GRAM / ST_BX
-  int32_t last;    // ST_BX of the last step writes O
+  float fcoef;     // coefficient of the term folded in from the resident slab
+  float diag;      // ST_POLY: added on the diagonal
+  float oscale;    // output factor (times s^2 / s for ST_GRAM / ST_BX in the first step)
+  int32_t first;   // fold the Frobenius scale
+  int32_t pin;     // ping-pong pair of X read by ST_GRAM / ST_BX
+  int32_t last;    // ST_BX writes O
+  int32_t l, r, out;  // square-buffer indices (SqBuf)
 };
 
 // 16-byte chunk c of LDS row r (128-byte rows) lives at chunk position
@@ -493,13 +502,12 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
     K = np;
     opa = x + int64_t(ti) * TILE * K;
     opb = x + int64_t(tj) * TILE * K;
-  } else if (STAGE == ST_POLY) {
-    const E* a = reinterpret_cast<const E*>(args.ws + d.a_off);
+  } else if (STAGE == ST_POLY || STAGE == ST_SYM) {
     K = mp;
-    opa = a + int64_t(ti) * TILE * K;
-    opb = a + int64_t(tj) * TILE * K;
+    opa = reinterpret_cast<const E*>(args.ws + d.sq_off[args.l]) + int64_t(ti) * TILE * K;
+    opb = reinterpret_cast<const E*>(args.ws + d.sq_off[STAGE == ST_POLY ? args.l : args.r]) + int64_t(tj) * TILE * K;
   } else {
-    const E* b = reinterpret_cast<const E*>(args.ws + d.b_off);
+    const E* b = reinterpret_cast<const E*>(args.ws + d.sq_off[args.l]);
     K = mp;
     opa = b + int64_t(ti) * TILE * K;
     if (TRB) {
@@ -528,8 +536,8 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
   const int nk = int(K / C::BK);
   // a*X (B*X) and b*A (A*A, as b/c * A, the product is scaled by c at the
   // end) are folded in while the slab holding them is in LDS.
-  constexpr bool FUSE = STAGE != ST_GRAM;
-  const float fcoef = STAGE == ST_BX ? args.a : args.b / args.c;
+  const bool FUSE = (STAGE == ST_POLY || STAGE == ST_BX) && args.fcoef != 0.f;
+  const float fcoef = args.fcoef;
   const int frow0 = ti * TILE + wm * C::WTM;
   if constexpr (TRB) {
     const E* srca = lane_src<C>(opa, K, wid, lane);
@@ -549,7 +557,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
       load_slab<C>(srca, K, kt + 1, stage1, wid);
       load_slab_rows<C>(srcb, np, kt + 1, stage1 + C::OPB, wid);
       slab_body_tr<C>(stage0, oa, ot, fa0, fb0, fa1, fb1, acc);
-      fuse_input<C, E, true>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
+      if (FUSE) fuse_input<C, E, true>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
       wait_vm_all();
       __syncthreads();
       read_frags_tr<C>(stage1, stage1 + C::OPB, oa[0], ot, 0, fa0, fb0);
@@ -559,7 +567,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
         load_slab_rows<C>(srcb, np, kt + 2, stage0 + C::OPB, wid);
       }
       slab_body_tr<C>(stage1, oa, ot, fa0, fb0, fa1, fb1, acc);
-      fuse_input<C, E, true>(stage1 + C::OPB, kt + 1, frow0, wn, lane, fcoef, acc);
+      if (FUSE) fuse_input<C, E, true>(stage1 + C::OPB, kt + 1, frow0, wn, lane, fcoef, acc);
       wait_vm_all();
       __syncthreads();
       if (kt + 2 < nk) read_frags_tr<C>(stage0, stage0 + C::OPB, oa[0], ot, 0, fa0, fb0);
@@ -567,7 +575,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
     }
     if (kt < nk) {  // odd slab count: the last slab is in stage 0
       slab_body_tr<C>(stage0, oa, ot, fa0, fb0, fa1, fb1, acc);
-      fuse_input<C, E, true>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
+      if (FUSE) fuse_input<C, E, true>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
       __syncthreads();
     }
   } else {
@@ -627,24 +635,31 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
   E* out_r = nullptr;        // row-major output
   int64_t ld_r = mp;
   bool rows_needed = true;
-  if (STAGE == ST_GRAM) {
-    // With c = 0 (the cubic iteration) B = b*A is written here and the A*A
-    // product is not launched.
-    out_t = reinterpret_cast<E*>(args.ws + (args.c == 0.f ? d.b_off : d.a_off));
+  if (STAGE != ST_BX) {
+    out_t = reinterpret_cast<E*>(args.ws + d.sq_off[args.out]);
     out_r = out_t;
     rows_needed = ti != tj;  // a diagonal tile is complete with one store
-  } else if (STAGE == ST_POLY) {
-    out_t = reinterpret_cast<E*>(args.ws + d.b_off);
-    out_r = out_t;
-    rows_needed = ti != tj;
   } else {
     out_t = TRB ? nullptr : reinterpret_cast<E*>(args.ws + d.xt_off[args.pin ^ 1]);
     out_r = reinterpret_cast<E*>(args.ws + d.x_off[args.pin ^ 1]);
     ld_r = np;
   }
-  // Gram: s^2 * acc (times b when c = 0);  A*A: c * (acc + b/c * A);
-  // B*X: s * (acc + a * X)
-  const float mul = STAGE == ST_GRAM ? (args.c == 0.f ? args.b * sc * sc : sc * sc) : STAGE == ST_POLY ? args.c : sc;
+  if (STAGE == ST_POLY && ti == tj && args.diag != 0.f) {
+    // diag * I on the real diagonal (the padding stays zero)
+#pragma unroll
+    for (int i = 0; i < C::NBM; ++i)
+#pragma unroll
+      for (int j = 0; j < C::NBN; ++j)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          const int r = wm * C::WTM + 32 * i + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
+          const int c = wn * C::WTN + 32 * j + (lane & 31);
+          if (r == c && ti * TILE + r < d.m) acc[i][j][q] += args.diag;
+        }
+  }
+  // Gram: oscale * s^2 * acc;  A*A: oscale * (acc + fcoef * A + diag * I);
+  // B*X: oscale * s * (acc + fcoef * X);  symmetric product: oscale * acc
+  const float mul = STAGE == ST_GRAM ? args.oscale * sc * sc : STAGE == ST_BX ? args.oscale * sc : args.oscale;
 #pragma unroll
   for (int i = 0; i < C::NBM; ++i)
 #pragma unroll
@@ -673,8 +688,11 @@ int launch_stage(int32_t stage, unsigned nblocks, const GemmArgs& g, hipStream_t
     case ST_POLY:
       hipLaunchKernelGGL((ns_gemm_kernel<E, TILE, WGM, WGN, ST_POLY>), dim3(nblocks), dim3(NT), 0, st, g);
       break;
-    default:
+    case ST_BX:
       hipLaunchKernelGGL((ns_gemm_kernel<E, TILE, WGM, WGN, ST_BX>), dim3(nblocks), dim3(NT), 0, st, g);
+      break;
+    default:
+      hipLaunchKernelGGL((ns_gemm_kernel<E, TILE, WGM, WGN, ST_SYM>), dim3(nblocks), dim3(NT), 0, st, g);
       break;
   }
   return hipGetLastError() == hipSuccess ? 0 : -1;
@@ -682,8 +700,8 @@ int launch_stage(int32_t stage, unsigned nblocks, const GemmArgs& g, hipStream_t
 
 }  // namespace
 
-int launch_ns_gemm(const Plan& p, const WaveHost& w, const ClassLaunch& cl, int32_t stage, int32_t iter,
-                   int32_t last, char* ws, const StepScalars& s, void* stream) {
+int launch_ns_gemm(const Plan& p, const WaveHost& w, const ClassLaunch& cl, int32_t stage, const GemmStep& gs,
+                   char* ws, void* stream) {
   GemmArgs g{};
   g.mats = p.d_mats;
   const bool full = stage == ST_BX;
@@ -692,12 +710,15 @@ int launch_ns_gemm(const Plan& p, const WaveHost& w, const ClassLaunch& cl, int3
   g.ws = ws;
   g.scale = reinterpret_cast<const float*>(ws + w.scale_off);
   g.flag = reinterpret_cast<const int32_t*>(ws + w.flag_off);
-  g.a = s.a;
-  g.b = s.b;
-  g.c = s.c;
-  g.first = iter == 0;
-  g.pin = iter & 1;
-  g.last = last;
+  g.fcoef = gs.fcoef;
+  g.diag = gs.diag;
+  g.oscale = gs.oscale;
+  g.first = gs.first;
+  g.pin = gs.pin;
+  g.last = gs.last;
+  g.l = gs.l;
+  g.r = gs.r;
+  g.out = gs.out;
   if (nblocks == 0) return 0;
   hipStream_t st = hipStream_t(stream);
   switch (cl.kclass) {

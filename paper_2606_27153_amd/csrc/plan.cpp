@@ -135,8 +135,14 @@ void emit_lower(std::vector<TileEntry>& t, int32_t mat, int64_t tm) {
 const ClassInfo& class_info(int32_t kc) { return kClasses[kc]; }
 
 int64_t launches_per_step(const Plan& p, int32_t ns_steps) {
+  // Eq. 2: Gram, A*A and B*X per step.  Gram space: the Gram product and
+  // B*X once, P_i per step, and P Q, G P, P (G P) on all but one step.
   int64_t n = 0;
-  for (const auto& w : p.waves) n += 3 + int64_t(ns_steps) * 3 * int64_t(w.launches.size());
+  const int64_t k = ns_steps;
+  for (const auto& w : p.waves) {
+    n += 3;  // momentum, finalize, apply
+    for (const auto& cl : w.launches) n += cl.gram ? (k > 0 ? 4 * k - 1 : 0) : 3 * k;
+  }
   return n;
 }
 
@@ -160,6 +166,14 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
     h.kclass = choose_class(h.m, h.n, o);
     const ClassInfo& ci = kClasses[h.kclass];
     h.fp32_ns = ci.fp32;
+    // Gram space (Eq. 4) pays off whenever n > m; nearly square matrices stay
+    // on Eq. 2, where bf16 rounding in the m x m chain costs more accuracy
+    // (the Gram matrix squares their conditioning).
+    h.gram = !ci.fp32 && o.gram_min_aspect > 0.f && o.c != 0.f &&
+                     double(h.n) >= double(o.gram_min_aspect) * double(h.m)
+                 ? 1
+                 : 0;
+    p.n_gram += h.gram;
     h.m_pad = round_up(h.m, ci.tile);
     h.n_pad = round_up(h.n, ci.tile);
     if (h.n_pad / ci.tile > 65535) {
@@ -169,7 +183,7 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
     h.rows_pad = h.transposed ? h.n_pad : h.m_pad;
     h.cols_pad = h.transposed ? h.m_pad : h.n_pad;
     h.ew_tiles = (h.rows_pad / EW_TILE) * (h.cols_pad / EW_TILE);
-    const auto key = std::make_tuple(h.kclass, h.m, h.n);
+    const auto key = std::make_tuple(h.kclass * 2 + h.gram, h.m, h.n);
     auto it = buckets.find(key);
     if (it == buckets.end()) it = buckets.emplace(key, int32_t(buckets.size())).first;
     h.bucket = it->second;
@@ -182,18 +196,27 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
       return at;
     };
     // X in both layouts for the fp32 classes; the bf16 classes read X^T
-    // straight from X with LDS transposing reads and keep X only.
+    // straight from X with LDS transposing reads and keep X only.  The
+    // Gram-space form reads X0 alone (no ping-pong) and keeps five square
+    // buffers instead of two.
     for (int pp = 0; pp < 2; ++pp) {
-      h.x_off[pp] = take(h.m_pad * h.n_pad * esz);
-      h.xt_off[pp] = ci.fp32 ? take(h.m_pad * h.n_pad * esz) : -1;
+      const bool need = pp == 0 || !h.gram;
+      h.x_off[pp] = need ? take(h.m_pad * h.n_pad * esz) : -1;
+      h.xt_off[pp] = need && ci.fp32 ? take(h.m_pad * h.n_pad * esz) : -1;
     }
-    h.a_off = take(h.m_pad * h.m_pad * esz);
-    h.b_off = take(h.m_pad * h.m_pad * esz);
+    for (int q = 0; q < SQ_COUNT; ++q) h.sq_off[q] = q < 2 || h.gram ? take(h.m_pad * h.m_pad * esz) : -1;
     h.o_off = take(h.m_pad * h.n_pad * 4);
     h.partial_off = take(h.ew_tiles * 4);
     h.ws_bytes = off;  // relative offsets for now, rebased per wave below
 
-    p.ns_flops += 3.0 * double(h.m) * double(h.m) * double(h.n) + double(h.m) * double(h.m) * double(h.m);
+    const double m = double(h.m), nn = double(h.n);
+    p.ns_flops += 3.0 * m * m * nn + m * m * m;
+    if (h.gram) {
+      p.ns_flops_fixed += 3.0 * m * m * nn - 3.0 * m * m * m;
+      p.ns_flops_step += 4.0 * m * m * m;
+    } else {
+      p.ns_flops_step += 3.0 * m * m * nn + m * m * m;
+    }
   }
   p.n_buckets = int32_t(buckets.size());
 
@@ -206,6 +229,7 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
     const int64_t ca = a.m_pad * a.n_pad, cb = b.m_pad * b.n_pad;
     if (ca != cb) return ca > cb;
     if (a.kclass != b.kclass) return a.kclass < b.kclass;
+    if (a.gram != b.gram) return a.gram < b.gram;
     return a.bucket < b.bucket;
   });
 
@@ -251,11 +275,11 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
       h.wave = wi;
       h.slot = s;
       for (int pp = 0; pp < 2; ++pp) {
-        h.x_off[pp] += off;
+        if (h.x_off[pp] >= 0) h.x_off[pp] += off;
         if (h.xt_off[pp] >= 0) h.xt_off[pp] += off;
       }
-      h.a_off += off;
-      h.b_off += off;
+      for (int q = 0; q < SQ_COUNT; ++q)
+        if (h.sq_off[q] >= 0) h.sq_off[q] += off;
       h.o_off += off;
       h.partial_off += off;
       off += h.ws_bytes;
@@ -274,8 +298,7 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
         d.x_off[pp] = h.x_off[pp];
         d.xt_off[pp] = h.xt_off[pp];
       }
-      d.a_off = h.a_off;
-      d.b_off = h.b_off;
+      for (int q = 0; q < SQ_COUNT; ++q) d.sq_off[q] = h.sq_off[q];
       d.o_off = h.o_off;
       d.partial_off = h.partial_off;
       d.rows = int32_t(h.rows);
@@ -291,6 +314,8 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
       d.slot = s;
       d.index = idx;
       d.ew_tiles_c = int32_t(h.cols_pad / EW_TILE);
+      d.gram = h.gram;
+      d.m = int32_t(h.m);
     }
     w.ew_tiles = ew;
     w.bytes_momentum = 0;
@@ -310,13 +335,14 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
     w.ws_bytes = off;
     p.ws_bytes = std::max(p.ws_bytes, off);
 
-    for (int32_t kc = 0; kc < KC_COUNT; ++kc) {
+    for (int32_t kg = 0; kg < 2 * KC_COUNT; ++kg) {
+      const int32_t kc = kg / 2, gram = kg % 2;
       std::vector<TileEntry> lower, full;
       const int64_t tile = kClasses[kc].tile;
       double fg = 0, fp = 0, fb = 0;
       for (int32_t s = 0; s < w.count; ++s) {
         const MatHost& h = p.mats[size_t(p.order[size_t(w.first + s)])];
-        if (h.kclass != kc) continue;
+        if (h.kclass != kc || h.gram != gram) continue;
         const int32_t pos = w.first + s;
         const double m = double(h.m), nn = double(h.n);
         fg += m * m * nn;
@@ -333,6 +359,7 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
       if (full.empty()) continue;
       ClassLaunch cl{};
       cl.kclass = kc;
+      cl.gram = gram;
       cl.flops_gram = fg;
       cl.flops_poly = fp;
       cl.flops_bx = fb;

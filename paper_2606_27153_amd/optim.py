@@ -28,12 +28,15 @@ def _dtype_code(t) -> int:
 class MuonPlan:
     """A plan over matrix descriptors ``(rows, cols, param_dtype, grad_dtype)``.
 
-    dtypes are 'f32' or 'bf16'; momentum is always fp32.
+    dtypes are 'f32' or 'bf16'; momentum is always fp32.  bf16-path matrices
+    with max(rows, cols) >= gram_min_aspect * min(rows, cols) run the
+    Gram-space recurrence (Eq. 4); 0 keeps every matrix on Eq. 2.
     """
 
     def __init__(self, descs: Sequence, *, precision: str = "bf16", max_ns_steps: int = 16,
                  abc: Optional[Sequence[float]] = None, eps: float = 1e-7,
-                 small_m_threshold: int = 64, wave_bytes: int = 0, host_only: bool = False):
+                 small_m_threshold: int = 64, wave_bytes: int = 0, gram_min_aspect: float = 2.0,
+                 host_only: bool = False):
         lib = L.load()
         n = len(descs)
         arr = (L.muon_matrix_desc * max(n, 1))()
@@ -52,6 +55,7 @@ class MuonPlan:
         opts.eps = float(eps)
         opts.small_m_threshold = int(small_m_threshold)
         opts.wave_bytes = int(wave_bytes)
+        opts.gram_min_aspect = float(gram_min_aspect)
         opts.flags = L.MUON_PLAN_HOST_ONLY if host_only else 0
         h = ctypes.c_void_p()
         L.check(lib.muon_plan_create(arr, n, ctypes.byref(opts), ctypes.byref(h)))
@@ -164,16 +168,16 @@ class Muon(_optimizer_base()):
     """
 
     def __init__(self, params, lr: float = 0.02, momentum: float = 0.95, weight_decay: float = 0.01,
-                 ns_steps: int = 5, nesterov: bool = True, precision: str = "bf16"):
+                 ns_steps: int = 5, nesterov: bool = True, precision: str = "bf16", gram_min_aspect: float = 2.0):
         defaults = dict(lr=lr, momentum=momentum, weight_decay=weight_decay, ns_steps=ns_steps,
-                        nesterov=nesterov, precision=precision)
+                        nesterov=nesterov, precision=precision, gram_min_aspect=gram_min_aspect)
         super().__init__(params, defaults)
         self._plans = {}
 
-    def _plan_for(self, key, descs, precision):
+    def _plan_for(self, key, descs, precision, gram_min_aspect):
         plan = self._plans.get(key)
         if plan is None:
-            plan = MuonPlan(descs, precision=precision)
+            plan = MuonPlan(descs, precision=precision, gram_min_aspect=gram_min_aspect)
             self._plans[key] = plan
         return plan
 
@@ -191,8 +195,8 @@ class Muon(_optimizer_base()):
                 if p.ndim != 2:
                     raise ValueError("Muon steps 2-D parameters only")
             descs = [(p.shape[0], p.shape[1], _dtype_code(p), _dtype_code(p.grad)) for p in ps]
-            key = (id(group), tuple(descs), group["precision"])
-            plan = self._plan_for(key, descs, group["precision"])
+            key = (id(group), tuple(descs), group["precision"], group["gram_min_aspect"])
+            plan = self._plan_for(key, descs, group["precision"], group["gram_min_aspect"])
             moms = []
             for p in ps:
                 st = self.state[p]

@@ -69,7 +69,8 @@ class ParityResult:
 def run_parity(wl: Workload, *, precision: str = "bf16", steps: Optional[int] = None,
                check: Optional[Sequence[int]] = None, ns_steps: Optional[int] = None,
                nesterov: Optional[bool] = None, wave_bytes: int = 0, device: str = "cuda:0",
-               plan: Optional[MuonPlan] = None, abc: Optional[Sequence[float]] = None) -> ParityResult:
+               plan: Optional[MuonPlan] = None, abc: Optional[Sequence[float]] = None,
+               gram_min_aspect: float = 2.0) -> ParityResult:
     """Runs ``steps`` HIP Muon steps over the whole workload and checks the
     matrices in ``check`` against the free-running oracle after every step."""
     steps = wl.steps if steps is None else steps
@@ -80,7 +81,8 @@ def run_parity(wl: Workload, *, precision: str = "bf16", steps: Optional[int] = 
     descs = [(m.rows, m.cols, m.param, m.grad) for m in wl.matrices]
     own_plan = plan is None
     if own_plan:
-        plan = MuonPlan(descs, precision=precision, wave_bytes=wave_bytes, abc=abc)
+        plan = MuonPlan(descs, precision=precision, wave_bytes=wave_bytes, abc=abc,
+                        gram_min_aspect=gram_min_aspect)
     abc = R.QUINTIC_ABC if abc is None else tuple(float(np.float32(v)) for v in abc)
     params, moms = make_state(torch, wl, device)
     torch.cuda.synchronize()

@@ -4,8 +4,10 @@
 // lower-triangular tile lists cover {(i, j): j <= i} and its full lists
 // cover every output tile of each of its matrices exactly once; workspace
 // regions inside a wave are 256-byte aligned and disjoint; the elementwise
-// tile prefix matches the matrices' tile counts.  Prints "OK" or the first
-// violation.
+// tile prefix matches the matrices' tile counts; the Gram-space form is
+// chosen exactly for bf16-class matrices with n >= aspect * m, and those keep
+// X0 alone plus five square buffers.  Prints "OK" or the first violation.
+// Arguments: precision, wave_bytes, gram_min_aspect.
 #include <algorithm>
 #include <cstdio>
 #include <cstdlib>
@@ -27,6 +29,7 @@ static int fail(const std::string& m) {
 int main(int argc, char** argv) {
   const int precision = argc > 1 ? std::atoi(argv[1]) : 0;
   const long long wave_bytes = argc > 2 ? std::atoll(argv[2]) : 0;
+  const float aspect = argc > 3 ? float(std::atof(argv[3])) : 2.f;
   std::vector<muon_matrix_desc> descs;
   long long r, c;
   while (std::scanf("%lld %lld", &r, &c) == 2) descs.push_back(muon_matrix_desc{r, c, MUON_BF16, MUON_BF16, MUON_F32, 0});
@@ -39,6 +42,7 @@ int main(int argc, char** argv) {
   o.eps = 1e-7f;
   o.small_m_threshold = 64;
   o.wave_bytes = wave_bytes;
+  o.gram_min_aspect = aspect;
   Plan p;
   std::string err;
   if (build_plan(descs.data(), int32_t(descs.size()), o, p, err) != MUON_OK) return fail("build_plan: " + err);
@@ -61,11 +65,17 @@ int main(int argc, char** argv) {
       const long long ab = h.m_pad * h.m_pad * esz;
       const std::pair<long long, long long> rs[] = {
           {h.x_off[0], xb}, {h.x_off[1], xb}, {h.xt_off[0], xb}, {h.xt_off[1], xb},
-          {h.a_off, ab},    {h.b_off, ab},    {h.o_off, h.m_pad * h.n_pad * 4}, {h.partial_off, h.ew_tiles * 4}};
-      if ((h.xt_off[0] < 0) != (h.fp32_ns == 0) || (h.xt_off[1] < 0) != (h.fp32_ns == 0))
+          {h.sq_off[0], ab},  {h.sq_off[1], ab},  {h.sq_off[2], ab}, {h.sq_off[3], ab}, {h.sq_off[4], ab},
+          {h.o_off, h.m_pad * h.n_pad * 4}, {h.partial_off, h.ew_tiles * 4}};
+      const bool want_gram = !h.fp32_ns && aspect > 0 && double(h.n) >= double(aspect) * double(h.m);
+      if (h.gram != int(want_gram) || d.gram != h.gram) return fail("Gram-space choice");
+      if ((h.x_off[1] < 0) != bool(h.gram)) return fail("second X buffer must exist exactly for Eq. 2");
+      if ((h.xt_off[0] < 0) != (h.fp32_ns == 0) || (h.xt_off[1] < 0) != (h.fp32_ns == 0 || h.gram))
         return fail("X^T buffers must exist exactly for the fp32 classes");
+      for (int q = 0; q < SQ_COUNT; ++q)
+        if ((h.sq_off[q] < 0) != (q >= 2 && !h.gram)) return fail("square buffers");
       for (const auto& rg : rs) {
-        if (rg.first < 0) continue;  // absent X^T buffer
+        if (rg.first < 0) continue;  // absent buffer
         if (rg.first % 256 != 0) return fail("unaligned region");
         regions.push_back(rg);
       }
@@ -94,8 +104,8 @@ int main(int argc, char** argv) {
       for (int s = 0; s < w.count; ++s) {
         const int pos = w.first + s;
         const MatHost& h = p.mats[size_t(p.order[size_t(pos)])];
-        if (h.kclass != cl.kclass) {
-          if (lower.count(pos) || full.count(pos)) return fail("tile of another class");
+        if (h.kclass != cl.kclass || h.gram != cl.gram) {
+          if (lower.count(pos) || full.count(pos)) return fail("tile of another class or form");
           continue;
         }
         const int tm = int(h.m_pad / tile), tn = int(h.n_pad / tile);
@@ -110,6 +120,19 @@ int main(int argc, char** argv) {
   }
   for (size_t i = 0; i < seen.size(); ++i)
     if (seen[i] != 1) return fail("matrix not in exactly one wave");
+  // launch count at k = 5: per wave 3 elementwise launches, per (class, form)
+  // group 15 (Eq. 2) or 1 + 5 + 4 + 8 + 1 = 19 (Gram space)
+  long long launches = 0;
+  for (const WaveHost& w : p.waves) {
+    std::set<std::pair<int, int>> groups;
+    for (int s = 0; s < w.count; ++s) {
+      const MatHost& h = p.mats[size_t(p.order[size_t(w.first + s)])];
+      groups.insert({h.kclass, h.gram});
+    }
+    launches += 3;
+    for (const auto& g : groups) launches += g.second ? 19 : 15;
+  }
+  if (launches != launches_per_step(p, 5)) return fail("launches per step");
   std::printf("OK %zu matrices %zu waves %zu tiles\n", descs.size(), p.waves.size(), p.h_tiles.size());
   return 0;
 }

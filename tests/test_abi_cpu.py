@@ -27,7 +27,7 @@ def test_every_declared_symbol_is_exported(lib):
     for name in names:
         assert hasattr(lib, name), name
         assert name in L.SIGNATURES, name
-    assert lib.muon_abi_version() == 1
+    assert lib.muon_abi_version() == 2
 
 
 def test_struct_layout_matches_c_compiler(tmp_path):

@@ -79,9 +79,11 @@ def test_moved_buffers_refresh_the_pointer_table():
     plan.close()
 
 
-def test_launch_timing_reports_every_kind():
-    wl = custom_workload([(1024, 4096), (96, 300)] * 2, seed=24)
-    plan = MuonPlan([(mm.rows, mm.cols, mm.param, mm.grad) for mm in wl.matrices])
+@pytest.mark.parametrize("aspect", [0.0, 2.0])
+def test_launch_timing_reports_every_kind(aspect):
+    shapes = ((1024, 4096), (96, 300))
+    wl = custom_workload(list(shapes) * 2, seed=24)
+    plan = MuonPlan([(mm.rows, mm.cols, mm.param, mm.grad) for mm in wl.matrices], gram_min_aspect=aspect)
     p, m = make_state(torch, wl, "cuda:0")
     g = make_grads(torch, wl, 0, "cuda:0")
     plan.set_timing(True)
@@ -89,15 +91,26 @@ def test_launch_timing_reports_every_kind():
     plan.set_timing(False)
     stats = plan.timing_read()
     kinds = {s["kind"] for s in stats}
-    assert kinds == {"momentum", "finalize", "gram", "poly", "bx", "apply"}
+    gram = aspect > 0  # both shapes are at least 3x wider than tall
+    assert kinds == {"momentum", "finalize", "gram", "poly", "bx", "apply"} | ({"symm"} if gram else set())
     info = plan.info()
-    assert sum(s["launches"] for s in stats) <= info["launches_per_step"]
     for s in stats:
         assert s["total_ms"] > 0
-        if s["kind"] in ("gram", "poly", "bx"):
+        if s["kind"] in ("gram", "poly", "bx", "symm"):
             assert s["algo_flops"] > 0
-    want = sum(3 * min(r, c) ** 2 * max(r, c) + min(r, c) ** 3 for r, c in ((1024, 4096), (96, 300))) * 2 * 5
+    k = 5
+    if gram:   # Eq. 4: 3 m^2 n once, 4k - 3 symmetric m^3 products
+        want = sum(3 * min(r, c) ** 2 * max(r, c) + (4 * k - 3) * min(r, c) ** 3 for r, c in shapes) * 2
+    else:      # Eq. 2: 3 m^2 n + m^3 per step
+        want = sum(3 * min(r, c) ** 2 * max(r, c) + min(r, c) ** 3 for r, c in shapes) * 2 * k
     got = sum(s["algo_flops"] for s in stats)
     assert abs(got - want) <= 1e-9 * want
+    assert abs(info["ns_flops_fixed"] + k * info["ns_flops_step"] - want) <= 1e-9 * want
+    # per kernel class: Eq. 2 launches Gram, A*A and B*X each step; Eq. 4 the
+    # Gram product and B*X once, P_i each step and 3 (k - 1) other m^3 products
+    per_class = {"gram": 1, "poly": k, "symm": 3 * (k - 1), "bx": 1} if gram else {"gram": k, "poly": k, "bx": k}
+    for s in stats:
+        if s["kernel_class"] is not None:
+            assert s["launches"] == per_class[s["kind"]], s
     assert plan.timing_read() == []     # records were dropped by the first read
     plan.close()

@@ -43,6 +43,50 @@ def test_ragged_shapes(precision, dtype):
     assert_parity(res, precision, "ragged")
 
 
+def test_ragged_shapes_eq2_only():
+    # the same set with the Gram-space form switched off: every bf16 matrix on Eq. 2
+    wl = custom_workload(RAGGED, seed=11)
+    res = run_parity(wl, precision="bf16", steps=2, gram_min_aspect=0.0)
+    assert_parity(res, "bf16", "ragged-eq2")
+
+
+GRAM_SET = [(256, 768), (768, 256), (320, 1000), (1000, 320), (512, 2048), (129, 4100), (1024, 2048),
+            (700, 1500), (300, 300), (2048, 1100)]
+
+
+@pytest.mark.parametrize("aspect", [2.0, 1.5])
+def test_gram_space_recurrence(aspect):
+    # Eq. 4 on the rectangular matrices of the set (all but the nearly square
+    # ones at aspect 2), Eq. 2 on the rest; both against the oracle.
+    wl = custom_workload(GRAM_SET, seed=21)
+    plan = MuonPlan([(m.rows, m.cols, m.param, m.grad) for m in wl.matrices], gram_min_aspect=aspect)
+    expect = [max(r, c) >= aspect * min(r, c) and min(r, c) > 64 for r, c in GRAM_SET]
+    got = [bool(plan.matrix_info(i)["gram_space"]) for i in range(wl.n)]
+    assert got == expect and plan.info()["n_gram"] == sum(expect)
+    _banner(f"gram-space aspect {aspect}: {sum(expect)} of {wl.n} matrices")
+    res = run_parity(wl, precision="bf16", steps=3, plan=plan)
+    _banner(f"gram-space aspect {aspect}: worst O {res.worst('o_rel'):.3e}")
+    plan.close()
+    assert_parity(res, "bf16", f"gram-space {aspect}")
+
+
+@pytest.mark.parametrize("ns_steps", [1, 2, 3, 7])
+def test_gram_space_step_counts(ns_steps):
+    # k = 1 has no P Q / G P products, k = 2 one of each; odd and even k end
+    # in different Q buffers.  The bf16 bar is stated for k = 5: every step
+    # amplifies the rounding error of small singular values (p'(0) = a =
+    # 3.4445), for Eq. 2 as much as for Eq. 4, so beyond k = 5 the Gram-space
+    # form is held to the Eq. 2 form's own error on the same input.
+    wl = custom_workload([(256, 1024), (1536, 512), (200, 900)], seed=22)
+    res = run_parity(wl, precision="bf16", steps=1, ns_steps=ns_steps)
+    if ns_steps <= 5:
+        assert_parity(res, "bf16", f"gram-space k={ns_steps}")
+        return
+    ref = run_parity(wl, precision="bf16", steps=1, ns_steps=ns_steps, gram_min_aspect=0.0)
+    for r, q in zip(res.reports, ref.reports):
+        assert r.o_rel <= max(TOL_O["bf16"], 1.25 * q.o_rel), (r.index, r.o_rel, q.o_rel)
+
+
 def test_ragged_shapes_small_waves():
     # every matrix in a wave of its own: same results as the single-wave plan
     wl = custom_workload(RAGGED, seed=12)

@@ -22,9 +22,10 @@ def plan_check(tmp_path_factory):
     return str(exe)
 
 
-def _run(exe, shapes, precision=0, wave_bytes=0):
+def _run(exe, shapes, precision=0, wave_bytes=0, aspect=2.0):
     inp = "\n".join(f"{r} {c}" for r, c in shapes)
-    out = subprocess.run([exe, str(precision), str(wave_bytes)], input=inp, capture_output=True, text=True)
+    out = subprocess.run([exe, str(precision), str(wave_bytes), str(aspect)], input=inp, capture_output=True,
+                         text=True)
     assert out.returncode == 0 and out.stdout.startswith("OK"), out.stdout + out.stderr
 
 
@@ -33,6 +34,7 @@ def test_workload_plans(plan_check, key):
     shapes = [(m.rows, m.cols) for m in get_workload(key).matrices]
     _run(plan_check, shapes)
     _run(plan_check, shapes, wave_bytes=1 << 30)
+    _run(plan_check, shapes, aspect=0.0)
 
 
 def test_ragged_and_random_plans(plan_check):
@@ -41,6 +43,8 @@ def test_ragged_and_random_plans(plan_check):
               (257, 513), (513, 257), (1000, 1000), (96, 4304), (1152, 1200), (2304, 9000), (4100, 4100)]
     _run(plan_check, ragged)
     _run(plan_check, ragged, precision=1)
+    _run(plan_check, ragged, aspect=1.0)
+    _run(plan_check, ragged, aspect=0.0)
     for trial in range(5):
         shapes = [(int(rng.integers(1, 3000)), int(rng.integers(1, 3000))) for _ in range(40)]
         _run(plan_check, shapes, wave_bytes=int(rng.integers(1, 4)) << 28)
