@@ -98,35 +98,51 @@ void emit_full(std::vector<TileEntry>& t, int32_t mat, int64_t tm, int64_t tn) {
   }
 }
 
-#ifndef MUON_LOWER_ORDER
-#define MUON_LOWER_ORDER 1
-#endif
-
-// Lower-triangular tile list (tj <= ti) of one matrix in dispatch order:
-// 8 x 8 blocks of output tiles, row-block by row-block.  In a full
-// off-diagonal block XCD x receives the 2 x 4 sub-block at rows 2*(x%4),
-// columns 4*(x/4), so each XCD's blocks share 6 operand panels; diagonal
-// and partial blocks are emitted row by row.
-void emit_lower(std::vector<TileEntry>& t, int32_t mat, int64_t tm) {
-  if (MUON_LOWER_ORDER == 0) {
-    for (int64_t ti = 0; ti < tm; ++ti)
-      for (int64_t tj = 0; tj <= ti; ++tj) t.push_back(TileEntry{mat, uint16_t(ti), uint16_t(tj)});
-    return;
-  }
+// Lower-triangular tiles (tj <= ti) of one matrix, cut into compact units:
+// each diagonal block of up to 8 x 8 tiles (a triangle) is one unit, and each
+// off-diagonal 8 x 8 block is two 4 x 8 units.  A unit reads at most 8 row
+// panels of each operand (a diagonal unit of a product with itself, 8 in
+// all), so the blocks of one XCD working through a unit share panels in
+// that XCD's L2.
+void lower_units(std::vector<std::vector<TileEntry>>& units, int32_t mat, int64_t tm) {
   for (int64_t r0 = 0; r0 < tm; r0 += 8) {
     const int64_t r1 = std::min(tm, r0 + 8);
-    for (int64_t c0 = 0; c0 <= r0; c0 += 8) {
-      if (c0 < r0 && r1 - r0 == 8 && t.size() % 8 == 0) {
-        for (int64_t b = 0; b < 64; ++b) {
-          const int64_t x = b % 8, k = b / 8;
-          t.push_back(TileEntry{mat, uint16_t(r0 + 2 * (x % 4) + k / 4), uint16_t(c0 + 4 * (x / 4) + k % 4)});
-        }
-      } else {
-        for (int64_t ti = r0; ti < r1; ++ti)
-          for (int64_t tj = c0; tj < std::min(c0 + 8, ti + 1); ++tj)
-            t.push_back(TileEntry{mat, uint16_t(ti), uint16_t(tj)});
+    for (int64_t c0 = 0; c0 < r0; c0 += 8)
+      for (int64_t h0 = r0; h0 < r1; h0 += 4) {
+        units.emplace_back();
+        for (int64_t ti = h0; ti < std::min(r1, h0 + 4); ++ti)
+          for (int64_t tj = c0; tj < c0 + 8; ++tj) units.back().push_back(TileEntry{mat, uint16_t(ti), uint16_t(tj)});
       }
+    units.emplace_back();
+    for (int64_t ti = r0; ti < r1; ++ti)
+      for (int64_t tj = r0; tj <= ti; ++tj) units.back().push_back(TileEntry{mat, uint16_t(ti), uint16_t(tj)});
+  }
+}
+
+// Dispatch order for a list of units.  Block b runs on XCD b % 8, so the
+// units are dealt to 8 per-XCD queues (each to the shortest so far) and the
+// queues are interleaved: position 8k + x holds the k-th tile of queue x.
+// Each XCD thus works through whole units, in the order they were listed.
+// When a queue runs dry near the end, the longest remaining one fills in.
+void interleave_units(std::vector<TileEntry>& out, const std::vector<std::vector<TileEntry>>& units) {
+  constexpr int kXcd = 8;
+  std::vector<std::vector<TileEntry>> q(kXcd);
+  size_t total = 0;
+  for (const auto& u : units) {
+    int best = 0;
+    for (int x = 1; x < kXcd; ++x)
+      if (q[size_t(x)].size() < q[size_t(best)].size()) best = x;
+    q[size_t(best)].insert(q[size_t(best)].end(), u.begin(), u.end());
+    total += u.size();
+  }
+  std::vector<size_t> pos(kXcd, 0);
+  for (size_t p = 0; p < total; ++p) {
+    int x = int(p % kXcd);
+    if (pos[size_t(x)] >= q[size_t(x)].size()) {
+      for (int y = 0; y < kXcd; ++y)
+        if (q[size_t(y)].size() - pos[size_t(y)] > q[size_t(x)].size() - pos[size_t(x)]) x = y;
     }
+    out.push_back(q[size_t(x)][pos[size_t(x)]++]);
   }
 }
 
@@ -338,6 +354,7 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
     for (int32_t kg = 0; kg < 2 * KC_COUNT; ++kg) {
       const int32_t kc = kg / 2, gram = kg % 2;
       std::vector<TileEntry> lower, full;
+      std::vector<std::vector<TileEntry>> units;
       const int64_t tile = kClasses[kc].tile;
       double fg = 0, fp = 0, fb = 0;
       for (int32_t s = 0; s < w.count; ++s) {
@@ -348,7 +365,7 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
         fg += m * m * nn;
         fp += m * m * m;
         fb += 2 * m * m * nn;
-        emit_lower(lower, pos, h.m_pad / tile);
+        lower_units(units, pos, h.m_pad / tile);
         emit_full(full, pos, h.m_pad / tile, h.n_pad / tile);
         const double t2 = double(tile) * double(tile);
         const int64_t tm = h.m_pad / tile;
@@ -357,6 +374,7 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
                           double(tm * (h.n_pad / tile)) * 2.0 * t2 * double(h.m_pad);
       }
       if (full.empty()) continue;
+      interleave_units(lower, units);
       ClassLaunch cl{};
       cl.kclass = kc;
       cl.gram = gram;
