@@ -43,10 +43,12 @@ def kernel_sources_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def read_traffic(kernel_key: str):
-    """HBM traffic of the dominant kernel from the committed rocprofv3 --pmc
-    summary, if it was taken on the current kernel sources."""
-    path = os.path.join(ROOT, "profiles", "traffic_summary.txt")
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "traffic_summary.txt")
+
+
+def read_traffic(kernel_key: str, path: str = TRAFFIC_SUMMARY):
+    """HBM bytes per launch of ``kernel_key`` from the committed rocprofv3
+    --pmc summary, if it was taken on the current kernel sources."""
     if not os.path.exists(path):
         return None
     vals = {}
@@ -56,31 +58,27 @@ def read_traffic(kernel_key: str):
                 continue
             k, v = line.split("=", 1)
             vals[k.strip()] = v.strip()
-    if vals.get("sources_sha256_16") != kernel_sources_hash() or vals.get("kernel") != kernel_key:
+    if vals.get("sources_sha256_16") != kernel_sources_hash():
         return None
     try:
-        return float(vals["hbm_bytes_per_launch"])
+        return float(vals[f"{kernel_key} hbm_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
 
 
-KERNEL_RE = [
+def _kernel_patterns():
+    pats = []
+    for e, cls in (("DF16b", "bf16"), ("f", "f32")):
+        for tile, wg in ((256, "2ELi4"), (128, "2ELi2"), (64, "2ELi2")):
+            if e == "f" and tile == 256:
+                continue
+            for stage, kind in enumerate(("gram", "poly", "bx", "symm")):
+                pats.append((rf"ns_gemm_kernelI{e}Li{tile}ELi{wg}ELi{stage}E", f"{kind}:{cls}_t{tile}"))
+    return pats
+
+
+KERNEL_RE = _kernel_patterns() + [
     # (regex on the mangled or plain kernel name, readable key)
-    (r"ns_gemm_kernelIDF16bLi256ELi2ELi4ELi0E", "gram:bf16_t256"),
-    (r"ns_gemm_kernelIDF16bLi256ELi2ELi4ELi1E", "poly:bf16_t256"),
-    (r"ns_gemm_kernelIDF16bLi256ELi2ELi4ELi2E", "bx:bf16_t256"),
-    (r"ns_gemm_kernelIDF16bLi128ELi2ELi2ELi0E", "gram:bf16_t128"),
-    (r"ns_gemm_kernelIDF16bLi128ELi2ELi2ELi1E", "poly:bf16_t128"),
-    (r"ns_gemm_kernelIDF16bLi128ELi2ELi2ELi2E", "bx:bf16_t128"),
-    (r"ns_gemm_kernelIDF16bLi64ELi2ELi2ELi0E", "gram:bf16_t64"),
-    (r"ns_gemm_kernelIDF16bLi64ELi2ELi2ELi1E", "poly:bf16_t64"),
-    (r"ns_gemm_kernelIDF16bLi64ELi2ELi2ELi2E", "bx:bf16_t64"),
-    (r"ns_gemm_kernelIfLi128ELi2ELi2ELi0E", "gram:f32_t128"),
-    (r"ns_gemm_kernelIfLi128ELi2ELi2ELi1E", "poly:f32_t128"),
-    (r"ns_gemm_kernelIfLi128ELi2ELi2ELi2E", "bx:f32_t128"),
-    (r"ns_gemm_kernelIfLi64ELi2ELi2ELi0E", "gram:f32_t64"),
-    (r"ns_gemm_kernelIfLi64ELi2ELi2ELi1E", "poly:f32_t64"),
-    (r"ns_gemm_kernelIfLi64ELi2ELi2ELi2E", "bx:f32_t64"),
     (r"momentum_kernel", "momentum"),
     (r"finalize_kernel", "finalize"),
     (r"apply_kernel", "apply"),
@@ -142,41 +140,39 @@ def rocprof_summary(root: str) -> str:
     return "\n".join(lines)
 
 
-def write_traffic_summary(root: str, kernel: str, copy_mib: int, command: str) -> str:
-    """Writes profiles/traffic_summary.txt for ``kernel`` from the FETCH_SIZE
-    and WRITE_SIZE passes under ``root``.  Each counter is scaled by the
-    ratio of the known size of the calibration copy to what the same counter
-    read for it."""
+def write_traffic_summary(root: str, kernels: str, copy_mib: int, command: str, path: str = TRAFFIC_SUMMARY) -> str:
+    """Writes profiles/traffic_summary.txt for the comma-separated kernel keys
+    from the FETCH_SIZE and WRITE_SIZE passes under ``root``.  Each counter is
+    scaled by the ratio of the known size of the calibration copy to what the
+    same counter read for it."""
     import csv
     import glob
     per = {}
-    for path in sorted(glob.glob(os.path.join(root, "**", "*counter_collection.csv"), recursive=True)):
-        for r in csv.DictReader(open(path)):
+    for csv_path in sorted(glob.glob(os.path.join(root, "**", "*counter_collection.csv"), recursive=True)):
+        for r in csv.DictReader(open(csv_path)):
             k = kernel_key(r["Kernel_Name"])
             c = per.setdefault(r["Counter_Name"], {}).setdefault(k, [0, 0.0])
             c[0] += 1
             c[1] += float(r["Counter_Value"])
     known_kib = copy_mib * 1024.0
-    out = {}
-    for cname in ("FETCH_SIZE", "WRITE_SIZE"):
-        copy_total = per[cname]["copy (device copy)"][1]
-        factor = known_kib / copy_total
-        n, v = per[cname][kernel]
-        out[cname] = (v / n, factor)
-    total = sum(kib * f * 1024.0 for kib, f in out.values())
+    factor = {c: known_kib / per[c]["copy (device copy)"][1] for c in ("FETCH_SIZE", "WRITE_SIZE")}
     lines = [
-        "# HBM traffic of one launch of the dominant kernel (rocprofv3 --pmc, one counter per run)",
+        "# HBM traffic per launch (rocprofv3 --pmc, one counter per run)",
         f"# command: {command}",
         f"# FETCH_SIZE and WRITE_SIZE scaled by a {copy_mib} MiB device-to-device copy in the same run",
-        f"kernel = {kernel}",
         f"sources_sha256_16 = {kernel_sources_hash()}",
-        f"fetch_kib_per_launch = {out['FETCH_SIZE'][0]:.0f}",
-        f"fetch_scale = {out['FETCH_SIZE'][1]:.4f}",
-        f"write_kib_per_launch = {out['WRITE_SIZE'][0]:.0f}",
-        f"write_scale = {out['WRITE_SIZE'][1]:.4f}",
-        f"hbm_bytes_per_launch = {total:.0f}",
+        f"fetch_scale = {factor['FETCH_SIZE']:.4f}",
+        f"write_scale = {factor['WRITE_SIZE']:.4f}",
     ]
-    path = os.path.join(ROOT, "profiles", "traffic_summary.txt")
+    for kernel in kernels.split(","):
+        kib = {}
+        for c in ("FETCH_SIZE", "WRITE_SIZE"):
+            n, v = per[c][kernel]
+            kib[c] = v / n
+        total = sum(kib[c] * factor[c] * 1024.0 for c in kib)
+        lines += [f"{kernel} fetch_kib_per_launch = {kib['FETCH_SIZE']:.0f}",
+                  f"{kernel} write_kib_per_launch = {kib['WRITE_SIZE']:.0f}",
+                  f"{kernel} hbm_bytes_per_launch = {total:.0f}"]
     with open(path, "w") as f:
         f.write("\n".join(lines) + "\n")
     return path
@@ -268,8 +264,9 @@ def main(argv=None) -> int:
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="run one device-to-device copy of this size first (HBM counter calibration)")
     ap.add_argument("--rocprof-summary", metavar="DIR", help="summarise rocprofv3 CSV output and exit")
-    ap.add_argument("--write-traffic", metavar="KERNEL",
-                    help="with --rocprof-summary: write profiles/traffic_summary.txt for this kernel key")
+    ap.add_argument("--write-traffic", metavar="KERNELS",
+                    help="with --rocprof-summary: write profiles/traffic_summary.txt for these comma-separated "
+                         "kernel keys")
     ap.add_argument("--traffic-command", default="", help="command recorded in the traffic summary")
     args = ap.parse_args(argv)
 

@@ -38,3 +38,30 @@ def test_gemm_algorithmic_bytes(lib, aspect):
         assert got[kind] == pytest.approx(2 * want[kind]), kind   # two matrices
     assert bench.gemm_algorithmic_bytes(plan, k, "bx", "f32_t64") == 0.0
     plan.close()
+
+
+def test_kernel_keys():
+    assert bench.kernel_key("_ZN4muon12_GLOBAL__N_114ns_gemm_kernelIDF16bLi256ELi2ELi4ELi3EEEvNS0_8GemmArgsE") \
+        == "symm:bf16_t256"
+    assert bench.kernel_key("_ZN4muon12_GLOBAL__N_114ns_gemm_kernelIfLi64ELi2ELi2ELi2EEEvNS0_8GemmArgsE") \
+        == "bx:f32_t64"
+    assert bench.kernel_key("muon::(anonymous namespace)::apply_kernel(...)") == "apply"
+
+
+def test_traffic_summary_round_trip(tmp_path):
+    # counter files as rocprofv3 writes them: a 1 MiB copy reads 512 KiB and
+    # writes 1024 KiB by the counters, so the scales are 2 and 1
+    sym = "_ZN4muon12_GLOBAL__N_114ns_gemm_kernelIDF16bLi256ELi2ELi4ELi3EEEvNS0_8GemmArgsE"
+    rows = [("__amd_rocclr_copyBuffer", "FETCH_SIZE", 512.0), ("__amd_rocclr_copyBuffer", "WRITE_SIZE", 1024.0),
+            (sym, "FETCH_SIZE", 100.0), (sym, "FETCH_SIZE", 300.0), (sym, "WRITE_SIZE", 50.0)]
+    d = tmp_path / "pmc"
+    d.mkdir()
+    with open(d / "run_counter_collection.csv", "w") as f:
+        f.write("Kernel_Name,Counter_Name,Counter_Value\n")
+        for k, c, v in rows:
+            f.write(f"{k},{c},{v}\n")
+    out = tmp_path / "traffic.txt"
+    bench.write_traffic_summary(str(tmp_path), "symm:bf16_t256", 1, "cmd", path=str(out))
+    got = bench.read_traffic("symm:bf16_t256", path=str(out))
+    assert got == pytest.approx((200.0 * 2 + 50.0 * 1) * 1024)
+    assert bench.read_traffic("bx:bf16_t256", path=str(out)) is None
