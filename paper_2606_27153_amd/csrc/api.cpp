@@ -183,7 +183,8 @@ muon_status step_impl(muon_plan plan, void* const* params, const void* const* gr
     e = run(MUON_KERNEL_FINALIZE, -1, 0.0, 0.0, [&] { return launch_finalize(p, w, ws, s, stream); });
     if (e != hipSuccess) return hip_fail(e, "finalize kernel launch");
     auto gemm = [&](const ClassLaunch& cl, int32_t stage, int32_t kind, const GemmStep& g) {
-      const double fl = kind == MUON_KERNEL_GRAM ? cl.flops_gram : kind == MUON_KERNEL_BX ? cl.flops_bx : cl.flops_poly;
+      const double fl = (kind == MUON_KERNEL_GRAM ? cl.flops_gram : kind == MUON_KERNEL_BX ? cl.flops_bx : cl.flops_poly) *
+                        (g.pair ? 2.0 : 1.0);
       return run(kind, cl.kclass, fl, 0.0, [&] { return launch_ns_gemm(p, w, cl, stage, g, ws, stream); });
     };
     // Eq. 2: per step A = s^2 X X^T, B = b A + c A A, X' = s (a X + B X).
@@ -212,7 +213,8 @@ muon_status step_impl(muon_plan plan, void* const* params, const void* const* gr
     // Gram space (Eq. 4): G0 = s^2 X0 X0^T; per step P_i = a I + b G + c G^2
     // (as c (G G + b/c G + a/c I)); Q_{i+1} = P_i Q_i (Q_1 = P_0, which is
     // written straight into Q0); R = G P_i and G <- P_i R except after the
-    // last step; finally O = s Q_k X0.
+    // last step; finally O = s Q_k X0.  P Q and G P only need P_i, so they
+    // share one launch.
     for (const ClassLaunch& cl : w.launches) {
       if (!cl.gram || ns_steps == 0) continue;
       e = gemm(cl, ST_GRAM, MUON_KERNEL_GRAM, GemmStep{1, 0, 0, SQ_A, SQ_A, SQ_A, 0.f, 0.f, 1.f});
@@ -220,13 +222,20 @@ muon_status step_impl(muon_plan plan, void* const* params, const void* const* gr
       for (int32_t it = 0; it < ns_steps; ++it) {
         const int32_t pbuf = it == 0 ? SQ_Q0 : SQ_B;
         e = gemm(cl, ST_POLY, MUON_KERNEL_POLY, GemmStep{0, 0, 0, SQ_A, SQ_A, pbuf, s.b / s.c, s.a / s.c, s.c});
-        if (e == hipSuccess && it > 0)
-          e = gemm(cl, ST_SYM, MUON_KERNEL_SYMM,
-                   GemmStep{0, 0, 0, SQ_B, (it - 1) & 1 ? SQ_Q1 : SQ_Q0, it & 1 ? SQ_Q1 : SQ_Q0, 0.f, 0.f, 1.f});
-        if (e == hipSuccess && it + 1 < ns_steps) {
-          e = gemm(cl, ST_SYM, MUON_KERNEL_SYMM, GemmStep{0, 0, 0, SQ_A, pbuf, SQ_R, 0.f, 0.f, 1.f});
-          if (e == hipSuccess) e = gemm(cl, ST_SYM, MUON_KERNEL_SYMM, GemmStep{0, 0, 0, pbuf, SQ_R, SQ_A, 0.f, 0.f, 1.f});
+        const GemmStep qu{0, 0, 0, SQ_B, (it - 1) & 1 ? SQ_Q1 : SQ_Q0, it & 1 ? SQ_Q1 : SQ_Q0, 0.f, 0.f, 1.f};
+        GemmStep gr{0, 0, 0, SQ_A, pbuf, SQ_R, 0.f, 0.f, 1.f};
+        const bool need_qu = it > 0, need_gr = it + 1 < ns_steps;
+        if (e == hipSuccess && need_qu && need_gr) {
+          gr.pair = 1;
+          gr.l2 = qu.l;
+          gr.r2 = qu.r;
+          gr.out2 = qu.out;
+          e = gemm(cl, ST_SYM, MUON_KERNEL_SYMM, gr);
+        } else if (e == hipSuccess && (need_qu || need_gr)) {
+          e = gemm(cl, ST_SYM, MUON_KERNEL_SYMM, need_qu ? qu : gr);
         }
+        if (e == hipSuccess && need_gr)
+          e = gemm(cl, ST_SYM, MUON_KERNEL_SYMM, GemmStep{0, 0, 0, pbuf, SQ_R, SQ_A, 0.f, 0.f, 1.f});
         if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
       }
       const int32_t qk = (ns_steps - 1) & 1 ? SQ_Q1 : SQ_Q0;

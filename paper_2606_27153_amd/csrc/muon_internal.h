@@ -170,7 +170,9 @@ int launch_apply(const Plan& p, const WaveHost& w, char* ws, const StepScalars& 
 //   ST_GRAM  sq[out] = oscale * s^2 * X X^T            (X = x[pin])
 //   ST_POLY  sq[out] = oscale * (L L + fcoef * L + diag * I),  L = sq[l]
 //   ST_BX    X' or O = s * (sq[l] X + fcoef * X)        (all tiles)
-//   ST_SYM   sq[out] = sq[l] sq[r]                      (a product known to be symmetric)
+//   ST_SYM   sq[out] = sq[l] sq[r]                      (a product known to be symmetric;
+//                                                         with `pair`, also sq[out2] = sq[l2] sq[r2]
+//                                                         in the same launch)
 // s is the Frobenius scale when `first` is set, else 1; `last` makes ST_BX
 // write O instead of x[pin ^ 1].
 enum Stage : int32_t { ST_GRAM = 0, ST_POLY = 1, ST_BX = 2, ST_SYM = 3 };
@@ -178,6 +180,8 @@ struct GemmStep {
   int32_t first, pin, last;
   int32_t l, r, out;          // SqBuf indices
   float fcoef, diag, oscale;
+  int32_t pair = 0;           // ST_SYM: a second product over the same tiles
+  int32_t l2 = 0, r2 = 0, out2 = 0;
 };
 int launch_ns_gemm(const Plan& p, const WaveHost& w, const ClassLaunch& cl, int32_t stage, const GemmStep& g,
                    char* ws, void* stream);

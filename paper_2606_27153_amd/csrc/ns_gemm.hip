@@ -58,6 +58,9 @@ struct GemmArgs {
   int32_t pin;     // ping-pong pair of X read by ST_GRAM / ST_BX
   int32_t last;    // ST_BX writes O
   int32_t l, r, out;  // square-buffer indices (SqBuf)
+  // ST_SYM may carry a second product over the same tiles: blocks from
+  // `split` on compute sq[out2] = sq[l2] sq[r2] (tile index minus split).
+  int32_t l2, r2, out2, split;
 };
 
 // 16-byte chunk c of LDS row r (128-byte rows) lives at chunk position
@@ -484,7 +487,9 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
   __shared__ __attribute__((aligned(1024))) char stage0[2 * C::OPB];
   __shared__ __attribute__((aligned(1024))) char stage1[2 * C::OPB];
 
-  const TileEntry te = args.tiles[blockIdx.x];
+  const bool second = STAGE == ST_SYM && int(blockIdx.x) >= args.split;
+  const TileEntry te = args.tiles[second ? int(blockIdx.x) - args.split : int(blockIdx.x)];
+  const int32_t bl = second ? args.l2 : args.l, br = second ? args.r2 : args.r, bo = second ? args.out2 : args.out;
   const MatDev& d = args.mats[te.mat];
   if (args.flag[d.slot]) return;  // all-zero update: O is never read
 
@@ -504,10 +509,10 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
     opb = x + int64_t(tj) * TILE * K;
   } else if (STAGE == ST_POLY || STAGE == ST_SYM) {
     K = mp;
-    opa = reinterpret_cast<const E*>(args.ws + d.sq_off[args.l]) + int64_t(ti) * TILE * K;
-    opb = reinterpret_cast<const E*>(args.ws + d.sq_off[STAGE == ST_POLY ? args.l : args.r]) + int64_t(tj) * TILE * K;
+    opa = reinterpret_cast<const E*>(args.ws + d.sq_off[bl]) + int64_t(ti) * TILE * K;
+    opb = reinterpret_cast<const E*>(args.ws + d.sq_off[STAGE == ST_POLY ? bl : br]) + int64_t(tj) * TILE * K;
   } else {
-    const E* b = reinterpret_cast<const E*>(args.ws + d.sq_off[args.l]);
+    const E* b = reinterpret_cast<const E*>(args.ws + d.sq_off[bl]);
     K = mp;
     opa = b + int64_t(ti) * TILE * K;
     if (TRB) {
@@ -636,7 +641,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
   int64_t ld_r = mp;
   bool rows_needed = true;
   if (STAGE != ST_BX) {
-    out_t = reinterpret_cast<E*>(args.ws + d.sq_off[args.out]);
+    out_t = reinterpret_cast<E*>(args.ws + d.sq_off[bo]);
     out_r = out_t;
     rows_needed = ti != tj;  // a diagonal tile is complete with one store
   } else {
@@ -707,6 +712,7 @@ int launch_ns_gemm(const Plan& p, const WaveHost& w, const ClassLaunch& cl, int3
   const bool full = stage == ST_BX;
   g.tiles = p.d_tiles + (full ? cl.full_off : cl.lower_off);
   const unsigned nblocks = unsigned(full ? cl.n_full : cl.n_lower);
+  const unsigned grid = stage == ST_SYM && gs.pair ? 2 * nblocks : nblocks;
   g.ws = ws;
   g.scale = reinterpret_cast<const float*>(ws + w.scale_off);
   g.flag = reinterpret_cast<const int32_t*>(ws + w.flag_off);
@@ -719,14 +725,18 @@ int launch_ns_gemm(const Plan& p, const WaveHost& w, const ClassLaunch& cl, int3
   g.l = gs.l;
   g.r = gs.r;
   g.out = gs.out;
+  g.l2 = gs.l2;
+  g.r2 = gs.r2;
+  g.out2 = gs.out2;
+  g.split = gs.pair ? int32_t(nblocks) : INT32_MAX;
   if (nblocks == 0) return 0;
   hipStream_t st = hipStream_t(stream);
   switch (cl.kclass) {
-    case KC_BF16_256: return launch_stage<__bf16, 256, 2, 4>(stage, nblocks, g, st);
-    case KC_BF16_128: return launch_stage<__bf16, 128, 2, 2>(stage, nblocks, g, st);
-    case KC_BF16_64: return launch_stage<__bf16, 64, 2, 2>(stage, nblocks, g, st);
-    case KC_F32_128: return launch_stage<float, 128, 2, 2>(stage, nblocks, g, st);
-    case KC_F32_64: return launch_stage<float, 64, 2, 2>(stage, nblocks, g, st);
+    case KC_BF16_256: return launch_stage<__bf16, 256, 2, 4>(stage, grid, g, st);
+    case KC_BF16_128: return launch_stage<__bf16, 128, 2, 2>(stage, grid, g, st);
+    case KC_BF16_64: return launch_stage<__bf16, 64, 2, 2>(stage, grid, g, st);
+    case KC_F32_128: return launch_stage<float, 128, 2, 2>(stage, grid, g, st);
+    case KC_F32_64: return launch_stage<float, 64, 2, 2>(stage, grid, g, st);
     default: return -1;
   }
 }

@@ -152,12 +152,13 @@ const ClassInfo& class_info(int32_t kc) { return kClasses[kc]; }
 
 int64_t launches_per_step(const Plan& p, int32_t ns_steps) {
   // Eq. 2: Gram, A*A and B*X per step.  Gram space: the Gram product and
-  // B*X once, P_i per step, and P Q, G P, P (G P) on all but one step.
+  // B*X once, P_i per step, P Q and G P (one launch when both are due) and
+  // P (G P) on all but one step: 3k + 1 launches for k >= 2.
   int64_t n = 0;
   const int64_t k = ns_steps;
   for (const auto& w : p.waves) {
     n += 3;  // momentum, finalize, apply
-    for (const auto& cl : w.launches) n += cl.gram ? (k > 0 ? 4 * k - 1 : 0) : 3 * k;
+    for (const auto& cl : w.launches) n += cl.gram ? (k > 1 ? 3 * k + 1 : 3 * k) : 3 * k;
   }
   return n;
 }

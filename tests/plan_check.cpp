@@ -121,7 +121,8 @@ int main(int argc, char** argv) {
   for (size_t i = 0; i < seen.size(); ++i)
     if (seen[i] != 1) return fail("matrix not in exactly one wave");
   // launch count at k = 5: per wave 3 elementwise launches, per (class, form)
-  // group 15 (Eq. 2) or 1 + 5 + 4 + 8 + 1 = 19 (Gram space)
+  // group 15 (Eq. 2) or 1 Gram + 5 P_i + (G P | P Q) 4 + P Q 1 + P (G P) 4
+  // + 1 B*X = 16 (Gram space)
   long long launches = 0;
   for (const WaveHost& w : p.waves) {
     std::set<std::pair<int, int>> groups;
@@ -130,7 +131,7 @@ int main(int argc, char** argv) {
       groups.insert({h.kclass, h.gram});
     }
     launches += 3;
-    for (const auto& g : groups) launches += g.second ? 19 : 15;
+    for (const auto& g : groups) launches += g.second ? 16 : 15;
   }
   if (launches != launches_per_step(p, 5)) return fail("launches per step");
   std::printf("OK %zu matrices %zu waves %zu tiles\n", descs.size(), p.waves.size(), p.h_tiles.size());

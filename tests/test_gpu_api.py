@@ -107,8 +107,9 @@ def test_launch_timing_reports_every_kind(aspect):
     assert abs(got - want) <= 1e-9 * want
     assert abs(info["ns_flops_fixed"] + k * info["ns_flops_step"] - want) <= 1e-9 * want
     # per kernel class: Eq. 2 launches Gram, A*A and B*X each step; Eq. 4 the
-    # Gram product and B*X once, P_i each step and 3 (k - 1) other m^3 products
-    per_class = {"gram": 1, "poly": k, "symm": 3 * (k - 1), "bx": 1} if gram else {"gram": k, "poly": k, "bx": k}
+    # Gram product and B*X once, P_i each step and 3 (k - 1) other m^3
+    # products in 2k - 1 launches (G P and P Q share one when both are due)
+    per_class = {"gram": 1, "poly": k, "symm": 2 * k - 1, "bx": 1} if gram else {"gram": k, "poly": k, "bx": k}
     for s in stats:
         if s["kernel_class"] is not None:
             assert s["launches"] == per_class[s["kind"]], s
