@@ -223,14 +223,16 @@ def cpu_baseline(wl, budget_s: float):
                        + "; ".join(sampled) + "), scaled by bucket counts to the whole set")}
 
 
-def gemm_algorithmic_bytes(plan, k: int, kind: str, kclass: str) -> float:
+def gemm_algorithmic_bytes(plan, k: int, kind: str, kclass: str, param_bytes) -> float:
     """HBM bytes one muon_step must move for the launches of one GEMM kind and
     kernel class, each operand read once and each output written once:
       Eq. 2, per step:  Gram  read X, write A;  A*A  read A, write B;
-                        B*X   read B and X, write X' (O, fp32, on the last step)
+                        B*X   read B and X, write X' (on the last step read
+                              and write the parameters W instead)
       Gram space:       Gram  read X0, write G (once);  P_i  read G, write P (k times);
                         m^3 products  read two, write one (3 (k - 1) times);
-                        B*X   read Q and X0, write O (once)."""
+                        B*X   read Q and X0, read and write W (once).
+    param_bytes[i] is the element size of matrix i's parameters."""
     from paper_2606_27153_amd import _lib as L
     total = 0.0
     for i in range(plan.n):
@@ -239,12 +241,13 @@ def gemm_algorithmic_bytes(plan, k: int, kind: str, kclass: str) -> float:
             continue
         m, n = float(mi["m"]), float(mi["n"])
         e = 4.0 if mi["fp32_ns"] else 2.0
+        w = 2.0 * param_bytes[i] * m * n
         if mi["gram_space"]:
             per = {"gram": e * (m * n + m * m), "poly": k * 2 * e * m * m, "symm": (k - 1) * 3 * 3 * e * m * m,
-                   "bx": e * (m * m + m * n) + 4.0 * m * n}
+                   "bx": e * (m * m + m * n) + w}
         else:
             per = {"gram": k * e * (m * n + m * m), "poly": k * 2 * e * m * m, "symm": 0.0,
-                   "bx": k * e * (m * m + m * n) + (k - 1) * e * m * n + 4.0 * m * n}
+                   "bx": k * e * (m * m + m * n) + (k - 1) * e * m * n + w}
         total += per[kind]
     return total
 
@@ -370,7 +373,8 @@ def main(argv=None) -> int:
     roof["traffic"] = None if traffic is None else round(traffic)
     if dom["kind"] in GEMM_KINDS:
         launches_per_step = dom["launches"] / args.steps
-        alg = gemm_algorithmic_bytes(plan, wl.ns_steps, dom["kind"], dom["kernel_class"])
+        alg = gemm_algorithmic_bytes(plan, wl.ns_steps, dom["kind"], dom["kernel_class"],
+                                     [2 if m.param == "bf16" else 4 for m in wl.matrices])
         roof["algorithmic_bytes"] = round(alg / launches_per_step)
         roof["flop_per_byte"] = round(dom["algo_flops"] / dom["launches"] / roof["algorithmic_bytes"], 1)
         if traffic is not None:

@@ -204,12 +204,13 @@ MUON_API muon_status muon_step_debug(muon_plan plan, void* const* params, const 
  * afterwards.  Flops and bytes are the algorithmic work of each launch:
  *   MUON_KERNEL_GRAM  m^2 n flops per matrix (half of the symmetric X X^T)
  *   MUON_KERNEL_POLY  m^3 flops (half of the symmetric A*A)
- *   MUON_KERNEL_BX    2 m^2 n flops
+ *   MUON_KERNEL_BX    2 m^2 n flops (the last one also applies Eq. 1 to the
+ *                     parameters, reading and writing W instead of storing O)
  *   MUON_KERNEL_SYMM  m^3 flops (a symmetric m x m product of the Gram-space
  *                     recurrence: G P, P (G P) or P Q; the P_i product itself
  *                     counts as MUON_KERNEL_POLY)
  *   MUON_KERNEL_MOMENTUM  read G, read and write M, write X0 once
- *   MUON_KERNEL_APPLY     read W and O (fp32), write W
+ *   MUON_KERNEL_APPLY     only when ns_steps = 0: read W and X0, write W
  * counted for every matrix of the launch, also ones skipped for a zero
  * gradient.  Timing must be read on the thread that steps the plan. */
 typedef enum muon_kernel_kind {

@@ -185,7 +185,7 @@ muon_status step_impl(muon_plan plan, void* const* params, const void* const* gr
     auto gemm = [&](const ClassLaunch& cl, int32_t stage, int32_t kind, const GemmStep& g) {
       const double fl = (kind == MUON_KERNEL_GRAM ? cl.flops_gram : kind == MUON_KERNEL_BX ? cl.flops_bx : cl.flops_poly) *
                         (g.pair ? 2.0 : 1.0);
-      return run(kind, cl.kclass, fl, 0.0, [&] { return launch_ns_gemm(p, w, cl, stage, g, ws, stream); });
+      return run(kind, cl.kclass, fl, 0.0, [&] { return launch_ns_gemm(p, w, cl, stage, g, ws, s, stream); });
     };
     // Eq. 2: per step A = s^2 X X^T, B = b A + c A A, X' = s (a X + B X).
     // With c = 0 (the cubic iteration) the Gram stage writes B = b A itself.
@@ -242,8 +242,12 @@ muon_status step_impl(muon_plan plan, void* const* params, const void* const* gr
       e = gemm(cl, ST_BX, MUON_KERNEL_BX, GemmStep{1, 0, 1, qk, qk, qk, 0.f, 0.f, 1.f});
       if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
     }
-    e = run(MUON_KERNEL_APPLY, -1, 0.0, w.bytes_apply, [&] { return launch_apply(p, w, ws, s, stream); });
-    if (e != hipSuccess) return hip_fail(e, "apply kernel launch");
+    // With k >= 1 the last B*X launch applied the update (zero-gradient
+    // matrices included); with k = 0 the update is O = s*u.
+    if (ns_steps == 0) {
+      e = run(MUON_KERNEL_APPLY, -1, 0.0, w.bytes_apply, [&] { return launch_apply(p, w, ws, s, stream); });
+      if (e != hipSuccess) return hip_fail(e, "apply kernel launch");
+    }
   }
   return ok();
 }

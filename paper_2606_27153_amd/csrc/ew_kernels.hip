@@ -8,12 +8,15 @@
 //                   Frobenius scale 1 / (||u||_F + eps) (deterministic; no
 //                   float atomics).  A zero sum marks the matrix as skipped.
 //  apply_kernel     W <- W*(1 - lr*wd) - lr*sqrt(max(1, rows/cols))*O  (Eq. 1
-//                   with decoupled weight decay), rounded to the param dtype.
+//                   with decoupled weight decay), rounded to the param dtype,
+//                   for k = 0 (O = s*u); otherwise the last B*X launch applies
+//                   the update in its epilogue.
 //
 // All three work on 64 x 64 tiles of the stored layout; a block finds its
 // matrix by binary search over the wave's tile prefix.
 #include <hip/hip_runtime.h>
 
+#include "ew_common.h"
 #include "muon_internal.h"
 
 namespace muon {
@@ -29,46 +32,6 @@ __device__ inline int find_slot(const int32_t* __restrict__ prefix, int count, i
     if (prefix[mid] <= bid) lo = mid; else hi = mid - 1;
   }
   return lo;
-}
-
-__device__ inline void load4(const void* base, int64_t idx, int dtype, bool vec, int valid, float v[4]) {
-  if (dtype == MUON_BF16) {
-    const __bf16* p = reinterpret_cast<const __bf16*>(base) + idx;
-    if (vec) {
-      const bf16x4 x = *reinterpret_cast<const bf16x4*>(p);
-      v[0] = float(x[0]); v[1] = float(x[1]); v[2] = float(x[2]); v[3] = float(x[3]);
-    } else {
-      for (int e = 0; e < 4; ++e) v[e] = e < valid ? float(p[e]) : 0.f;
-    }
-  } else {
-    const float* p = reinterpret_cast<const float*>(base) + idx;
-    if (vec) {
-      const f32x4 x = *reinterpret_cast<const f32x4*>(p);
-      v[0] = x[0]; v[1] = x[1]; v[2] = x[2]; v[3] = x[3];
-    } else {
-      for (int e = 0; e < 4; ++e) v[e] = e < valid ? p[e] : 0.f;
-    }
-  }
-}
-
-__device__ inline void store4(void* base, int64_t idx, int dtype, bool vec, int valid, const float v[4]) {
-  if (dtype == MUON_BF16) {
-    __bf16* p = reinterpret_cast<__bf16*>(base) + idx;
-    if (vec) {
-      bf16x4 x;
-      x[0] = __bf16(v[0]); x[1] = __bf16(v[1]); x[2] = __bf16(v[2]); x[3] = __bf16(v[3]);
-      *reinterpret_cast<bf16x4*>(p) = x;
-    } else {
-      for (int e = 0; e < valid; ++e) p[e] = __bf16(v[e]);
-    }
-  } else {
-    float* p = reinterpret_cast<float*>(base) + idx;
-    if (vec) {
-      *reinterpret_cast<f32x4*>(p) = f32x4{v[0], v[1], v[2], v[3]};
-    } else {
-      for (int e = 0; e < valid; ++e) p[e] = v[e];
-    }
-  }
 }
 
 // Stores 4 NS-operand values (bf16 or fp32) at an aligned position of a
@@ -176,11 +139,13 @@ __global__ __launch_bounds__(256) void finalize_kernel(const MatDev* __restrict_
   }
 }
 
+// Used only when no NS step runs (k = 0): O = s*u.  With k >= 1 the last
+// B*X launch applies the update in its epilogue.
 __global__ __launch_bounds__(256) void apply_kernel(const MatDev* __restrict__ mats,
                                                     const int32_t* __restrict__ prefix, int count,
                                                     const PtrEntry* __restrict__ ptrs, const char* __restrict__ ws,
                                                     const float* __restrict__ scale, const int32_t* __restrict__ flag,
-                                                    float lr, float decay, int ns_steps) {
+                                                    float lr, float decay) {
   const int bid = blockIdx.x;
   const int s = find_slot(prefix, count, bid);
   const MatDev& d = mats[s];
@@ -193,10 +158,9 @@ __global__ __launch_bounds__(256) void apply_kernel(const MatDev* __restrict__ m
   const bool vec = (cols & 3) == 0;
   const bool zero = flag[s] != 0;
   const float sc = scale[s];
-  const float lrs = lr * sqrtf(fmaxf(1.f, float(rows) / float(cols)));
-  const char* obuf = ws + d.o_off;
-  // ns_steps == 0: O = s*u, read from X (transposed for a tall bf16 matrix,
-  // whose stored-layout copy does not exist) or from the fp32 X^T.
+  const float lrs = update_lr(lr, rows, cols);
+  // u is read from X (transposed for a tall bf16 matrix, whose stored-layout
+  // copy does not exist) or from the fp32 X^T.
   const bool u_transposed = d.transposed && !d.x_f32;
   const char* ubuf = ws + (d.transposed && d.x_f32 ? d.xt_off[0] : d.x_off[0]);
 #pragma unroll
@@ -208,10 +172,7 @@ __global__ __launch_bounds__(256) void apply_kernel(const MatDev* __restrict__ m
     float o[4] = {0.f, 0.f, 0.f, 0.f};
     if (!zero) {
       const int64_t pidx = int64_t(r) * d.cols_pad + c;
-      if (ns_steps > 0) {
-        const f32x4 x = *reinterpret_cast<const f32x4*>(reinterpret_cast<const float*>(obuf) + pidx);
-        o[0] = x[0]; o[1] = x[1]; o[2] = x[2]; o[3] = x[3];
-      } else if (d.x_f32) {
+      if (d.x_f32) {
         const f32x4 x = *reinterpret_cast<const f32x4*>(reinterpret_cast<const float*>(ubuf) + pidx);
         o[0] = sc * x[0]; o[1] = sc * x[1]; o[2] = sc * x[2]; o[3] = sc * x[3];
       } else if (!u_transposed) {
@@ -223,13 +184,7 @@ __global__ __launch_bounds__(256) void apply_kernel(const MatDev* __restrict__ m
         for (int e = 0; e < 4; ++e) o[e] = sc * float(xb[int64_t(c + e) * d.rows_pad + r]);
       }
     }
-    const int64_t idx = int64_t(r) * cols + c;
-    float w[4];
-    load4(pe.param, idx, d.param_dtype, vec, valid, w);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) w[e] = fmaf(-lrs, o[e], w[e] * decay);
-    store4(pe.param, idx, d.param_dtype, vec, valid, w);
-    if (pe.out) store4(pe.out, idx, MUON_F32, vec, valid, o);
+    apply4(pe, d.param_dtype, int64_t(r) * cols + c, vec, valid, o, lrs, decay);
   }
 }
 
@@ -254,7 +209,7 @@ int launch_apply(const Plan& p, const WaveHost& w, char* ws, const StepScalars& 
   hipLaunchKernelGGL(apply_kernel, dim3(unsigned(w.ew_tiles)), dim3(256), 0, hipStream_t(stream),
                      p.d_mats + w.first, p.d_prefix + w.prefix_off, w.count, p.d_ptrs, ws,
                      reinterpret_cast<const float*>(ws + w.scale_off),
-                     reinterpret_cast<const int32_t*>(ws + w.flag_off), s.lr, s.decay, s.ns_steps);
+                     reinterpret_cast<const int32_t*>(ws + w.flag_off), s.lr, s.decay);
   return check_launch();
 }
 

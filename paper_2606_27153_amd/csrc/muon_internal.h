@@ -48,7 +48,6 @@ struct MatDev {
   int64_t x_off[2];    // oriented X, m_pad x n_pad (ping-pong pair p; Gram-space: X0 only)
   int64_t xt_off[2];   // X^T, n_pad x m_pad (fp32 classes only)
   int64_t sq_off[SQ_COUNT];
-  int64_t o_off;       // fp32 O in stored layout, rows_pad x cols_pad
   int64_t partial_off; // fp32 partial sums of squares, one per EW tile
   int32_t rows, cols;          // stored shape
   int32_t rows_pad, cols_pad;  // stored shape padded to the tile
@@ -85,7 +84,7 @@ struct MatHost {
   int32_t param_dtype, grad_dtype, momentum_dtype;
   int32_t wave, slot, bucket;
   int64_t ew_tiles;
-  int64_t x_off[2], xt_off[2], sq_off[SQ_COUNT], o_off, partial_off;
+  int64_t x_off[2], xt_off[2], sq_off[SQ_COUNT], partial_off;
   int64_t ws_bytes;    // workspace bytes of this matrix within its wave
 };
 
@@ -174,7 +173,8 @@ int launch_apply(const Plan& p, const WaveHost& w, char* ws, const StepScalars& 
 //                                                         with `pair`, also sq[out2] = sq[l2] sq[r2]
 //                                                         in the same launch)
 // s is the Frobenius scale when `first` is set, else 1; `last` makes ST_BX
-// write O instead of x[pin ^ 1].
+// apply the update of Eq. 1 to the caller's parameters (and write O to the
+// debug buffer, if any) instead of writing x[pin ^ 1].
 enum Stage : int32_t { ST_GRAM = 0, ST_POLY = 1, ST_BX = 2, ST_SYM = 3 };
 struct GemmStep {
   int32_t first, pin, last;
@@ -184,6 +184,6 @@ struct GemmStep {
   int32_t l2 = 0, r2 = 0, out2 = 0;
 };
 int launch_ns_gemm(const Plan& p, const WaveHost& w, const ClassLaunch& cl, int32_t stage, const GemmStep& g,
-                   char* ws, void* stream);
+                   char* ws, const StepScalars& s, void* stream);
 
 }  // namespace muon

@@ -35,6 +35,7 @@
 // by global_load_lds_dwordx4 (no staging registers).
 #include <hip/hip_runtime.h>
 
+#include "ew_common.h"
 #include "muon_internal.h"
 
 namespace muon {
@@ -61,6 +62,10 @@ struct GemmArgs {
   // ST_SYM may carry a second product over the same tiles: blocks from
   // `split` on compute sq[out2] = sq[l2] sq[r2] (tile index minus split).
   int32_t l2, r2, out2, split;
+  // ST_BX with `last`: the update of Eq. 1 is applied to the caller's
+  // parameters from the epilogue
+  const PtrEntry* ptrs;
+  float lr, decay;
 };
 
 // 16-byte chunk c of LDS row r (128-byte rows) lives at chunk position
@@ -328,6 +333,172 @@ __device__ __forceinline__ void store_t_via_lds(const f32x16 (&acc)[C::NBM][C::N
   }
 }
 
+// The last B*X applies the update instead of storing O: the fp32 result is
+// staged through the wave's LDS region, 16 oriented rows at a time, as for a
+// row (wide matrix) or a transposed (tall matrix) store, and every 16-byte
+// piece -- 4 consecutive elements of one stored row -- updates the caller's
+// parameters W (of element type P) in place, clipped to the unpadded
+// rows x cols: W <- RNE(W * decay - lrs * O); O also goes to the debug
+// buffer, if any.  All parameter loads of a pass are issued before its
+// stores (a store to W may not be moved above a later load of W, so
+// interleaving them would serialise the load latencies).
+template <typename P>
+__device__ __forceinline__ void load_w4(const P* w, bool vec, int valid, float v[4]) {
+  if (vec) {
+    const typename Vec4<P>::T x = *reinterpret_cast<const typename Vec4<P>::T*>(w);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = float(x[e]);
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = e < valid ? float(w[e]) : 0.f;
+  }
+}
+
+template <typename P>
+__device__ __forceinline__ void store_w4(P* w, bool vec, int valid, const float v[4]) {
+  if (vec) {
+    typename Vec4<P>::T x;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) x[e] = P(v[e]);
+    *reinterpret_cast<typename Vec4<P>::T*>(w) = x;
+  } else {
+    for (int e = 0; e < valid; ++e) w[e] = P(v[e]);
+  }
+}
+
+// One pass: pieces it = 0..NP-1 of this lane, whose LDS offset, stored row
+// and stored column come from `at`.
+template <typename P, int NP, class At>
+__device__ __forceinline__ void apply_pass(const char* region, const PtrEntry& pe, const MatDev& d, float lrs,
+                                           float decay, int lane, At at) {
+  P* wbase = reinterpret_cast<P*>(pe.param);
+  const bool vec = (d.cols & 3) == 0;
+  float w[NP][4];
+#pragma unroll
+  for (int it = 0; it < NP; ++it) {
+    int off;
+    int64_t row, col;
+    at(lane + 64 * it, off, row, col);
+    if (row < d.rows && col < d.cols)
+      load_w4<P>(wbase + row * d.cols + col, vec, int(d.cols - col < 4 ? d.cols - col : 4), w[it]);
+  }
+  __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the staged values have landed
+#pragma unroll
+  for (int it = 0; it < NP; ++it) {
+    int off;
+    int64_t row, col;
+    at(lane + 64 * it, off, row, col);
+    if (row >= d.rows || col >= d.cols) continue;
+    const int valid = int(d.cols - col < 4 ? d.cols - col : 4);
+    const f32x4 v = *reinterpret_cast<const f32x4*>(region + off);
+    const float o[4] = {v[0], v[1], v[2], v[3]};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) w[it][e] = fmaf(-lrs, o[e], w[it][e] * decay);
+    store_w4<P>(wbase + row * d.cols + col, vec, valid, w[it]);
+    if (pe.out) store_w4<float>(pe.out + row * d.cols + col, vec, valid, o);
+  }
+  __builtin_amdgcn_s_waitcnt(0xc07f);  // reads done before the region is rewritten
+}
+
+// Passes of 16 oriented rows over the wave tile.  Wide matrix (TRANS
+// false): LDS row r is oriented (= stored) row r of the pass.  Tall matrix:
+// LDS row j holds the pass's 16 oriented rows of column j, i.e. 16
+// consecutive elements of stored row col0 + j.
+template <class C, bool TRANS>
+struct ApplyLay {
+  static constexpr int ROWB = TRANS ? 64 : C::WTN * 4;            // LDS bytes per row
+  static constexpr int PPR = ROWB / 16;                           // 16-byte pieces per LDS row
+  static constexpr int NP = (TRANS ? C::WTN : 16) * PPR / 64;     // pieces per lane and pass
+  static constexpr int NPASS = 2 * C::NBM;
+  static_assert((TRANS ? C::WTN : 16) * ROWB <= C::WAVE_LDS && NP * 64 == (TRANS ? C::WTN : 16) * PPR,
+                "pass fits the region");
+  __device__ static __forceinline__ int loff(int r, int pc) {
+    return TRANS ? r * ROWB + ((pc ^ (r & 3)) << 4) : r * ROWB + pc * 16;
+  }
+  // LDS offset and stored position of piece `piece` of pass `pass`
+  __device__ static __forceinline__ void at(int pass, int piece, int64_t row0, int64_t col0, int& off, int64_t& row,
+                                            int64_t& col) {
+    const int r = piece / PPR, pc = piece % PPR;
+    off = loff(r, pc);
+    if (TRANS) {
+      row = col0 + r;                      // stored row = oriented column
+      col = row0 + 16 * pass + pc * 4;     // stored column = oriented row
+    } else {
+      row = row0 + 16 * pass + r;
+      col = col0 + pc * 4;
+    }
+  }
+  // writes pass `pass` (half hh of MFMA block row i) of acc to the region
+  __device__ static __forceinline__ void stage(const f32x16 (&acc)[C::NBM][C::NBN], char* region, int i, int hh,
+                                               int lane) {
+#pragma unroll
+    for (int j = 0; j < C::NBN; ++j)
+#pragma unroll
+      for (int g = 2 * hh; g < 2 * hh + 2; ++g) {
+        const int c = 8 * g + 4 * (lane >> 5) - 16 * hh;  // oriented row within the pass
+        if (TRANS) {
+          const int r = j * 32 + (lane & 31);
+          *reinterpret_cast<f32x4*>(region + loff(r, c >> 2)) =
+              f32x4{acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            *reinterpret_cast<float*>(region + (c + e) * ROWB + (j * 32 + (lane & 31)) * 4) = acc[i][j][4 * g + e];
+        }
+      }
+  }
+};
+
+template <class C, bool TRANS, typename P>
+__device__ __forceinline__ void apply_via_lds(const f32x16 (&acc)[C::NBM][C::NBN], char* region,
+                                              const PtrEntry& pe, const MatDev& d, float lrs, float decay,
+                                              int64_t row0, int64_t col0, int lane) {
+  using A = ApplyLay<C, TRANS>;
+  const int64_t srow_end = TRANS ? col0 + C::WTN : row0 + C::WTM;
+  const int64_t scol_end = TRANS ? row0 + C::WTM : col0 + C::WTN;
+  if (sizeof(P) == 2 && (d.cols & 3) == 0 && srow_end <= d.rows && scol_end <= d.cols) {
+    // whole wave tile inside W: every parameter load of the tile goes out
+    // before the first update, so their latencies overlap
+    typename Vec4<__bf16>::T w[A::NPASS][A::NP];
+    __bf16* wb = reinterpret_cast<__bf16*>(pe.param);
+#pragma unroll
+    for (int pass = 0; pass < A::NPASS; ++pass)
+#pragma unroll
+      for (int it = 0; it < A::NP; ++it) {
+        int off;
+        int64_t row, col;
+        A::at(pass, lane + 64 * it, row0, col0, off, row, col);
+        w[pass][it] = *reinterpret_cast<const typename Vec4<__bf16>::T*>(wb + row * d.cols + col);
+      }
+#pragma unroll
+    for (int pass = 0; pass < A::NPASS; ++pass) {
+      A::stage(acc, region, pass >> 1, pass & 1, lane);
+      __builtin_amdgcn_s_waitcnt(0xc07f);
+#pragma unroll
+      for (int it = 0; it < A::NP; ++it) {
+        int off;
+        int64_t row, col;
+        A::at(pass, lane + 64 * it, row0, col0, off, row, col);
+        const f32x4 v = *reinterpret_cast<const f32x4*>(region + off);
+        typename Vec4<__bf16>::T x;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[e] = __bf16(fmaf(-lrs, v[e], float(w[pass][it][e]) * decay));
+        *reinterpret_cast<typename Vec4<__bf16>::T*>(wb + row * d.cols + col) = x;
+        if (pe.out) *reinterpret_cast<f32x4*>(pe.out + row * d.cols + col) = v;
+      }
+      __builtin_amdgcn_s_waitcnt(0xc07f);
+    }
+    return;
+  }
+#pragma unroll
+  for (int pass = 0; pass < A::NPASS; ++pass) {
+    A::stage(acc, region, pass >> 1, pass & 1, lane);
+    apply_pass<P, A::NP>(region, pe, d, lrs, decay, lane, [&](int piece, int& off, int64_t& row, int64_t& col) {
+      A::at(pass, piece, row0, col0, off, row, col);
+    });
+  }
+}
+
 // ---------------------------------------------------------------------------
 // bf16 B*X reads its second operand straight from row-major X.  The slab of
 // X (64 K-rows x TILE columns) sits in LDS row-major; ds_read_b64_tr_b16
@@ -491,7 +662,10 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
   const TileEntry te = args.tiles[second ? int(blockIdx.x) - args.split : int(blockIdx.x)];
   const int32_t bl = second ? args.l2 : args.l, br = second ? args.r2 : args.r, bo = second ? args.out2 : args.out;
   const MatDev& d = args.mats[te.mat];
-  if (args.flag[d.slot]) return;  // all-zero update: O is never read
+  // An all-zero gradient has O = 0: its products are skipped, and the last
+  // B*X only applies the weight decay.
+  const bool zero = args.flag[d.slot] != 0;
+  if (zero && !(STAGE == ST_BX && args.last)) return;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
@@ -544,85 +718,87 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
   const bool FUSE = (STAGE == ST_POLY || STAGE == ST_BX) && args.fcoef != 0.f;
   const float fcoef = args.fcoef;
   const int frow0 = ti * TILE + wm * C::WTM;
-  if constexpr (TRB) {
-    const E* srca = lane_src<C>(opa, K, wid, lane);
-    const __bf16* srcb = lane_src_rows<C>(reinterpret_cast<const __bf16*>(opb), np, wid, lane);
-    int oa[4], ot[2 * C::NBN];
+  if (!zero) {
+    if constexpr (TRB) {
+      const E* srca = lane_src<C>(opa, K, wid, lane);
+      const __bf16* srcb = lane_src_rows<C>(reinterpret_cast<const __bf16*>(opb), np, wid, lane);
+      int oa[4], ot[2 * C::NBN];
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) oa[ks] = frag_off(wm * C::WTM, lane, ks);
-    tr_offsets<C>(wn, lane, ot);
-    bf16x8 fa0[C::NBM], fb0[C::NBN], fa1[C::NBM], fb1[C::NBN];
-    load_slab<C>(srca, K, 0, stage0, wid);
-    load_slab_rows<C>(srcb, np, 0, stage0 + C::OPB, wid);
-    wait_vm_all();
-    __syncthreads();
-    read_frags_tr<C>(stage0, stage0 + C::OPB, oa[0], ot, 0, fa0, fb0);
-    int kt = 0;
-    for (; kt + 2 <= nk; kt += 2) {
-      load_slab<C>(srca, K, kt + 1, stage1, wid);
-      load_slab_rows<C>(srcb, np, kt + 1, stage1 + C::OPB, wid);
-      slab_body_tr<C>(stage0, oa, ot, fa0, fb0, fa1, fb1, acc);
-      if (FUSE) fuse_input<C, E, true>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
+      for (int ks = 0; ks < 4; ++ks) oa[ks] = frag_off(wm * C::WTM, lane, ks);
+      tr_offsets<C>(wn, lane, ot);
+      bf16x8 fa0[C::NBM], fb0[C::NBN], fa1[C::NBM], fb1[C::NBN];
+      load_slab<C>(srca, K, 0, stage0, wid);
+      load_slab_rows<C>(srcb, np, 0, stage0 + C::OPB, wid);
       wait_vm_all();
       __syncthreads();
-      read_frags_tr<C>(stage1, stage1 + C::OPB, oa[0], ot, 0, fa0, fb0);
-      __builtin_amdgcn_sched_barrier(0);
-      if (kt + 2 < nk) {
-        load_slab<C>(srca, K, kt + 2, stage0, wid);
-        load_slab_rows<C>(srcb, np, kt + 2, stage0 + C::OPB, wid);
+      read_frags_tr<C>(stage0, stage0 + C::OPB, oa[0], ot, 0, fa0, fb0);
+      int kt = 0;
+      for (; kt + 2 <= nk; kt += 2) {
+        load_slab<C>(srca, K, kt + 1, stage1, wid);
+        load_slab_rows<C>(srcb, np, kt + 1, stage1 + C::OPB, wid);
+        slab_body_tr<C>(stage0, oa, ot, fa0, fb0, fa1, fb1, acc);
+        if (FUSE) fuse_input<C, E, true>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
+        wait_vm_all();
+        __syncthreads();
+        read_frags_tr<C>(stage1, stage1 + C::OPB, oa[0], ot, 0, fa0, fb0);
+        __builtin_amdgcn_sched_barrier(0);
+        if (kt + 2 < nk) {
+          load_slab<C>(srca, K, kt + 2, stage0, wid);
+          load_slab_rows<C>(srcb, np, kt + 2, stage0 + C::OPB, wid);
+        }
+        slab_body_tr<C>(stage1, oa, ot, fa0, fb0, fa1, fb1, acc);
+        if (FUSE) fuse_input<C, E, true>(stage1 + C::OPB, kt + 1, frow0, wn, lane, fcoef, acc);
+        wait_vm_all();
+        __syncthreads();
+        if (kt + 2 < nk) read_frags_tr<C>(stage0, stage0 + C::OPB, oa[0], ot, 0, fa0, fb0);
+        __builtin_amdgcn_sched_barrier(0);
       }
-      slab_body_tr<C>(stage1, oa, ot, fa0, fb0, fa1, fb1, acc);
-      if (FUSE) fuse_input<C, E, true>(stage1 + C::OPB, kt + 1, frow0, wn, lane, fcoef, acc);
-      wait_vm_all();
-      __syncthreads();
-      if (kt + 2 < nk) read_frags_tr<C>(stage0, stage0 + C::OPB, oa[0], ot, 0, fa0, fb0);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    if (kt < nk) {  // odd slab count: the last slab is in stage 0
-      slab_body_tr<C>(stage0, oa, ot, fa0, fb0, fa1, fb1, acc);
-      if (FUSE) fuse_input<C, E, true>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
-      __syncthreads();
-    }
-  } else {
-    const E* srca = lane_src<C>(opa, K, wid, lane);
-    const E* srcb = lane_src<C>(opb, K, wid, lane);
-    int oa[4], ob[4];
-  #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      oa[ks] = frag_off(wm * C::WTM, lane, ks);
-      ob[ks] = frag_off(wn * C::WTN, lane, ks);
-    }
-    typename Frag<E>::T fa0[C::NBM], fb0[C::NBN], fa1[C::NBM], fb1[C::NBN];
-    load_slab<C>(srca, K, 0, stage0, wid);
-    load_slab<C>(srcb, K, 0, stage0 + C::OPB, wid);
-    wait_vm_all();
-    __syncthreads();
-    read_frags<C, E>(stage0, stage0 + C::OPB, oa[0], ob[0], fa0, fb0);
-    int kt = 0;
-    for (; kt + 2 <= nk; kt += 2) {
-      load_slab<C>(srca, K, kt + 1, stage1, wid);
-      load_slab<C>(srcb, K, kt + 1, stage1 + C::OPB, wid);
-      slab_body<C, E>(stage0, oa, ob, fa0, fb0, fa1, fb1, acc);
-      if (FUSE) fuse_input<C, E, false>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
-      wait_vm_all();
-      __syncthreads();
-      read_frags<C, E>(stage1, stage1 + C::OPB, oa[0], ob[0], fa0, fb0);
-      __builtin_amdgcn_sched_barrier(0);
-      if (kt + 2 < nk) {
-        load_slab<C>(srca, K, kt + 2, stage0, wid);
-        load_slab<C>(srcb, K, kt + 2, stage0 + C::OPB, wid);
+      if (kt < nk) {  // odd slab count: the last slab is in stage 0
+        slab_body_tr<C>(stage0, oa, ot, fa0, fb0, fa1, fb1, acc);
+        if (FUSE) fuse_input<C, E, true>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
+        __syncthreads();
       }
-      slab_body<C, E>(stage1, oa, ob, fa0, fb0, fa1, fb1, acc);
-      if (FUSE) fuse_input<C, E, false>(stage1 + C::OPB, kt + 1, frow0, wn, lane, fcoef, acc);
+    } else {
+      const E* srca = lane_src<C>(opa, K, wid, lane);
+      const E* srcb = lane_src<C>(opb, K, wid, lane);
+      int oa[4], ob[4];
+    #pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        oa[ks] = frag_off(wm * C::WTM, lane, ks);
+        ob[ks] = frag_off(wn * C::WTN, lane, ks);
+      }
+      typename Frag<E>::T fa0[C::NBM], fb0[C::NBN], fa1[C::NBM], fb1[C::NBN];
+      load_slab<C>(srca, K, 0, stage0, wid);
+      load_slab<C>(srcb, K, 0, stage0 + C::OPB, wid);
       wait_vm_all();
       __syncthreads();
-      if (kt + 2 < nk) read_frags<C, E>(stage0, stage0 + C::OPB, oa[0], ob[0], fa0, fb0);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    if (kt < nk) {  // odd slab count: the last slab is in stage 0
-      slab_body<C, E>(stage0, oa, ob, fa0, fb0, fa1, fb1, acc);
-      if (FUSE) fuse_input<C, E, false>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
-      __syncthreads();
+      read_frags<C, E>(stage0, stage0 + C::OPB, oa[0], ob[0], fa0, fb0);
+      int kt = 0;
+      for (; kt + 2 <= nk; kt += 2) {
+        load_slab<C>(srca, K, kt + 1, stage1, wid);
+        load_slab<C>(srcb, K, kt + 1, stage1 + C::OPB, wid);
+        slab_body<C, E>(stage0, oa, ob, fa0, fb0, fa1, fb1, acc);
+        if (FUSE) fuse_input<C, E, false>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
+        wait_vm_all();
+        __syncthreads();
+        read_frags<C, E>(stage1, stage1 + C::OPB, oa[0], ob[0], fa0, fb0);
+        __builtin_amdgcn_sched_barrier(0);
+        if (kt + 2 < nk) {
+          load_slab<C>(srca, K, kt + 2, stage0, wid);
+          load_slab<C>(srcb, K, kt + 2, stage0 + C::OPB, wid);
+        }
+        slab_body<C, E>(stage1, oa, ob, fa0, fb0, fa1, fb1, acc);
+        if (FUSE) fuse_input<C, E, false>(stage1 + C::OPB, kt + 1, frow0, wn, lane, fcoef, acc);
+        wait_vm_all();
+        __syncthreads();
+        if (kt + 2 < nk) read_frags<C, E>(stage0, stage0 + C::OPB, oa[0], ob[0], fa0, fb0);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if (kt < nk) {  // odd slab count: the last slab is in stage 0
+        slab_body<C, E>(stage0, oa, ob, fa0, fb0, fa1, fb1, acc);
+        if (FUSE) fuse_input<C, E, false>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
+        __syncthreads();
+      }
     }
   }
 
@@ -672,11 +848,19 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
 #pragma unroll
       for (int q = 0; q < 16; ++q) acc[i][j][q] *= mul;
   if (STAGE == ST_BX && args.last) {
-    float* o = reinterpret_cast<float*>(args.ws + d.o_off);
-    if (d.transposed)
-      store_t_via_lds<C, float>(acc, region, o, mp, row0, col0, lane);
-    else
-      store_rows_via_lds<C, float>(acc, region, o, np, row0, col0, lane);
+    const PtrEntry pe = args.ptrs[d.index];
+    const float lrs = update_lr(args.lr, d.rows, d.cols);
+    if (d.param_dtype == MUON_BF16) {
+      if (d.transposed)
+        apply_via_lds<C, true, __bf16>(acc, region, pe, d, lrs, args.decay, row0, col0, lane);
+      else
+        apply_via_lds<C, false, __bf16>(acc, region, pe, d, lrs, args.decay, row0, col0, lane);
+    } else {
+      if (d.transposed)
+        apply_via_lds<C, true, float>(acc, region, pe, d, lrs, args.decay, row0, col0, lane);
+      else
+        apply_via_lds<C, false, float>(acc, region, pe, d, lrs, args.decay, row0, col0, lane);
+    }
   } else {
     if (!TRB) store_t_via_lds<C, E>(acc, region, out_t, mp, row0, col0, lane);
     if (rows_needed) store_rows_via_lds<C, E>(acc, region, out_r, ld_r, row0, col0, lane);
@@ -706,7 +890,7 @@ int launch_stage(int32_t stage, unsigned nblocks, const GemmArgs& g, hipStream_t
 }  // namespace
 
 int launch_ns_gemm(const Plan& p, const WaveHost& w, const ClassLaunch& cl, int32_t stage, const GemmStep& gs,
-                   char* ws, void* stream) {
+                   char* ws, const StepScalars& sc, void* stream) {
   GemmArgs g{};
   g.mats = p.d_mats;
   const bool full = stage == ST_BX;
@@ -729,6 +913,9 @@ int launch_ns_gemm(const Plan& p, const WaveHost& w, const ClassLaunch& cl, int3
   g.r2 = gs.r2;
   g.out2 = gs.out2;
   g.split = gs.pair ? int32_t(nblocks) : INT32_MAX;
+  g.ptrs = p.d_ptrs;
+  g.lr = sc.lr;
+  g.decay = sc.decay;
   if (nblocks == 0) return 0;
   hipStream_t st = hipStream_t(stream);
   switch (cl.kclass) {

@@ -157,7 +157,7 @@ int64_t launches_per_step(const Plan& p, int32_t ns_steps) {
   int64_t n = 0;
   const int64_t k = ns_steps;
   for (const auto& w : p.waves) {
-    n += 3;  // momentum, finalize, apply
+    n += k > 0 ? 2 : 3;  // momentum, finalize (and apply when no NS step runs)
     for (const auto& cl : w.launches) n += cl.gram ? (k > 1 ? 3 * k + 1 : 3 * k) : 3 * k;
   }
   return n;
@@ -222,7 +222,6 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
       h.xt_off[pp] = need && ci.fp32 ? take(h.m_pad * h.n_pad * esz) : -1;
     }
     for (int q = 0; q < SQ_COUNT; ++q) h.sq_off[q] = q < 2 || h.gram ? take(h.m_pad * h.m_pad * esz) : -1;
-    h.o_off = take(h.m_pad * h.n_pad * 4);
     h.partial_off = take(h.ew_tiles * 4);
     h.ws_bytes = off;  // relative offsets for now, rebased per wave below
 
@@ -297,7 +296,6 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
       }
       for (int q = 0; q < SQ_COUNT; ++q)
         if (h.sq_off[q] >= 0) h.sq_off[q] += off;
-      h.o_off += off;
       h.partial_off += off;
       off += h.ws_bytes;
       ew += h.ew_tiles;
@@ -316,7 +314,6 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
         d.xt_off[pp] = h.xt_off[pp];
       }
       for (int q = 0; q < SQ_COUNT; ++q) d.sq_off[q] = h.sq_off[q];
-      d.o_off = h.o_off;
       d.partial_off = h.partial_off;
       d.rows = int32_t(h.rows);
       d.cols = int32_t(h.cols);
@@ -343,7 +340,7 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
       const double gsz = h.grad_dtype == MUON_BF16 ? 2 : 4, psz = h.param_dtype == MUON_BF16 ? 2 : 4;
       const double xsz = h.fp32_ns ? 4 : 2;
       w.bytes_momentum += el * (gsz + 4 + 4 + xsz);
-      w.bytes_apply += el * (psz + 4 + psz);
+      w.bytes_apply += el * (psz + xsz + psz);  // k = 0 only: read W and u, write W
     }
     w.scale_off = off;
     off += round_up(int64_t(w.count) * 4, kAlign);

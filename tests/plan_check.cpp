@@ -66,7 +66,7 @@ int main(int argc, char** argv) {
       const std::pair<long long, long long> rs[] = {
           {h.x_off[0], xb}, {h.x_off[1], xb}, {h.xt_off[0], xb}, {h.xt_off[1], xb},
           {h.sq_off[0], ab},  {h.sq_off[1], ab},  {h.sq_off[2], ab}, {h.sq_off[3], ab}, {h.sq_off[4], ab},
-          {h.o_off, h.m_pad * h.n_pad * 4}, {h.partial_off, h.ew_tiles * 4}};
+          {h.partial_off, h.ew_tiles * 4}};
       const bool want_gram = !h.fp32_ns && aspect > 0 && double(h.n) >= double(aspect) * double(h.m);
       if (h.gram != int(want_gram) || d.gram != h.gram) return fail("Gram-space choice");
       if ((h.x_off[1] < 0) != bool(h.gram)) return fail("second X buffer must exist exactly for Eq. 2");
@@ -120,7 +120,7 @@ int main(int argc, char** argv) {
   }
   for (size_t i = 0; i < seen.size(); ++i)
     if (seen[i] != 1) return fail("matrix not in exactly one wave");
-  // launch count at k = 5: per wave 3 elementwise launches, per (class, form)
+  // launch count at k = 5: per wave 2 elementwise launches, per (class, form)
   // group 15 (Eq. 2) or 1 Gram + 5 P_i + (G P | P Q) 4 + P Q 1 + P (G P) 4
   // + 1 B*X = 16 (Gram space)
   long long launches = 0;
@@ -130,7 +130,7 @@ int main(int argc, char** argv) {
       const MatHost& h = p.mats[size_t(p.order[size_t(w.first + s)])];
       groups.insert({h.kclass, h.gram});
     }
-    launches += 3;
+    launches += 2;
     for (const auto& g : groups) launches += g.second ? 16 : 15;
   }
   if (launches != launches_per_step(p, 5)) return fail("launches per step");

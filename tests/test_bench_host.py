@@ -27,7 +27,8 @@ def test_gemm_algorithmic_bytes(lib, aspect):
     cls = "bf16_t256"
     assert plan.matrix_info(0)["kernel_class"] == plan.matrix_info(1)["kernel_class"] == 0
     m, n, k = 512.0, 2048.0, 5
-    got = {kind: bench.gemm_algorithmic_bytes(plan, k, kind, cls) for kind in ("gram", "poly", "bx", "symm")}
+    pb = [2, 2]   # bf16 parameters: the last B*X reads and writes W, 4 bytes per element
+    got = {kind: bench.gemm_algorithmic_bytes(plan, k, kind, cls, pb) for kind in ("gram", "poly", "bx", "symm")}
     if aspect:
         want = {"gram": 2 * (m * n + m * m), "poly": k * 4 * m * m, "symm": (k - 1) * 9 * 2 * m * m,
                 "bx": 2 * (m * m + m * n) + 4 * m * n}
@@ -36,7 +37,7 @@ def test_gemm_algorithmic_bytes(lib, aspect):
                 "bx": k * 2 * (m * m + m * n) + (k - 1) * 2 * m * n + 4 * m * n}
     for kind in want:
         assert got[kind] == pytest.approx(2 * want[kind]), kind   # two matrices
-    assert bench.gemm_algorithmic_bytes(plan, k, "bx", "f32_t64") == 0.0
+    assert bench.gemm_algorithmic_bytes(plan, k, "bx", "f32_t64", pb) == 0.0
     plan.close()
 
 
