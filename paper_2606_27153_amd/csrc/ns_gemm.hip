@@ -115,6 +115,18 @@ struct Cfg {
   static_assert(CPW >= 1 && TILE_ / 8 % NW == 0, "tile too small for the block");
 };
 
+// One direct-to-LDS 16-byte load per lane: lane l's 16 bytes from g land at
+// LDS byte lds + 16*l.  Written as inline assembly: the compiler counts the
+// builtin's LDS write against the LDS-read counter as an out-of-order event
+// and then waits for every outstanding LDS read before each MFMA; the
+// completion of these loads is waited for explicitly (vmcnt) before the
+// barrier that publishes a slab.  The LDS address goes in M0, which needs
+// one wait state before the load.
+__device__ __forceinline__ void dma16(const void* g, const char* lds) {
+  const uint32_t m0 = uint32_t(reinterpret_cast<uintptr_t>((const lds_void_t*)(lds)));
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(m0) : "memory", "m0");
+}
+
 // Direct-to-LDS loads of one operand slab.  global_load_lds_dwordx4 writes
 // lane l's 16 bytes to LDS offset chunk*1024 + 16*l of the wave's 1 KB chunk,
 // i.e. row 8*chunk + l/8 at physical chunk position l%8; lane l therefore
@@ -134,8 +146,7 @@ __device__ __forceinline__ void load_slab(const E* src, int64_t K, int kt, char*
 #pragma unroll
   for (int i = 0; i < C::CPW; ++i) {
     const E* g = src + int64_t(i) * (8 * C::NW) * K + int64_t(kt) * C::BK;
-    __builtin_amdgcn_global_load_lds((gbl_void_t*)(g), (lds_void_t*)(lds + (wid + C::NW * i) * 1024), 16, 0,
-                                     0);
+    dma16(g, lds + (wid + C::NW * i) * 1024);
   }
 }
 
@@ -546,7 +557,7 @@ __device__ __forceinline__ void load_slab_rows(const __bf16* src, int64_t ld, in
 #pragma unroll
   for (int i = 0; i < C::CPW; ++i) {
     const __bf16* g = src + int64_t(i) * (RPC * C::NW) * ld + int64_t(kt) * 64 * ld;
-    __builtin_amdgcn_global_load_lds((gbl_void_t*)(g), (lds_void_t*)(lds + (wid + C::NW * i) * 1024), 16, 0, 0);
+    dma16(g, lds + (wid + C::NW * i) * 1024);
   }
 }
 
