@@ -169,10 +169,12 @@ struct Frag<float> { typedef f32x4 T; };
 template <class C, typename E>
 __device__ __forceinline__ void read_frags(const char* sa, const char* sb, int oa, int ob,
                                            typename Frag<E>::T (&fa)[C::NBM], typename Frag<E>::T (&fb)[C::NBN]) {
-#pragma unroll
-  for (int i = 0; i < C::NBM; ++i) fa[i] = *reinterpret_cast<const typename Frag<E>::T*>(sa + oa + i * 4096);
+  // second operand first: the first MFMA of the sub-step (block 0, 0) then
+  // waits for two of the reads instead of NBM + 1
 #pragma unroll
   for (int j = 0; j < C::NBN; ++j) fb[j] = *reinterpret_cast<const typename Frag<E>::T*>(sb + ob + j * 4096);
+#pragma unroll
+  for (int i = 0; i < C::NBM; ++i) fa[i] = *reinterpret_cast<const typename Frag<E>::T*>(sa + oa + i * 4096);
 }
 
 template <class C, typename E>
@@ -582,14 +584,14 @@ __device__ __forceinline__ void read_frags_tr(const char* sa, const char* sb, in
                                               int ks, bf16x8 (&fa)[C::NBM], bf16x8 (&fb)[C::NBN]) {
   constexpr int KSB = 16 * C::TILE * 2;  // bytes of 16 K-rows
 #pragma unroll
-  for (int i = 0; i < C::NBM; ++i) fa[i] = *reinterpret_cast<const bf16x8*>(sa + oa + i * 4096);
-#pragma unroll
   for (int j = 0; j < C::NBN; ++j) {
     const i16x4 lo = lds_tr16(sb + ot[2 * j] + ks * KSB);
     const i16x4 hi = lds_tr16(sb + ot[2 * j + 1] + ks * KSB);
     const i16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
     fb[j] = __builtin_bit_cast(bf16x8, v);
   }
+#pragma unroll
+  for (int i = 0; i < C::NBM; ++i) fa[i] = *reinterpret_cast<const bf16x8*>(sa + oa + i * 4096);
 }
 
 template <class C>
