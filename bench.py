@@ -68,7 +68,7 @@ def read_traffic(kernel_key: str, path: str = TRAFFIC_SUMMARY):
 
 def _kernel_patterns():
     pats = []
-    for e, cls in (("DF16b", "bf16"), ("f", "f32")):
+    for e, cls in (("DF16b", "bf16"), ("f", "f32"), ("DF16_", "f16")):
         for tile, wg in ((256, "2ELi4"), (128, "2ELi2"), (64, "2ELi2")):
             if e == "f" and tile == 256:
                 continue
@@ -258,7 +258,7 @@ def main(argv=None) -> int:
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", default="8b", choices=["tiny", "1b", "8b", "vla", "moe"])
-    ap.add_argument("--precision", default="bf16", choices=["bf16", "fp32"])
+    ap.add_argument("--precision", default="bf16", choices=["bf16", "fp16", "fp32"])
     ap.add_argument("--wave-bytes", type=int, default=0)
     ap.add_argument("--gram-min-aspect", type=float, default=2.0,
                     help="Gram-space recurrence (Eq. 4) for matrices with n >= this * m; 0 = Eq. 2 only")
@@ -335,7 +335,8 @@ def main(argv=None) -> int:
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     log(f"[bench] {args.steps} timed steps: {ms_per_step:.3f} ms/step")
 
-    peak_mm = PEAK_BF16_TFLOPS if args.precision == "bf16" else PEAK_F32_TFLOPS
+    # fp16 MFMA has the bf16 dense peak
+    peak_mm = PEAK_F32_TFLOPS if args.precision == "fp32" else PEAK_BF16_TFLOPS
     per_kernel = []
     for s in sorted(stats, key=lambda s: -s["total_ms"]):
         mean_ms = s["total_ms"] / max(1, s["launches"])
@@ -398,7 +399,7 @@ def main(argv=None) -> int:
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16" if args.precision == "bf16" else "f32",
+        "dtype": {"bf16": "bf16", "fp16": "f16", "fp32": "f32"}[args.precision],
         "data": "synthetic",
         "config": {"workload": wl.key, "description": wl.description, "matrices": wl.n,
                    "elements": wl.elements(), "ns_steps": wl.ns_steps,

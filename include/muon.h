@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define MUON_ABI_VERSION 2
+#define MUON_ABI_VERSION 3
 
 #if defined(__GNUC__)
 #define MUON_API __attribute__((visibility("default")))
@@ -67,8 +67,14 @@ typedef enum muon_dtype { MUON_F32 = 0, MUON_BF16 = 1 } muon_dtype;
 /* Arithmetic of the Newton-Schulz GEMMs.  MUON_NS_BF16: bf16 operands in
  * HBM, fp32 accumulation on the matrix cores (matrices with
  * min(rows, cols) <= small_m_threshold still use fp32).  MUON_NS_FP32: fp32
- * operands and fp32 matrix-core arithmetic for every matrix (validation). */
-typedef enum muon_ns_precision { MUON_NS_BF16 = 0, MUON_NS_FP32 = 1 } muon_ns_precision;
+ * operands and fp32 matrix-core arithmetic for every matrix (validation).
+ * MUON_NS_FP16: fp16 operands, fp32 accumulation, for every matrix size (the
+ * NS precision of the paper's implementation, Sec. 5 "Configurations"): the
+ * same matrix-core rate as bf16 and about 8x less rounding error.  Its range
+ * is fp16's: the Nesterov input u = G + mu*M is stored in fp16 before it is
+ * normalised, so |u| must stay below 65504, and entries below 2^-24 round to
+ * zero. */
+typedef enum muon_ns_precision { MUON_NS_BF16 = 0, MUON_NS_FP32 = 1, MUON_NS_FP16 = 2 } muon_ns_precision;
 
 /* Plan flags. */
 #define MUON_PLAN_HOST_ONLY 0x1u     /* build host metadata only: no device memory is

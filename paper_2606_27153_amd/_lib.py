@@ -28,6 +28,7 @@ MUON_BF16 = 1
 # muon_ns_precision
 MUON_NS_BF16 = 0
 MUON_NS_FP32 = 1
+MUON_NS_FP16 = 2
 
 MUON_PLAN_HOST_ONLY = 0x1
 
@@ -72,7 +73,7 @@ class muon_kernel_stat(ctypes.Structure):
 
 
 KERNEL_KINDS = ("momentum", "finalize", "gram", "poly", "bx", "apply", "symm")
-KERNEL_CLASSES = ("bf16_t256", "bf16_t128", "bf16_t64", "f32_t128", "f32_t64")
+KERNEL_CLASSES = ("bf16_t256", "bf16_t128", "bf16_t64", "f32_t128", "f32_t64", "f16_t256", "f16_t128", "f16_t64")
 
 _VP = ctypes.c_void_p
 _PP = ctypes.POINTER(ctypes.c_void_p)

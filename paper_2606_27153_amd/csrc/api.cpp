@@ -35,8 +35,8 @@ muon_status hip_fail(hipError_t e, const char* what) {
 bool valid_dtype(int32_t d) { return d == MUON_F32 || d == MUON_BF16; }
 
 muon_status check_opts(const muon_plan_opts& o) {
-  if (o.precision != MUON_NS_BF16 && o.precision != MUON_NS_FP32)
-    return fail(MUON_ERR_INVALID_ARG, "opts.precision must be MUON_NS_BF16 or MUON_NS_FP32");
+  if (o.precision != MUON_NS_BF16 && o.precision != MUON_NS_FP32 && o.precision != MUON_NS_FP16)
+    return fail(MUON_ERR_INVALID_ARG, "opts.precision must be MUON_NS_BF16, MUON_NS_FP32 or MUON_NS_FP16");
   if (o.max_ns_steps < 1 || o.max_ns_steps > 64)
     return fail(MUON_ERR_INVALID_ARG, "opts.max_ns_steps must be in [1, 64]");
   if (!std::isfinite(o.a) || !std::isfinite(o.b) || !std::isfinite(o.c))

@@ -23,6 +23,7 @@ namespace muon {
 namespace {
 
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 __device__ inline int find_slot(const int32_t* __restrict__ prefix, int count, int bid) {
@@ -34,11 +35,15 @@ __device__ inline int find_slot(const int32_t* __restrict__ prefix, int count, i
   return lo;
 }
 
-// Stores 4 NS-operand values (bf16 or fp32) at an aligned position of a
-// padded workspace buffer.
-__device__ inline void store_x4(char* buf, int64_t idx, int x_f32, const float v[4]) {
+// Stores 4 NS-operand values (bf16, fp16 or fp32) at an aligned position of
+// a padded workspace buffer.
+__device__ inline void store_x4(char* buf, int64_t idx, int x_f32, int x_f16, const float v[4]) {
   if (x_f32) {
     *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(buf) + idx) = f32x4{v[0], v[1], v[2], v[3]};
+  } else if (x_f16) {
+    f16x4 x;
+    x[0] = _Float16(v[0]); x[1] = _Float16(v[1]); x[2] = _Float16(v[2]); x[3] = _Float16(v[3]);
+    *reinterpret_cast<f16x4*>(reinterpret_cast<_Float16*>(buf) + idx) = x;
   } else {
     bf16x4 x;
     x[0] = __bf16(v[0]); x[1] = __bf16(v[1]); x[2] = __bf16(v[2]); x[3] = __bf16(v[3]);
@@ -92,7 +97,7 @@ __global__ __launch_bounds__(256) void momentum_kernel(const MatDev* __restrict_
       }
       store4(pe.mom, idx, MUON_F32, vec, valid, m);
     }
-    if (ubuf) store_x4(ubuf, int64_t(r) * d.cols_pad + c, d.x_f32, u);
+    if (ubuf) store_x4(ubuf, int64_t(r) * d.cols_pad + c, d.x_f32, d.x_f16, u);
 #pragma unroll
     for (int e = 0; e < 4; ++e) tile_t[rl][4 * cg + e] = u[e];
   }
@@ -104,7 +109,7 @@ __global__ __launch_bounds__(256) void momentum_kernel(const MatDev* __restrict_
       float v[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) v[e] = tile_t[4 * cg + e][oc];
-      store_x4(utbuf, int64_t(c0 + oc) * d.rows_pad + r0 + 4 * cg, d.x_f32, v);
+      store_x4(utbuf, int64_t(c0 + oc) * d.rows_pad + r0 + 4 * cg, d.x_f32, d.x_f16, v);
     }
   }
 #pragma unroll
@@ -159,8 +164,8 @@ __global__ __launch_bounds__(256) void apply_kernel(const MatDev* __restrict__ m
   const bool zero = flag[s] != 0;
   const float sc = scale[s];
   const float lrs = update_lr(lr, rows, cols);
-  // u is read from X (transposed for a tall bf16 matrix, whose stored-layout
-  // copy does not exist) or from the fp32 X^T.
+  // u is read from X (transposed for a tall 16-bit matrix, whose
+  // stored-layout copy does not exist) or from the fp32 X^T.
   const bool u_transposed = d.transposed && !d.x_f32;
   const char* ubuf = ws + (d.transposed && d.x_f32 ? d.xt_off[0] : d.x_off[0]);
 #pragma unroll
@@ -175,6 +180,16 @@ __global__ __launch_bounds__(256) void apply_kernel(const MatDev* __restrict__ m
       if (d.x_f32) {
         const f32x4 x = *reinterpret_cast<const f32x4*>(reinterpret_cast<const float*>(ubuf) + pidx);
         o[0] = sc * x[0]; o[1] = sc * x[1]; o[2] = sc * x[2]; o[3] = sc * x[3];
+      } else if (d.x_f16) {
+        const _Float16* xh = reinterpret_cast<const _Float16*>(ubuf);
+        if (!u_transposed) {
+          const f16x4 x = *reinterpret_cast<const f16x4*>(xh + pidx);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) o[e] = sc * float(x[e]);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) o[e] = sc * float(xh[int64_t(c + e) * d.rows_pad + r]);
+        }
       } else if (!u_transposed) {
         const bf16x4 x = *reinterpret_cast<const bf16x4*>(reinterpret_cast<const __bf16*>(ubuf) + pidx);
         o[0] = sc * float(x[0]); o[1] = sc * float(x[1]); o[2] = sc * float(x[2]); o[3] = sc * float(x[3]);

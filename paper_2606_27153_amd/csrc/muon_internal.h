@@ -22,12 +22,16 @@ enum KernelClass : int32_t {
   KC_BF16_64 = 2,
   KC_F32_128 = 3,
   KC_F32_64 = 4,
-  KC_COUNT = 5
+  KC_F16_256 = 5,
+  KC_F16_128 = 6,
+  KC_F16_64 = 7,
+  KC_COUNT = 8
 };
 
 struct ClassInfo {
   int32_t tile;
-  int32_t fp32;     // operands stored as fp32 (else bf16)
+  int32_t fp32;     // operands stored as fp32 (else 16-bit)
+  int32_t f16;      // 16-bit operands are fp16 (else bf16)
   const char* name;
 };
 
@@ -60,7 +64,7 @@ struct MatDev {
   int32_t ew_tiles_c;          // cols_pad / 64
   int32_t gram;                // runs the Gram-space recurrence
   int32_t m;                   // oriented unpadded m
-  int32_t pad0;
+  int32_t x_f16;               // 16-bit X and square buffers are fp16 (else bf16)
 };
 
 // One output tile of a grouped GEMM launch.

@@ -30,9 +30,12 @@
 //
 // Block: WGM x WGN waves (2 x 4 for the 256 tile, 2 x 2 otherwise), output
 // tile TILE x TILE, each wave owning a (TILE/WGM) x (TILE/WGN) piece made of
-// 32 x 32 MFMA blocks.  K advances in 128-byte slabs (64 bf16 / 32 fp32)
-// moved straight from global memory into double-buffered, XOR-swizzled LDS
-// by global_load_lds_dwordx4 (no staging registers).
+// 32 x 32 MFMA blocks.  K advances in 128-byte slabs (64 bf16 or fp16 / 32
+// fp32) moved straight from global memory into double-buffered, XOR-swizzled
+// LDS by global_load_lds_dwordx4 (no staging registers).  Operands are bf16,
+// fp16 (the NS precision of the paper's implementation) or fp32; the 16-bit
+// kinds share every path and differ only in the MFMA instruction and the
+// conversions.
 #include <hip/hip_runtime.h>
 
 #include "ew_common.h"
@@ -43,6 +46,8 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -84,6 +89,8 @@ __device__ __forceinline__ E to_e(float v);
 template <>
 __device__ __forceinline__ __bf16 to_e<__bf16>(float v) { return __bf16(v); }
 template <>
+__device__ __forceinline__ _Float16 to_e<_Float16>(float v) { return _Float16(v); }
+template <>
 __device__ __forceinline__ float to_e<float>(float v) { return v; }
 
 template <typename E>
@@ -93,6 +100,12 @@ __device__ __forceinline__ void store_vec4<__bf16>(__bf16* p, float v0, float v1
   bf16x4 x;
   x[0] = __bf16(v0); x[1] = __bf16(v1); x[2] = __bf16(v2); x[3] = __bf16(v3);
   *reinterpret_cast<bf16x4*>(p) = x;
+}
+template <>
+__device__ __forceinline__ void store_vec4<_Float16>(_Float16* p, float v0, float v1, float v2, float v3) {
+  f16x4 x;
+  x[0] = _Float16(v0); x[1] = _Float16(v1); x[2] = _Float16(v2); x[3] = _Float16(v3);
+  *reinterpret_cast<f16x4*>(p) = x;
 }
 template <>
 __device__ __forceinline__ void store_vec4<float>(float* p, float v0, float v1, float v2, float v3) {
@@ -164,6 +177,8 @@ struct Frag;
 template <>
 struct Frag<__bf16> { typedef bf16x8 T; };
 template <>
+struct Frag<_Float16> { typedef f16x8 T; };
+template <>
 struct Frag<float> { typedef f32x4 T; };
 
 template <class C, typename E>
@@ -180,12 +195,18 @@ __device__ __forceinline__ void read_frags(const char* sa, const char* sb, int o
 template <class C, typename E>
 __device__ __forceinline__ void mfma_frags(const typename Frag<E>::T (&fa)[C::NBM],
                                            const typename Frag<E>::T (&fb)[C::NBN], f32x16 (&acc)[C::NBM][C::NBN]) {
-  if constexpr (sizeof(E) == 2) {
+  if constexpr (__is_same(E, __bf16)) {
 #pragma unroll
     for (int i = 0; i < C::NBM; ++i)
 #pragma unroll
       for (int j = 0; j < C::NBN; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+  } else if constexpr (__is_same(E, _Float16)) {
+#pragma unroll
+    for (int i = 0; i < C::NBM; ++i)
+#pragma unroll
+      for (int j = 0; j < C::NBN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[i], fb[j], acc[i][j], 0, 0, 0);
   } else {
     // fp32: lane half h holds k = 4*(2*ks + h) + q for element q, and the
     // same mapping on both operands, so the four 32x32x2 MFMAs cover 8 k.
@@ -242,6 +263,8 @@ template <typename T>
 struct Vec4;
 template <>
 struct Vec4<__bf16> { typedef bf16x4 T; };
+template <>
+struct Vec4<_Float16> { typedef f16x4 T; };
 template <>
 struct Vec4<float> { typedef f32x4 T; };
 
@@ -328,9 +351,9 @@ __device__ __forceinline__ void store_t_via_lds(const f32x16 (&acc)[C::NBM][C::N
           const float v0 = acc[i][j][4 * g], v1 = acc[i][j][4 * g + 1];
           const float v2 = acc[i][j][4 * g + 2], v3 = acc[i][j][4 * g + 3];
           if constexpr (sizeof(OUT) == 2) {
-            bf16x4 x;
-            x[0] = __bf16(v0); x[1] = __bf16(v1); x[2] = __bf16(v2); x[3] = __bf16(v3);
-            *reinterpret_cast<bf16x4*>(region + L::off(r, c * 2)) = x;
+            typename Vec4<OUT>::T x;
+            x[0] = OUT(v0); x[1] = OUT(v1); x[2] = OUT(v2); x[3] = OUT(v3);
+            *reinterpret_cast<typename Vec4<OUT>::T*>(region + L::off(r, c * 2)) = x;
           } else {
             *reinterpret_cast<f32x4*>(region + L::off(r, c * 4)) = f32x4{v0, v1, v2, v3};
           }
@@ -544,8 +567,8 @@ __device__ __forceinline__ int seg_swz(int row) {
 // lane l fills 16-byte slot l of the chunk, i.e. row l / LPR, slot l % LPR,
 // and fetches the logical segment the swizzle stores there.  Across the
 // wave's chunks (q + NW*i) the swizzle of a lane's row is unchanged.
-template <class C>
-__device__ __forceinline__ const __bf16* lane_src_rows(const __bf16* xcol, int64_t ld, int wid, int lane) {
+template <class C, typename E>
+__device__ __forceinline__ const E* lane_src_rows(const E* xcol, int64_t ld, int wid, int lane) {
   constexpr int ROWB = C::TILE * 2, RPC = 1024 / ROWB, LPR = ROWB / 16;
   const int row = wid * RPC + lane / LPR;
   const int slot = lane % LPR;
@@ -553,12 +576,12 @@ __device__ __forceinline__ const __bf16* lane_src_rows(const __bf16* xcol, int64
   return xcol + int64_t(row) * ld + seg * 16 + (slot & 1) * 8;
 }
 
-template <class C>
-__device__ __forceinline__ void load_slab_rows(const __bf16* src, int64_t ld, int kt, char* lds, int wid) {
+template <class C, typename E>
+__device__ __forceinline__ void load_slab_rows(const E* src, int64_t ld, int kt, char* lds, int wid) {
   constexpr int ROWB = C::TILE * 2, RPC = 1024 / ROWB;
 #pragma unroll
   for (int i = 0; i < C::CPW; ++i) {
-    const __bf16* g = src + int64_t(i) * (RPC * C::NW) * ld + int64_t(kt) * 64 * ld;
+    const E* g = src + int64_t(i) * (RPC * C::NW) * ld + int64_t(kt) * 64 * ld;
     dma16(g, lds + (wid + C::NW * i) * 1024);
   }
 }
@@ -579,37 +602,39 @@ __device__ __forceinline__ void tr_offsets(int wn, int lane, int (&ot)[2 * C::NB
     }
 }
 
-template <class C>
+template <class C, typename E>
 __device__ __forceinline__ void read_frags_tr(const char* sa, const char* sb, int oa, const int (&ot)[2 * C::NBN],
-                                              int ks, bf16x8 (&fa)[C::NBM], bf16x8 (&fb)[C::NBN]) {
+                                              int ks, typename Frag<E>::T (&fa)[C::NBM],
+                                              typename Frag<E>::T (&fb)[C::NBN]) {
   constexpr int KSB = 16 * C::TILE * 2;  // bytes of 16 K-rows
 #pragma unroll
   for (int j = 0; j < C::NBN; ++j) {
     const i16x4 lo = lds_tr16(sb + ot[2 * j] + ks * KSB);
     const i16x4 hi = lds_tr16(sb + ot[2 * j + 1] + ks * KSB);
     const i16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-    fb[j] = __builtin_bit_cast(bf16x8, v);
+    fb[j] = __builtin_bit_cast(typename Frag<E>::T, v);
   }
 #pragma unroll
-  for (int i = 0; i < C::NBM; ++i) fa[i] = *reinterpret_cast<const bf16x8*>(sa + oa + i * 4096);
+  for (int i = 0; i < C::NBM; ++i) fa[i] = *reinterpret_cast<const typename Frag<E>::T*>(sa + oa + i * 4096);
 }
 
-template <class C>
+template <class C, typename E>
 __device__ __forceinline__ void slab_body_tr(const char* st, const int (&oa)[4], const int (&ot)[2 * C::NBN],
-                                             bf16x8 (&fa0)[C::NBM], bf16x8 (&fb0)[C::NBN], bf16x8 (&fa1)[C::NBM],
-                                             bf16x8 (&fb1)[C::NBN], f32x16 (&acc)[C::NBM][C::NBN]) {
+                                             typename Frag<E>::T (&fa0)[C::NBM], typename Frag<E>::T (&fb0)[C::NBN],
+                                             typename Frag<E>::T (&fa1)[C::NBM], typename Frag<E>::T (&fb1)[C::NBN],
+                                             f32x16 (&acc)[C::NBM][C::NBN]) {
   constexpr int NR = C::NBM + 2 * C::NBN;
   constexpr int NM = C::NBM * C::NBN;
-  read_frags_tr<C>(st, st + C::OPB, oa[1], ot, 1, fa1, fb1);
-  mfma_frags<C, __bf16>(fa0, fb0, acc);
+  read_frags_tr<C, E>(st, st + C::OPB, oa[1], ot, 1, fa1, fb1);
+  mfma_frags<C, E>(fa0, fb0, acc);
   interleave<NR, NM>();
-  read_frags_tr<C>(st, st + C::OPB, oa[2], ot, 2, fa0, fb0);
-  mfma_frags<C, __bf16>(fa1, fb1, acc);
+  read_frags_tr<C, E>(st, st + C::OPB, oa[2], ot, 2, fa0, fb0);
+  mfma_frags<C, E>(fa1, fb1, acc);
   interleave<NR, NM>();
-  read_frags_tr<C>(st, st + C::OPB, oa[3], ot, 3, fa1, fb1);
-  mfma_frags<C, __bf16>(fa0, fb0, acc);
+  read_frags_tr<C, E>(st, st + C::OPB, oa[3], ot, 3, fa1, fb1);
+  mfma_frags<C, E>(fa0, fb0, acc);
   interleave<NR, NM>();
-  mfma_frags<C, __bf16>(fa1, fb1, acc);
+  mfma_frags<C, E>(fa1, fb1, acc);
   __builtin_amdgcn_sched_barrier(0);
 }
 
@@ -644,8 +669,8 @@ __device__ __forceinline__ void fuse_input(const char* sb, int kt, int row0, int
           const int jj = lane & 15;
           const int row = k4 + (jj >> 2);
           const int col = wn * C::WTN + 32 * j + 16 * ((lane >> 4) & 1) + 4 * (jj & 3);
-          const bf16x4 v = __builtin_bit_cast(
-              bf16x4, lds_tr16(sb + row * ROWB + (((col >> 4) ^ seg_swz<ROWB>(row)) << 5) + (col & 15) * 2));
+          const typename Vec4<E>::T v = __builtin_bit_cast(
+              typename Vec4<E>::T, lds_tr16(sb + row * ROWB + (((col >> 4) ^ seg_swz<ROWB>(row)) << 5) + (col & 15) * 2));
 #pragma unroll
           for (int e = 0; e < 4; ++e) x[e] = float(v[e]);
         } else {
@@ -734,40 +759,40 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
   if (!zero) {
     if constexpr (TRB) {
       const E* srca = lane_src<C>(opa, K, wid, lane);
-      const __bf16* srcb = lane_src_rows<C>(reinterpret_cast<const __bf16*>(opb), np, wid, lane);
+      const E* srcb = lane_src_rows<C, E>(opb, np, wid, lane);
       int oa[4], ot[2 * C::NBN];
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) oa[ks] = frag_off(wm * C::WTM, lane, ks);
       tr_offsets<C>(wn, lane, ot);
-      bf16x8 fa0[C::NBM], fb0[C::NBN], fa1[C::NBM], fb1[C::NBN];
+      typename Frag<E>::T fa0[C::NBM], fb0[C::NBN], fa1[C::NBM], fb1[C::NBN];
       load_slab<C>(srca, K, 0, stage0, wid);
       load_slab_rows<C>(srcb, np, 0, stage0 + C::OPB, wid);
       wait_vm_all();
       __syncthreads();
-      read_frags_tr<C>(stage0, stage0 + C::OPB, oa[0], ot, 0, fa0, fb0);
+      read_frags_tr<C, E>(stage0, stage0 + C::OPB, oa[0], ot, 0, fa0, fb0);
       int kt = 0;
       for (; kt + 2 <= nk; kt += 2) {
         load_slab<C>(srca, K, kt + 1, stage1, wid);
         load_slab_rows<C>(srcb, np, kt + 1, stage1 + C::OPB, wid);
-        slab_body_tr<C>(stage0, oa, ot, fa0, fb0, fa1, fb1, acc);
+        slab_body_tr<C, E>(stage0, oa, ot, fa0, fb0, fa1, fb1, acc);
         if (FUSE) fuse_input<C, E, true>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
         wait_vm_all();
         __syncthreads();
-        read_frags_tr<C>(stage1, stage1 + C::OPB, oa[0], ot, 0, fa0, fb0);
+        read_frags_tr<C, E>(stage1, stage1 + C::OPB, oa[0], ot, 0, fa0, fb0);
         __builtin_amdgcn_sched_barrier(0);
         if (kt + 2 < nk) {
           load_slab<C>(srca, K, kt + 2, stage0, wid);
           load_slab_rows<C>(srcb, np, kt + 2, stage0 + C::OPB, wid);
         }
-        slab_body_tr<C>(stage1, oa, ot, fa0, fb0, fa1, fb1, acc);
+        slab_body_tr<C, E>(stage1, oa, ot, fa0, fb0, fa1, fb1, acc);
         if (FUSE) fuse_input<C, E, true>(stage1 + C::OPB, kt + 1, frow0, wn, lane, fcoef, acc);
         wait_vm_all();
         __syncthreads();
-        if (kt + 2 < nk) read_frags_tr<C>(stage0, stage0 + C::OPB, oa[0], ot, 0, fa0, fb0);
+        if (kt + 2 < nk) read_frags_tr<C, E>(stage0, stage0 + C::OPB, oa[0], ot, 0, fa0, fb0);
         __builtin_amdgcn_sched_barrier(0);
       }
       if (kt < nk) {  // odd slab count: the last slab is in stage 0
-        slab_body_tr<C>(stage0, oa, ot, fa0, fb0, fa1, fb1, acc);
+        slab_body_tr<C, E>(stage0, oa, ot, fa0, fb0, fa1, fb1, acc);
         if (FUSE) fuse_input<C, E, true>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
         __syncthreads();
       }
@@ -937,6 +962,9 @@ int launch_ns_gemm(const Plan& p, const WaveHost& w, const ClassLaunch& cl, int3
     case KC_BF16_64: return launch_stage<__bf16, 64, 2, 2>(stage, grid, g, st);
     case KC_F32_128: return launch_stage<float, 128, 2, 2>(stage, grid, g, st);
     case KC_F32_64: return launch_stage<float, 64, 2, 2>(stage, grid, g, st);
+    case KC_F16_256: return launch_stage<_Float16, 256, 2, 4>(stage, grid, g, st);
+    case KC_F16_128: return launch_stage<_Float16, 128, 2, 2>(stage, grid, g, st);
+    case KC_F16_64: return launch_stage<_Float16, 64, 2, 2>(stage, grid, g, st);
     default: return -1;
   }
 }

@@ -18,11 +18,14 @@ namespace muon {
 namespace {
 
 constexpr ClassInfo kClasses[KC_COUNT] = {
-    {256, 0, "bf16_t256"},
-    {128, 0, "bf16_t128"},
-    {64, 0, "bf16_t64"},
-    {128, 1, "f32_t128"},
-    {64, 1, "f32_t64"},
+    {256, 0, 0, "bf16_t256"},
+    {128, 0, 0, "bf16_t128"},
+    {64, 0, 0, "bf16_t64"},
+    {128, 1, 0, "f32_t128"},
+    {64, 1, 0, "f32_t64"},
+    {256, 0, 1, "f16_t256"},
+    {128, 0, 1, "f16_t128"},
+    {64, 0, 1, "f16_t64"},
 };
 
 // Relative throughput assumed for each class when choosing a tile: larger
@@ -30,7 +33,7 @@ constexpr ClassInfo kClasses[KC_COUNT] = {
 #ifndef MUON_EFF128
 #define MUON_EFF128 0.8
 #endif
-constexpr double kClassEfficiency[KC_COUNT] = {1.0, MUON_EFF128, 0.45, 1.0, 0.6};
+constexpr double kClassEfficiency[KC_COUNT] = {1.0, MUON_EFF128, 0.45, 1.0, 0.6, 1.0, MUON_EFF128, 0.45};
 
 constexpr int64_t kDefaultWaveBytes = int64_t(12) << 30;  // 12 GiB
 constexpr int64_t kAlign = 256;
@@ -43,9 +46,11 @@ double padded_cost(int64_t m, int64_t n, int32_t tile) {
 }
 
 int32_t choose_class(int64_t m, int64_t n, const muon_plan_opts& o) {
-  const bool fp32 = o.precision == MUON_NS_FP32 || m <= o.small_m_threshold;
-  const int32_t lo = fp32 ? KC_F32_128 : KC_BF16_256;
-  const int32_t hi = fp32 ? KC_F32_64 : KC_BF16_64;
+  // fp16 keeps enough precision for every size; bf16 hands small m to fp32
+  const bool f16 = o.precision == MUON_NS_FP16;
+  const bool fp32 = o.precision == MUON_NS_FP32 || (!f16 && m <= o.small_m_threshold);
+  const int32_t lo = fp32 ? KC_F32_128 : f16 ? KC_F16_256 : KC_BF16_256;
+  const int32_t hi = fp32 ? KC_F32_64 : f16 ? KC_F16_64 : KC_BF16_64;
   int32_t best = hi;
   double best_cost = 0;
   for (int32_t kc = lo; kc <= hi; ++kc) {
@@ -323,6 +328,7 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
       d.n_pad = int32_t(h.n_pad);
       d.transposed = h.transposed;
       d.x_f32 = h.fp32_ns;
+      d.x_f16 = kClasses[h.kclass].f16;
       d.param_dtype = h.param_dtype;
       d.grad_dtype = h.grad_dtype;
       d.slot = s;

@@ -14,6 +14,9 @@ from typing import List, Optional, Sequence
 from . import _lib as L
 
 _DT = {"f32": L.MUON_F32, "bf16": L.MUON_BF16}
+# NS arithmetic: bf16 (the default), fp16 (the paper's implementation
+# choice, Sec. 5) or fp32 (validation)
+PRECISIONS = {"bf16": L.MUON_NS_BF16, "fp32": L.MUON_NS_FP32, "fp16": L.MUON_NS_FP16}
 
 
 def _dtype_code(t) -> int:
@@ -48,7 +51,7 @@ class MuonPlan:
             arr[i].momentum_dtype = L.MUON_F32
         opts = L.muon_plan_opts()
         L.check(lib.muon_plan_opts_default(ctypes.byref(opts)))
-        opts.precision = {"bf16": L.MUON_NS_BF16, "fp32": L.MUON_NS_FP32}[precision]
+        opts.precision = PRECISIONS[precision]
         opts.max_ns_steps = int(max_ns_steps)
         if abc is not None:
             opts.a, opts.b, opts.c = (float(v) for v in abc)

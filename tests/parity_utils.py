@@ -20,8 +20,11 @@ from paper_2606_27153_amd.optim import MuonPlan
 from paper_2606_27153_amd.workloads import Workload, make_grads, make_state
 
 # Bounds of the contract: relative Frobenius error of the orthogonalised
-# update per matrix, bf16 NS path and fp32 validation path.
-TOL_O = {"bf16": 2e-2, "fp32": 1e-5}
+# update per matrix, bf16 NS path and fp32 validation path.  The fp16 path
+# has no stated bound; its unit roundoff is 8x smaller than bf16's (2^-11 vs
+# 2^-8), and an fp32-accumulate emulation with fp16 stores measured at most
+# 3.3e-3 (m = 32, Gram space) and 1.7e-3 for m >= 64, so it is held to 5e-3.
+TOL_O = {"bf16": 2e-2, "fp32": 1e-5, "fp16": 5e-3}
 # Momentum is one fp32 fused multiply-add per element on both sides.
 TOL_M = 1e-6
 

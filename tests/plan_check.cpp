@@ -5,8 +5,10 @@
 // cover every output tile of each of its matrices exactly once; workspace
 // regions inside a wave are 256-byte aligned and disjoint; the elementwise
 // tile prefix matches the matrices' tile counts; the Gram-space form is
-// chosen exactly for bf16-class matrices with n >= aspect * m, and those keep
-// X0 alone plus five square buffers.  Prints "OK" or the first violation.
+// chosen exactly for 16-bit-class matrices with n >= aspect * m, and those keep
+// X0 alone plus five square buffers; the operand type of each matrix's class
+// follows the precision (fp32 for small m only under bf16, fp16 everywhere
+// under fp16).  Prints "OK" or the first violation.
 // Arguments: precision, wave_bytes, gram_min_aspect.
 #include <algorithm>
 #include <cstdio>
@@ -67,6 +69,13 @@ int main(int argc, char** argv) {
           {h.x_off[0], xb}, {h.x_off[1], xb}, {h.xt_off[0], xb}, {h.xt_off[1], xb},
           {h.sq_off[0], ab},  {h.sq_off[1], ab},  {h.sq_off[2], ab}, {h.sq_off[3], ab}, {h.sq_off[4], ab},
           {h.partial_off, h.ew_tiles * 4}};
+      // operand type: fp32 for the fp32 mode and for small m under bf16,
+      // fp16 for every matrix under fp16, bf16 otherwise
+      const bool want_f32 = precision == MUON_NS_FP32 || (precision == MUON_NS_BF16 && h.m <= 64);
+      const bool want_f16 = precision == MUON_NS_FP16;
+      if (class_info(h.kclass).fp32 != int(want_f32) || class_info(h.kclass).f16 != int(want_f16) ||
+          h.fp32_ns != int(want_f32) || d.x_f32 != int(want_f32) || d.x_f16 != int(want_f16))
+        return fail("operand type of the kernel class");
       const bool want_gram = !h.fp32_ns && aspect > 0 && double(h.n) >= double(aspect) * double(h.m);
       if (h.gram != int(want_gram) || d.gram != h.gram) return fail("Gram-space choice");
       if ((h.x_off[1] < 0) != bool(h.gram)) return fail("second X buffer must exist exactly for Eq. 2");

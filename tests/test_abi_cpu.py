@@ -27,7 +27,7 @@ def test_every_declared_symbol_is_exported(lib):
     for name in names:
         assert hasattr(lib, name), name
         assert name in L.SIGNATURES, name
-    assert lib.muon_abi_version() == 2
+    assert lib.muon_abi_version() == 3
 
 
 def test_struct_layout_matches_c_compiler(tmp_path):
@@ -105,6 +105,19 @@ def test_fp32_precision_uses_fp32_everywhere():
     wl = get_workload("tiny")
     plan = MuonPlan(_descs(wl), precision="fp32", host_only=True)
     assert all(plan.matrix_info(i)["fp32_ns"] == 1 for i in range(wl.n))
+
+
+def test_fp16_precision_uses_fp16_everywhere():
+    # fp16 keeps every size on 16-bit operands (no fp32 fallback for small m)
+    # and still takes the Gram-space form for wide matrices
+    wl = get_workload("vla")
+    plan = MuonPlan(_descs(wl), precision="fp16", host_only=True)
+    for i in range(wl.n):
+        mi = plan.matrix_info(i)
+        assert mi["fp32_ns"] == 0
+        assert L.KERNEL_CLASSES[mi["kernel_class"]].startswith("f16_")
+        assert mi["gram_space"] == int(mi["n"] >= 2 * mi["m"])
+    plan.close()
 
 
 def test_buckets_of_the_8b_set():

@@ -46,6 +46,8 @@ def test_kernel_keys():
         == "symm:bf16_t256"
     assert bench.kernel_key("_ZN4muon12_GLOBAL__N_114ns_gemm_kernelIfLi64ELi2ELi2ELi2EEEvNS0_8GemmArgsE") \
         == "bx:f32_t64"
+    assert bench.kernel_key("_ZN4muon12_GLOBAL__N_114ns_gemm_kernelIDF16_Li256ELi2ELi4ELi2EEEvNS0_8GemmArgsE") \
+        == "bx:f16_t256"
     assert bench.kernel_key("muon::(anonymous namespace)::apply_kernel(...)") == "apply"
 
 

@@ -1,8 +1,9 @@
 """GPU parity: the HIP Muon step (through the C ABI) against the fp64 oracle.
 
-Bars: relative Frobenius error of O per matrix <= 2e-2 on the bf16 NS path
-and <= 1e-5 on the fp32 path; momentum <= 1e-6; parameters within the drift
-bound of parity_utils; zero-gradient matrices bitwise unchanged.
+Bars: relative Frobenius error of O per matrix <= 2e-2 on the bf16 NS path,
+<= 5e-3 on the fp16 path and <= 1e-5 on the fp32 path; momentum <= 1e-6;
+parameters within the drift bound of parity_utils; zero-gradient matrices
+bitwise unchanged.
 """
 import numpy as np
 import pytest
@@ -20,7 +21,7 @@ def _banner(msg):
     print(f"[gpu-test] {msg}", flush=True)
 
 
-@pytest.mark.parametrize("precision", ["bf16", "fp32"])
+@pytest.mark.parametrize("precision", ["bf16", "fp32", "fp16"])
 def test_tiny_three_steps(precision):
     wl = get_workload("tiny")
     _banner(f"tiny {precision}")
@@ -33,7 +34,7 @@ RAGGED = [(1, 1), (1, 300), (300, 1), (7, 13), (65, 200), (200, 65), (130, 700),
           (257, 513), (513, 257), (1000, 1000), (96, 4304), (1152, 1200), (33, 1030)]
 
 
-@pytest.mark.parametrize("precision", ["bf16", "fp32"])
+@pytest.mark.parametrize("precision", ["bf16", "fp32", "fp16"])
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_ragged_shapes(precision, dtype):
     wl = custom_workload(RAGGED, param=dtype, grad=dtype, seed=11)
@@ -68,6 +69,20 @@ def test_gram_space_recurrence(aspect):
     _banner(f"gram-space aspect {aspect}: worst O {res.worst('o_rel'):.3e}")
     plan.close()
     assert_parity(res, "bf16", f"gram-space {aspect}")
+
+
+def test_fp16_gram_space_recurrence():
+    # fp16 keeps small m on 16-bit operands, so every rectangular matrix of
+    # the set takes the Gram-space form, the 129-row one included.
+    wl = custom_workload(GRAM_SET, seed=23)
+    plan = MuonPlan([(m.rows, m.cols, m.param, m.grad) for m in wl.matrices], precision="fp16")
+    expect = [max(r, c) >= 2 * min(r, c) for r, c in GRAM_SET]
+    assert [bool(plan.matrix_info(i)["gram_space"]) for i in range(wl.n)] == expect
+    _banner(f"fp16 gram-space: {sum(expect)} of {wl.n} matrices")
+    res = run_parity(wl, precision="fp16", steps=3, plan=plan)
+    _banner(f"fp16 gram-space: worst O {res.worst('o_rel'):.3e}")
+    plan.close()
+    assert_parity(res, "fp16", "fp16 gram-space")
 
 
 @pytest.mark.parametrize("ns_steps", [1, 2, 3, 7])
@@ -150,12 +165,13 @@ def test_deterministic_and_batching_invariant():
             assert torch.equal(s, t)
 
 
-@pytest.mark.parametrize("precision", ["bf16", "fp32"])
+@pytest.mark.parametrize("precision", ["bf16", "fp32", "fp16"])
 def test_zero_ns_steps_is_normalised_input(precision):
     wl = custom_workload([(64, 200), (200, 128), (256, 256)], seed=3)
     res = run_parity(wl, precision=precision, steps=1, ns_steps=0)
-    # with k = 0, O = u/||u||: bf16 storage of u costs at most 2^-9 relative
-    bound = 4e-3 if precision == "bf16" else 1e-6
+    # with k = 0, O = u/||u||: 16-bit storage of u costs at most 2^-9
+    # (bf16) or 2^-12 (fp16) relative
+    bound = {"bf16": 4e-3, "fp16": 5e-4, "fp32": 1e-6}[precision]
     for r in res.reports:
         assert r.o_rel <= bound, (r.index, r.o_rel)
 
@@ -166,7 +182,7 @@ def test_plain_momentum_without_nesterov():
     assert_parity(res, "bf16", "no-nesterov")
 
 
-@pytest.mark.parametrize("precision", ["bf16", "fp32"])
+@pytest.mark.parametrize("precision", ["bf16", "fp32", "fp16"])
 @pytest.mark.parametrize("abc", [(15 / 8, -10 / 8, 3 / 8), (1.5, -0.5, 0.0)], ids=["quintic-classic", "cubic"])
 def test_other_ns_coefficients(precision, abc):
     # Eq. 2 with other (a, b, c): the textbook quintic and, with c = 0, the
@@ -227,11 +243,13 @@ def _sample(wl, per_bucket, extra=()):
     return sorted(out)
 
 
-@pytest.mark.parametrize("key,per_bucket", [("1b", 1), ("vla", 1), ("moe", 1), ("8b", 1)])
-def test_full_size_workload_sampled(key, per_bucket):
+@pytest.mark.parametrize("key,per_bucket,precision",
+                         [("1b", 1, "bf16"), ("vla", 1, "bf16"), ("moe", 1, "bf16"), ("8b", 1, "bf16"),
+                          ("8b", 1, "fp16")])
+def test_full_size_workload_sampled(key, per_bucket, precision):
     wl = get_workload(key)
     check = _sample(wl, per_bucket)
-    _banner(f"{key}: full plan on GPU, oracle on {len(check)} sampled matrices")
-    res = run_parity(wl, precision="bf16", steps=1, check=check)
-    _banner(f"{key}: worst O {res.worst('o_rel'):.3e} M {res.worst('m_rel'):.3e}")
-    assert_parity(res, "bf16", key)
+    _banner(f"{key} {precision}: full plan on GPU, oracle on {len(check)} sampled matrices")
+    res = run_parity(wl, precision=precision, steps=1, check=check)
+    _banner(f"{key} {precision}: worst O {res.worst('o_rel'):.3e} M {res.worst('m_rel'):.3e}")
+    assert_parity(res, precision, key)

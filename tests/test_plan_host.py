@@ -35,6 +35,7 @@ def test_workload_plans(plan_check, key):
     _run(plan_check, shapes)
     _run(plan_check, shapes, wave_bytes=1 << 30)
     _run(plan_check, shapes, aspect=0.0)
+    _run(plan_check, shapes, precision=2)
 
 
 def test_ragged_and_random_plans(plan_check):
@@ -43,6 +44,7 @@ def test_ragged_and_random_plans(plan_check):
               (257, 513), (513, 257), (1000, 1000), (96, 4304), (1152, 1200), (2304, 9000), (4100, 4100)]
     _run(plan_check, ragged)
     _run(plan_check, ragged, precision=1)
+    _run(plan_check, ragged, precision=2)
     _run(plan_check, ragged, aspect=1.0)
     _run(plan_check, ragged, aspect=0.0)
     for trial in range(5):
