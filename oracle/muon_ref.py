@@ -13,7 +13,10 @@ What is computed, per matrix (DMuon, Sec. 2.1, Eq. 1 and Eq. 2):
   3. normalise:  X0 = X / (||X||_F + eps)
   4. Eq. 2, k times:  A = X X^T ; B = b*A + c*A A ; X <- a*X + B X
      (this is X <- aX + bXX^TX + c(XX^T)^2 X regrouped; the paper leaves
-     (a,b,c) open, the quintic set used is (3.4445, -4.7750, 2.0315))
+     (a,b,c) open, the quintic set used is (3.4445, -4.7750, 2.0315)).  A
+     schedule of one (a_i, b_i, c_i) per step may replace the fixed triple
+     (Sec. 5, "Configurations": the paper's default is a per-step set):
+     step i then uses its own triple.
   5. O = X^T if transposed else X
   6. Eq. 1 with decoupled weight decay and the shape scale:
         W <- W*(1 - lr*wd) - lr*sqrt(max(1, rows/cols))*O
@@ -21,7 +24,9 @@ What is computed, per matrix (DMuon, Sec. 2.1, Eq. 1 and Eq. 2):
 Readings taken where the paper is silent (momentum form, eps, shape scale,
 decay form, orientation) are listed in the design notes of the repository.
 
-Pins (tests/test_oracle_pins.py): SVD closed form U p^{ok}(s/||s||) V^T,
+Pins (tests/test_oracle_pins.py): SVD closed form U p^{ok}(s/||s||) V^T
+(and U (p_{k-1} o ... o p_0)(s/||s||) V^T for a per-step schedule, with
+hand-computed 1 x 1 values that fix the order),
 transpose / sign / scale / orthogonal equivariance, rank-1 closed form,
 2x2 and 3x3 brute force against numpy.linalg.svd, the Gram-space identity of
 Eq. 4, the momentum closed form under constant gradients, the apply special
@@ -38,6 +43,7 @@ import numpy as np
 
 __all__ = [
     "QUINTIC_ABC",
+    "step_coefficients",
     "DEFAULT_EPS",
     "bf16_round",
     "f32_round",
@@ -119,17 +125,35 @@ def momentum_update(m, g, mu: float, nesterov: bool = True):
     return m_new, u
 
 
+def step_coefficients(abc, steps: int):
+    """The (a, b, c) of each of ``steps`` NS steps.
+
+    ``abc`` is either one triple, used for every step, or a schedule of at
+    least ``steps`` triples, step i taking the i-th (Sec. 5,
+    "Configurations").
+    """
+    seq = list(abc)
+    if len(seq) == 3 and all(np.ndim(v) == 0 for v in seq):
+        return [tuple(float(v) for v in seq)] * int(steps)
+    if len(seq) < int(steps):
+        raise ValueError("coefficient schedule shorter than the step count")
+    out = []
+    for t in seq[:int(steps)]:
+        a, b, c = (float(v) for v in t)
+        out.append((a, b, c))
+    return out
+
+
 def newton_schulz(x, steps: int, abc=QUINTIC_ABC):
     """k steps of the quintic Newton-Schulz iteration (Eq. 2) on an m x n X.
 
     Each step forms the Gram matrix A = X X^T, the polynomial part
     B = b*A + c*A*A, and X <- a*X + B*X, which equals
     a*X + b*X X^T X + c*(X X^T)^2 X.  X is used as given (no orientation,
-    no normalisation).
+    no normalisation).  ``abc`` is a triple or a per-step schedule.
     """
-    a, b, c = (float(v) for v in abc)
     x = np.array(x, dtype=np.float64, copy=True)
-    for _ in range(int(steps)):
+    for a, b, c in step_coefficients(abc, steps):
         gram = x @ x.T
         poly = b * gram + c * (gram @ gram)
         x = a * x + poly @ x
@@ -141,15 +165,15 @@ def newton_schulz_gram(x, steps: int, abc=QUINTIC_ABC):
 
     With G_0 = X_0 X_0^T and P_i = a I + b G_i + c G_i^2, the Gram matrix
     obeys G_{i+1} = P_i G_i P_i and X_k = P_{k-1} ... P_0 X_0.  In exact
-    arithmetic this equals ``newton_schulz``.
+    arithmetic this equals ``newton_schulz``.  With a per-step schedule, P_i
+    takes step i's (a_i, b_i, c_i).
     """
-    a, b, c = (float(v) for v in abc)
     x = np.asarray(x, dtype=np.float64)
     m = x.shape[0]
     eye = np.eye(m)
     gram = x @ x.T
     q = eye.copy()
-    for _ in range(int(steps)):
+    for a, b, c in step_coefficients(abc, steps):
         p = a * eye + b * gram + c * (gram @ gram)
         gram = p @ gram @ p
         q = p @ q

@@ -185,6 +185,83 @@ def test_orthogonal_equivariance():
     assert np.max(np.abs(lhs - rhs)) < 1e-12
 
 
+# ---------------------------------------------------------------- per-step schedules
+# Sec. 5 ("Configurations"): a schedule gives each NS step its own (a, b, c).
+# Step i then maps a singular value x to p_i(x), so k steps apply the
+# composition p_{k-1} o ... o p_0, in that order.
+
+CLASSIC = (15 / 8, -10 / 8, 3 / 8)   # the textbook quintic, p(1) = 1
+CUBIC = (1.5, -0.5, 0.0)             # Newton-Schulz cubic, p(1) = 1
+SCHEDULE = [ABC, ABC, CLASSIC, CUBIC, CLASSIC]
+
+
+def _p_of(t, x):
+    a, b, c = t
+    return a * x + b * x ** 3 + c * x ** 5
+
+
+def _compose(schedule, x):
+    for t in schedule:
+        x = _p_of(t, x)
+    return x
+
+
+def test_schedule_worked_values_by_hand():
+    # 1 x 1 inputs normalise to +-1.  cubic then quintic: p_c(1) = 1.5 - 0.5
+    # = 1, then p(1) = 0.701.  quintic then cubic: p(1) = 0.701, then
+    # 1.5 * 0.701 - 0.5 * 0.701^3 = 1.0515 - 0.5 * 0.344472101 = 0.8792639495.
+    got = R.orthogonalize(np.array([[2.5]]), 2, [CUBIC, ABC], eps=0.0)[0, 0]
+    assert abs(got - 0.701) < 1e-14
+    got = R.orthogonalize(np.array([[-0.3]]), 2, [ABC, CUBIC], eps=0.0)[0, 0]
+    assert abs(got + 0.8792639495) < 1e-12
+
+
+@pytest.mark.parametrize("rows,cols", [(6, 11), (11, 6), (9, 9), (16, 40)])
+def test_schedule_svd_closed_form(rows, cols):
+    rng = np.random.default_rng(rows * 31 + cols)
+    u, s, v = _svd_input(rng, rows, cols, rng.uniform(0.05, 3.0, size=min(rows, cols)))
+    g = (u * s) @ v.T
+    for k in (1, 3, 5):
+        got = R.orthogonalize(g, k, SCHEDULE, eps=0.0)
+        want = (u * _compose(SCHEDULE[:k], s / np.linalg.norm(s))) @ v.T
+        assert _rel(got, want) < 1e-12
+    # the order matters: the reversed schedule is a different map
+    rev = R.orthogonalize(g, 5, SCHEDULE[::-1], eps=0.0)
+    assert _rel(rev, R.orthogonalize(g, 5, SCHEDULE, eps=0.0)) > 1e-3
+
+
+def test_schedule_of_one_triple_is_the_fixed_iteration():
+    rng = np.random.default_rng(4)
+    x = rng.standard_normal((7, 19))
+    assert np.array_equal(R.orthogonalize(x, 5, [ABC] * 5), R.orthogonalize(x, 5, ABC))
+    # a longer schedule uses only its first k triples
+    assert np.array_equal(R.orthogonalize(x, 3, SCHEDULE), R.orthogonalize(x, 3, SCHEDULE[:3]))
+    with pytest.raises(ValueError):
+        R.orthogonalize(x, 6, SCHEDULE)
+
+
+def test_gram_space_identity_with_schedule():
+    rng = np.random.default_rng(9)
+    for rows, cols in [(6, 40), (12, 30)]:
+        x = rng.standard_normal((rows, cols))
+        x /= np.linalg.norm(x)
+        assert _rel(R.newton_schulz_gram(x, 5, SCHEDULE), R.newton_schulz(x, 5, SCHEDULE)) < 1e-11
+
+
+def test_pins_catch_schedule_taken_in_reverse(monkeypatch):
+    orig = R.step_coefficients
+
+    def reversed_schedule(abc, steps):
+        return orig(abc, steps)[::-1]
+    monkeypatch.setattr(R, "step_coefficients", reversed_schedule)
+    rng = np.random.default_rng(6 * 31 + 11)
+    u, s, v = _svd_input(rng, 6, 11, rng.uniform(0.05, 3.0, size=6))
+    g = (u * s) @ v.T
+    got = R.orthogonalize(g, 5, SCHEDULE, eps=0.0)
+    want = (u * _compose(SCHEDULE, s / np.linalg.norm(s))) @ v.T
+    assert not _rel(got, want) < 1e-6
+
+
 def test_gram_space_identity():
     rng = np.random.default_rng(8)
     for rows, cols in [(6, 40), (16, 16), (20, 33)]:
