@@ -102,10 +102,16 @@ typedef struct muon_plan_opts {
   uint32_t flags;                    /* MUON_PLAN_* */
   int64_t wave_bytes;                /* cap on the NS working set of one group ("wave")
                                         of matrices processed together; 0 = default */
-  float gram_min_aspect;             /* bf16 NS matrices with n >= gram_min_aspect * m run the
+  float gram_min_aspect;             /* 16-bit NS matrices with n >= gram_min_aspect * m run the
                                         Gram-space recurrence (Eq. 4); 0 = never.  Must be 0 or
-                                        >= 1; ignored when c = 0 */
+                                        >= 1; ignored when c = 0 at some step */
   int32_t reserved;                  /* must be 0 */
+  const float* abc_per_step;         /* NULL (a, b, c above at every step), or 3 * max_ns_steps
+                                        floats: NS step i uses (a, b, c) = abc_per_step[3i],
+                                        [3i + 1], [3i + 2] (a per-step coefficient set, Sec. 5
+                                        "Configurations").  Read once by muon_plan_create, which
+                                        keeps a copy; every triple obeys the rule for a, b, c.  A
+                                        cubic step (c = 0) keeps every matrix on Eq. 2. */
 } muon_plan_opts;
 
 typedef struct muon_plan_s* muon_plan;
@@ -145,8 +151,8 @@ typedef struct muon_matrix_info {
 
 /* Fills *o with the defaults: precision BF16, max_ns_steps 16,
  * (a,b,c) = (3.4445, -4.7750, 2.0315), eps 1e-7, small_m_threshold 64,
- * flags 0, wave_bytes 0, gram_min_aspect 2.  Returns INVALID_ARG if o is
- * NULL. */
+ * flags 0, wave_bytes 0, gram_min_aspect 2, abc_per_step NULL.  Returns
+ * INVALID_ARG if o is NULL. */
 MUON_API muon_status muon_plan_opts_default(muon_plan_opts* o);
 
 /* Builds a plan for n matrices (orientation, buckets, kernel classes, tile

@@ -44,7 +44,8 @@ class muon_plan_opts(ctypes.Structure):
                 ("a", ctypes.c_float), ("b", ctypes.c_float), ("c", ctypes.c_float),
                 ("eps", ctypes.c_float), ("small_m_threshold", ctypes.c_int32),
                 ("flags", ctypes.c_uint32), ("wave_bytes", ctypes.c_int64),
-                ("gram_min_aspect", ctypes.c_float), ("reserved", ctypes.c_int32)]
+                ("gram_min_aspect", ctypes.c_float), ("reserved", ctypes.c_int32),
+                ("abc_per_step", ctypes.POINTER(ctypes.c_float))]
 
 
 class muon_plan_info(ctypes.Structure):

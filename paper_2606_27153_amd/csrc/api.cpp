@@ -43,6 +43,16 @@ muon_status check_opts(const muon_plan_opts& o) {
     return fail(MUON_ERR_INVALID_ARG, "opts.a, opts.b, opts.c must be finite");
   if (o.c != 0.f && !std::isfinite(o.b / o.c))
     return fail(MUON_ERR_INVALID_ARG, "opts.c must be 0 or large enough that b / c is finite in fp32");
+  if (o.abc_per_step && o.max_ns_steps >= 1 && o.max_ns_steps <= 64) {
+    for (int32_t i = 0; i < o.max_ns_steps; ++i) {
+      const float a = o.abc_per_step[3 * i], b = o.abc_per_step[3 * i + 1], c = o.abc_per_step[3 * i + 2];
+      const std::string at = "opts.abc_per_step step " + std::to_string(i);
+      if (!std::isfinite(a) || !std::isfinite(b) || !std::isfinite(c))
+        return fail(MUON_ERR_INVALID_ARG, at + ": a, b, c must be finite");
+      if (c != 0.f && !std::isfinite(b / c))
+        return fail(MUON_ERR_INVALID_ARG, at + ": c must be 0 or large enough that b / c is finite in fp32");
+    }
+  }
   if (!std::isfinite(o.eps) || o.eps < 0.f) return fail(MUON_ERR_INVALID_ARG, "opts.eps must be finite and >= 0");
   if (o.small_m_threshold < 0) return fail(MUON_ERR_INVALID_ARG, "opts.small_m_threshold must be >= 0");
   if (o.flags & ~uint32_t(MUON_PLAN_HOST_ONLY)) return fail(MUON_ERR_INVALID_ARG, "opts.flags has unknown bits");
@@ -144,9 +154,6 @@ muon_status step_impl(muon_plan plan, void* const* params, const void* const* gr
   s.mu = mu;
   s.wd = wd;
   s.decay = float(1.0 - double(lr) * double(wd));
-  s.a = p.opts.a;
-  s.b = p.opts.b;
-  s.c = p.opts.c;
   s.eps = p.opts.eps;
   s.nesterov = nesterov;
   s.ns_steps = ns_steps;
@@ -187,31 +194,34 @@ muon_status step_impl(muon_plan plan, void* const* params, const void* const* gr
                         (g.pair ? 2.0 : 1.0);
       return run(kind, cl.kclass, fl, 0.0, [&] { return launch_ns_gemm(p, w, cl, stage, g, ws, s, stream); });
     };
-    // Eq. 2: per step A = s^2 X X^T, B = b A + c A A, X' = s (a X + B X).
-    // With c = 0 (the cubic iteration) the Gram stage writes B = b A itself.
+    // Eq. 2: per step A = s^2 X X^T, B = b A + c A A, X' = s (a X + B X),
+    // with step it's (a, b, c).  With c = 0 (a cubic step) the Gram stage
+    // writes B = b A itself.
     for (int32_t it = 0; it < ns_steps; ++it) {
       const int32_t first = it == 0, pin = it & 1, last = it == ns_steps - 1;
+      const float a = p.abc[size_t(3 * it)], b = p.abc[size_t(3 * it + 1)], c = p.abc[size_t(3 * it + 2)];
+      const bool cubic = c == 0.f;
       for (const ClassLaunch& cl : w.launches) {
         if (cl.gram) continue;
-        const bool cubic = s.c == 0.f;
         e = gemm(cl, ST_GRAM, MUON_KERNEL_GRAM,
-                 GemmStep{first, pin, last, SQ_A, SQ_A, cubic ? SQ_B : SQ_A, 0.f, 0.f, cubic ? s.b : 1.f});
+                 GemmStep{first, pin, last, SQ_A, SQ_A, cubic ? SQ_B : SQ_A, 0.f, 0.f, cubic ? b : 1.f});
         if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
       }
-      if (s.c != 0.f)
+      if (!cubic)
         for (const ClassLaunch& cl : w.launches) {
           if (cl.gram) continue;
-          e = gemm(cl, ST_POLY, MUON_KERNEL_POLY, GemmStep{first, pin, last, SQ_A, SQ_A, SQ_B, s.b / s.c, 0.f, s.c});
+          e = gemm(cl, ST_POLY, MUON_KERNEL_POLY, GemmStep{first, pin, last, SQ_A, SQ_A, SQ_B, b / c, 0.f, c});
           if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
         }
       for (const ClassLaunch& cl : w.launches) {
         if (cl.gram) continue;
-        e = gemm(cl, ST_BX, MUON_KERNEL_BX, GemmStep{first, pin, last, SQ_B, SQ_B, SQ_B, s.a, 0.f, 1.f});
+        e = gemm(cl, ST_BX, MUON_KERNEL_BX, GemmStep{first, pin, last, SQ_B, SQ_B, SQ_B, a, 0.f, 1.f});
         if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
       }
     }
-    // Gram space (Eq. 4): G0 = s^2 X0 X0^T; per step P_i = a I + b G + c G^2
-    // (as c (G G + b/c G + a/c I)); Q_{i+1} = P_i Q_i (Q_1 = P_0, which is
+    // Gram space (Eq. 4): G0 = s^2 X0 X0^T; per step P_i = a_i I + b_i G +
+    // c_i G^2 (as c_i (G G + b_i/c_i G + a_i/c_i I); the plan takes this form
+    // only when no c_i is 0); Q_{i+1} = P_i Q_i (Q_1 = P_0, which is
     // written straight into Q0); R = G P_i and G <- P_i R except after the
     // last step; finally O = s Q_k X0.  P Q and G P only need P_i, so they
     // share one launch.
@@ -221,7 +231,8 @@ muon_status step_impl(muon_plan plan, void* const* params, const void* const* gr
       if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
       for (int32_t it = 0; it < ns_steps; ++it) {
         const int32_t pbuf = it == 0 ? SQ_Q0 : SQ_B;
-        e = gemm(cl, ST_POLY, MUON_KERNEL_POLY, GemmStep{0, 0, 0, SQ_A, SQ_A, pbuf, s.b / s.c, s.a / s.c, s.c});
+        const float a = p.abc[size_t(3 * it)], b = p.abc[size_t(3 * it + 1)], c = p.abc[size_t(3 * it + 2)];
+        e = gemm(cl, ST_POLY, MUON_KERNEL_POLY, GemmStep{0, 0, 0, SQ_A, SQ_A, pbuf, b / c, a / c, c});
         const GemmStep qu{0, 0, 0, SQ_B, (it - 1) & 1 ? SQ_Q1 : SQ_Q0, it & 1 ? SQ_Q1 : SQ_Q0, 0.f, 0.f, 1.f};
         GemmStep gr{0, 0, 0, SQ_A, pbuf, SQ_R, 0.f, 0.f, 1.f};
         const bool need_qu = it > 0, need_gr = it + 1 < ns_steps;
@@ -291,6 +302,8 @@ muon_status muon_plan_opts_default(muon_plan_opts* o) {
   o->flags = 0;
   o->wave_bytes = 0;
   o->gram_min_aspect = 2.f;
+  o->reserved = 0;
+  o->abc_per_step = nullptr;
   return ok();
 }
 

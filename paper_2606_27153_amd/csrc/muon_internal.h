@@ -124,7 +124,9 @@ struct TimingRecord {
 };
 
 struct Plan {
-  muon_plan_opts opts;
+  muon_plan_opts opts;              // abc_per_step cleared: the plan keeps abc
+  std::vector<float> abc;           // (a, b, c) of NS steps 0 .. max_ns_steps - 1
+  bool quintic_every_step = true;   // c != 0 at every step (Gram space allowed)
   std::vector<MatHost> mats;        // descriptor order
   std::vector<int32_t> order;       // wave order -> descriptor index
   std::vector<WaveHost> waves;
@@ -160,7 +162,7 @@ int64_t launches_per_step(const Plan& p, int32_t ns_steps);
 // Per-launch arguments shared by the kernel launchers.
 struct StepScalars {
   float lr, mu, wd, decay;  // decay = 1 - lr*wd
-  float a, b, c, eps;
+  float eps;
   int32_t nesterov, ns_steps;
 };
 

@@ -159,11 +159,14 @@ int64_t launches_per_step(const Plan& p, int32_t ns_steps) {
   // Eq. 2: Gram, A*A and B*X per step.  Gram space: the Gram product and
   // B*X once, P_i per step, P Q and G P (one launch when both are due) and
   // P (G P) on all but one step: 3k + 1 launches for k >= 2.
+  // A cubic step (c = 0) of Eq. 2 has no A*A launch.
   int64_t n = 0;
   const int64_t k = ns_steps;
+  int64_t eq2 = 0;
+  for (int32_t it = 0; it < ns_steps; ++it) eq2 += p.abc[size_t(3 * it + 2)] != 0.f ? 3 : 2;
   for (const auto& w : p.waves) {
     n += k > 0 ? 2 : 3;  // momentum, finalize (and apply when no NS step runs)
-    for (const auto& cl : w.launches) n += cl.gram ? (k > 1 ? 3 * k + 1 : 3 * k) : 3 * k;
+    for (const auto& cl : w.launches) n += cl.gram ? (k > 1 ? 3 * k + 1 : 3 * k) : eq2;
   }
   return n;
 }
@@ -171,6 +174,14 @@ int64_t launches_per_step(const Plan& p, int32_t ns_steps) {
 muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan_opts& o, Plan& p,
                        std::string& err) {
   p.opts = o;
+  p.opts.abc_per_step = nullptr;
+  p.abc.resize(size_t(3 * o.max_ns_steps));
+  p.quintic_every_step = true;
+  for (int32_t i = 0; i < o.max_ns_steps; ++i) {
+    for (int32_t j = 0; j < 3; ++j)
+      p.abc[size_t(3 * i + j)] = o.abc_per_step ? o.abc_per_step[3 * i + j] : (j == 0 ? o.a : j == 1 ? o.b : o.c);
+    p.quintic_every_step = p.quintic_every_step && p.abc[size_t(3 * i + 2)] != 0.f;
+  }
   p.mats.resize(size_t(n));
   std::map<std::tuple<int32_t, int64_t, int64_t>, int32_t> buckets;
 
@@ -191,7 +202,7 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
     // Gram space (Eq. 4) pays off whenever n > m; nearly square matrices stay
     // on Eq. 2, where bf16 rounding in the m x m chain costs more accuracy
     // (the Gram matrix squares their conditioning).
-    h.gram = !ci.fp32 && o.gram_min_aspect > 0.f && o.c != 0.f &&
+    h.gram = !ci.fp32 && o.gram_min_aspect > 0.f && p.quintic_every_step &&
                      double(h.n) >= double(o.gram_min_aspect) * double(h.m)
                  ? 1
                  : 0;

@@ -31,9 +31,12 @@ def _dtype_code(t) -> int:
 class MuonPlan:
     """A plan over matrix descriptors ``(rows, cols, param_dtype, grad_dtype)``.
 
-    dtypes are 'f32' or 'bf16'; momentum is always fp32.  bf16-path matrices
-    with max(rows, cols) >= gram_min_aspect * min(rows, cols) run the
-    Gram-space recurrence (Eq. 4); 0 keeps every matrix on Eq. 2.
+    dtypes are 'f32' or 'bf16'; momentum is always fp32.  16-bit-path
+    matrices with max(rows, cols) >= gram_min_aspect * min(rows, cols) run the
+    Gram-space recurrence (Eq. 4); 0 keeps every matrix on Eq. 2.  ``abc`` is
+    one (a, b, c) for every NS step or a list with one triple per step (the
+    per-step coefficient sets of Sec. 5); a list sets max_ns_steps to its
+    length.
     """
 
     def __init__(self, descs: Sequence, *, precision: str = "bf16", max_ns_steps: int = 16,
@@ -53,8 +56,19 @@ class MuonPlan:
         L.check(lib.muon_plan_opts_default(ctypes.byref(opts)))
         opts.precision = PRECISIONS[precision]
         opts.max_ns_steps = int(max_ns_steps)
+        schedule = None
         if abc is not None:
-            opts.a, opts.b, opts.c = (float(v) for v in abc)
+            abc = list(abc)
+            if len(abc) == 3 and all(isinstance(v, (int, float)) for v in abc):
+                opts.a, opts.b, opts.c = (float(v) for v in abc)
+            else:
+                # one (a, b, c) per NS step; the schedule sets max_ns_steps
+                triples = [tuple(float(v) for v in t) for t in abc]
+                if any(len(t) != 3 for t in triples) or not triples:
+                    raise ValueError("abc must be a triple or a non-empty list of triples")
+                opts.max_ns_steps = len(triples)
+                schedule = (ctypes.c_float * (3 * len(triples)))(*[v for t in triples for v in t])
+                opts.abc_per_step = schedule
         opts.eps = float(eps)
         opts.small_m_threshold = int(small_m_threshold)
         opts.wave_bytes = int(wave_bytes)
@@ -167,20 +181,33 @@ class Muon(_optimizer_base()):
 
     Per-parameter state: ``momentum_buffer`` (fp32).  Parameters without a
     gradient are skipped for that step (a new plan is built when the set of
-    stepped parameters changes).
+    stepped parameters changes).  ``ns_coefficients`` is None (the quintic
+    (3.4445, -4.7750, 2.0315) at every step), one (a, b, c), or one triple
+    per NS step.
     """
 
     def __init__(self, params, lr: float = 0.02, momentum: float = 0.95, weight_decay: float = 0.01,
-                 ns_steps: int = 5, nesterov: bool = True, precision: str = "bf16", gram_min_aspect: float = 2.0):
+                 ns_steps: int = 5, nesterov: bool = True, precision: str = "bf16", gram_min_aspect: float = 2.0,
+                 ns_coefficients=None):
         defaults = dict(lr=lr, momentum=momentum, weight_decay=weight_decay, ns_steps=ns_steps,
-                        nesterov=nesterov, precision=precision, gram_min_aspect=gram_min_aspect)
+                        nesterov=nesterov, precision=precision, gram_min_aspect=gram_min_aspect,
+                        ns_coefficients=ns_coefficients)
         super().__init__(params, defaults)
         self._plans = {}
 
-    def _plan_for(self, key, descs, precision, gram_min_aspect):
+    @staticmethod
+    def _coef_key(abc):
+        if abc is None:
+            return None
+        abc = list(abc)
+        if len(abc) == 3 and all(isinstance(v, (int, float)) for v in abc):
+            return tuple(float(v) for v in abc)
+        return tuple(tuple(float(v) for v in t) for t in abc)
+
+    def _plan_for(self, key, descs, precision, gram_min_aspect, abc):
         plan = self._plans.get(key)
         if plan is None:
-            plan = MuonPlan(descs, precision=precision, gram_min_aspect=gram_min_aspect)
+            plan = MuonPlan(descs, precision=precision, gram_min_aspect=gram_min_aspect, abc=abc)
             self._plans[key] = plan
         return plan
 
@@ -198,8 +225,9 @@ class Muon(_optimizer_base()):
                 if p.ndim != 2:
                     raise ValueError("Muon steps 2-D parameters only")
             descs = [(p.shape[0], p.shape[1], _dtype_code(p), _dtype_code(p.grad)) for p in ps]
-            key = (id(group), tuple(descs), group["precision"], group["gram_min_aspect"])
-            plan = self._plan_for(key, descs, group["precision"], group["gram_min_aspect"])
+            abc = group.get("ns_coefficients")
+            key = (id(group), tuple(descs), group["precision"], group["gram_min_aspect"], self._coef_key(abc))
+            plan = self._plan_for(key, descs, group["precision"], group["gram_min_aspect"], abc)
             moms = []
             for p in ps:
                 st = self.state[p]

@@ -86,7 +86,13 @@ def run_parity(wl: Workload, *, precision: str = "bf16", steps: Optional[int] = 
     if own_plan:
         plan = MuonPlan(descs, precision=precision, wave_bytes=wave_bytes, abc=abc,
                         gram_min_aspect=gram_min_aspect)
-    abc = R.QUINTIC_ABC if abc is None else tuple(float(np.float32(v)) for v in abc)
+    # the oracle takes the fp32 values the ABI passes (one triple or a schedule)
+    if abc is None:
+        abc = R.QUINTIC_ABC
+    elif len(abc) == 3 and all(np.ndim(v) == 0 for v in abc):
+        abc = tuple(float(np.float32(v)) for v in abc)
+    else:
+        abc = [tuple(float(np.float32(v)) for v in t) for t in abc]
     params, moms = make_state(torch, wl, device)
     torch.cuda.synchronize()
     # oracle state: its own stored values, starting from the same seeded ones

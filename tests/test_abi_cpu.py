@@ -190,6 +190,60 @@ def test_plan_create_accepts_cubic_coefficients(lib):
     assert lib.muon_plan_destroy(h) == L.MUON_OK
 
 
+QUINTIC = (3.4445, -4.7750, 2.0315)
+CLASSIC = (15 / 8, -10 / 8, 3 / 8)
+CUBIC = (1.5, -0.5, 0.0)
+
+
+def _schedule_opts(lib, triples):
+    opts = L.muon_plan_opts()
+    lib.muon_plan_opts_default(ctypes.byref(opts))
+    opts.flags = L.MUON_PLAN_HOST_ONLY
+    opts.max_ns_steps = len(triples)
+    arr = (ctypes.c_float * (3 * len(triples)))(*[v for t in triples for v in t])
+    opts.abc_per_step = arr
+    return opts, arr
+
+
+@pytest.mark.parametrize("bad", [(float("nan"), -1.0, 1.0), (1.0, float("inf"), 1.0), (1.0, -1.0, 1e-39)])
+def test_schedule_rejects_bad_triples(lib, bad):
+    opts, arr = _schedule_opts(lib, [QUINTIC, QUINTIC, bad, QUINTIC])
+    st, h = _create(lib, [(8, 8, 1, 1, 0)], opts)
+    assert st == L.MUON_ERR_INVALID_ARG
+    assert "abc_per_step step 2" in L.last_error()
+
+
+def _info(lib, h):
+    info = L.muon_plan_info()
+    assert lib.muon_plan_get_info(h, ctypes.byref(info)) == L.MUON_OK
+    return info
+
+
+def test_schedule_form_choice_and_launch_count(lib):
+    # one wide and one square bf16 matrix
+    descs = [(256, 1024, 1, 1, 0), (512, 512, 1, 1, 0)]
+    opts, arr = _schedule_opts(lib, [QUINTIC, QUINTIC, QUINTIC, CLASSIC, CLASSIC])
+    st, h = _create(lib, descs, opts)
+    assert st == L.MUON_OK
+    info = _info(lib, h)
+    # every c != 0: the wide matrix takes the Gram-space form (3k + 1 = 16
+    # launches), the square one Eq. 2 (3 per step)
+    assert info.n_gram == 1
+    assert info.launches_per_step == 2 + 16 + 15
+    # the plan keeps its own copy of the schedule
+    arr[3 * 4 + 2] = 0.0
+    assert _info(lib, h).launches_per_step == 2 + 16 + 15
+    assert lib.muon_plan_destroy(h) == L.MUON_OK
+    # a cubic step keeps every matrix on Eq. 2 and drops that step's A*A
+    opts, arr = _schedule_opts(lib, [QUINTIC, QUINTIC, QUINTIC, CUBIC, CLASSIC])
+    st, h = _create(lib, descs, opts)
+    assert st == L.MUON_OK
+    info = _info(lib, h)
+    assert info.n_gram == 0
+    assert info.launches_per_step == 2 + 14
+    assert lib.muon_plan_destroy(h) == L.MUON_OK
+
+
 def test_null_arguments(lib):
     h = ctypes.c_void_p()
     assert lib.muon_plan_create(None, 1, None, ctypes.byref(h)) == L.MUON_ERR_INVALID_ARG

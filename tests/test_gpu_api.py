@@ -12,13 +12,18 @@ pytestmark = pytest.mark.gpu
 SHAPES = [(256, 768), (768, 256), (512, 512), (64, 300)]
 
 
-def test_optimizer_wrapper_matches_plan_step():
+SCHEDULE = [(3.4445, -4.7750, 2.0315)] * 3 + [(15 / 8, -10 / 8, 3 / 8)] * 2
+
+
+@pytest.mark.parametrize("precision,abc", [("bf16", None), ("fp16", SCHEDULE)], ids=["bf16", "fp16-schedule"])
+def test_optimizer_wrapper_matches_plan_step(precision, abc):
     wl = custom_workload(SHAPES, seed=21)
     pa, ma = make_state(torch, wl, "cuda:0")
     pb, _ = make_state(torch, wl, "cuda:0")
     params = [torch.nn.Parameter(p) for p in pb]
-    opt = Muon(params, lr=0.02, momentum=0.95, weight_decay=0.01, ns_steps=5)
-    plan = MuonPlan([(m.rows, m.cols, m.param, m.grad) for m in wl.matrices])
+    opt = Muon(params, lr=0.02, momentum=0.95, weight_decay=0.01, ns_steps=5, precision=precision,
+               ns_coefficients=abc)
+    plan = MuonPlan([(m.rows, m.cols, m.param, m.grad) for m in wl.matrices], precision=precision, abc=abc)
     for step in range(3):
         g = make_grads(torch, wl, step, "cuda:0")
         plan.step(pa, g, ma, lr=0.02, momentum=0.95, weight_decay=0.01, ns_steps=5)

@@ -192,6 +192,31 @@ def test_other_ns_coefficients(precision, abc):
     assert_parity(res, precision, f"abc={abc}")
 
 
+QUINTIC = (3.4445, -4.7750, 2.0315)
+SCHEDULE = [QUINTIC] * 3 + [(15 / 8, -10 / 8, 3 / 8)] * 2
+SCHEDULE_CUBIC = [QUINTIC] * 3 + [(1.5, -0.5, 0.0), (15 / 8, -10 / 8, 3 / 8)]
+
+
+@pytest.mark.parametrize("precision", ["bf16", "fp16", "fp32"])
+@pytest.mark.parametrize("schedule", [SCHEDULE, SCHEDULE_CUBIC], ids=["quintic-steps", "with-cubic-step"])
+def test_per_step_coefficients(precision, schedule):
+    # one (a, b, c) per NS step (Sec. 5).  Without a cubic step the wide
+    # 16-bit matrices take the Gram-space form, whose P_i change per step;
+    # a cubic step keeps everything on Eq. 2 and skips that step's A*A.
+    wl = custom_workload([(64, 200), (200, 128), (256, 768), (768, 256), (300, 300), (512, 2048)], seed=7)
+    plan = MuonPlan([(m.rows, m.cols, m.param, m.grad) for m in wl.matrices], precision=precision, abc=schedule)
+    n_gram = plan.info()["n_gram"]
+    if schedule is SCHEDULE_CUBIC or precision == "fp32":
+        assert n_gram == 0
+    else:
+        assert n_gram == (4 if precision == "fp16" else 3)
+    _banner(f"schedule {precision} {len(schedule)} steps, {n_gram} Gram-space matrices")
+    res = run_parity(wl, precision=precision, steps=2, plan=plan, abc=schedule)
+    _banner(f"schedule {precision}: worst O {res.worst('o_rel'):.3e}")
+    plan.close()
+    assert_parity(res, precision, f"schedule {precision}")
+
+
 def test_step_and_debug_step_are_bitwise_identical():
     wl = custom_workload([(300, 500), (500, 300), (2048, 512)], seed=6)
     descs = [(m.rows, m.cols, m.param, m.grad) for m in wl.matrices]
