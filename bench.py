@@ -1,6 +1,8 @@
 """Benchmark of the single-GPU Muon optimizer step (one JSON line on stdout).
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 8b]
+    python bench.py --sweep [--config 8b]          # per-shape batch sweep (table)
+    python bench.py --owner-share 8 [--owner 0]    # one owner's cost-balanced share
 
 A step is one muon_step over every matrix of the chosen synthetic set:
 momentum + Nesterov, Frobenius normalisation, 5 Newton-Schulz steps, apply.
@@ -223,6 +225,100 @@ def cpu_baseline(wl, budget_s: float):
                        + "; ".join(sampled) + "), scaled by bucket counts to the whole set")}
 
 
+def ns_cost(rows: int, cols: int, k: int = 5, gram_min_aspect: float = 2.0) -> float:
+    """Algorithmic NS flops of one matrix in the form the plan gives it
+    (16-bit classes; Eq. 4 when n >= aspect * m and m > 64, else Eq. 2)."""
+    m, n = min(rows, cols), max(rows, cols)
+    if gram_min_aspect > 0 and n >= gram_min_aspect * m and m > 64:
+        return 3.0 * m * m * n + (4 * k - 3) * float(m) ** 3
+    return k * (3.0 * m * m * n + float(m) ** 3)
+
+
+def lpt_partition(costs, n_owners: int):
+    """Longest-processing-time assignment: matrices in decreasing cost, each
+    to the owner with the least load so far (ties to the lowest rank).
+    Returns (owners, loads); owners[r] lists matrix indices in input order."""
+    owners = [[] for _ in range(n_owners)]
+    loads = [0.0] * n_owners
+    for i in sorted(range(len(costs)), key=lambda i: (-costs[i], i)):
+        r = min(range(n_owners), key=lambda r: (loads[r], r))
+        owners[r].append(i)
+        loads[r] += costs[i]
+    return [sorted(o) for o in owners], loads
+
+
+def time_steps(plan, params, grads, moms, kw, warmup: int, steps: int):
+    """Runs warmup steps, then times ``steps`` steps as one block (returns ms
+    per step) and each step on its own with events on the step's stream
+    (returns the per-step list)."""
+    import torch
+    for _ in range(warmup):
+        plan.step(params, grads, moms, **kw)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    stream = kw["stream"]
+    t0 = time.perf_counter()
+    ev[0].record(stream)
+    for i in range(steps):
+        plan.step(params, grads, moms, **kw)
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    return (t1 - t0) * 1e3 / steps, [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+
+
+def percentile(vals, q: float) -> float:
+    v = sorted(vals)
+    if not v:
+        return 0.0
+    pos = (len(v) - 1) * q
+    lo = int(pos)
+    hi = min(lo + 1, len(v) - 1)
+    return v[lo] + (v[hi] - v[lo]) * (pos - lo)
+
+
+def batch_sweep(wl, precision: str, gram_min_aspect: float, batches=(1, 2, 4, 8, 16), steps: int = 5) -> str:
+    """Per distinct (rows, cols, dtypes) of the set: the step time of a plan
+    holding b copies, for each batch size b, and the per-matrix time
+    normalised to b = 1 (the measured c_{s,b} of Sec. 3.4)."""
+    import dataclasses
+
+    import torch
+
+    from paper_2606_27153_amd.optim import MuonPlan
+    from paper_2606_27153_amd.workloads import make_grads, make_state
+
+    shapes = []
+    for m in wl.matrices:
+        key = (m.rows, m.cols, m.param, m.grad)
+        if key not in shapes:
+            shapes.append(key)
+    dev = "cuda:0"
+    lines = [f"# Batch sweep, {wl.key} set, {precision} NS, {wl.ns_steps} NS steps: ms per muon_step over b "
+             f"copies of one shape (median of {steps} steps)", "",
+             "| rows x cols | b | ms / step | ms / matrix | per-matrix vs b = 1 |", "|---|---|---|---|---|"]
+    for rows, cols, pd, gd in shapes:
+        base = None
+        for b in batches:
+            same = [m for m in wl.matrices if (m.rows, m.cols, m.param, m.grad) == (rows, cols, pd, gd)]
+            spec = ([m for m in same if not m.zero_grad] or same)[0]   # a matrix that runs the NS chain
+            sub = dataclasses.replace(wl, key=f"{rows}x{cols}", description="", matrices=[spec] * b)
+            plan = MuonPlan([(rows, cols, pd, gd)] * b, precision=precision, gram_min_aspect=gram_min_aspect)
+            params, moms = make_state(torch, sub, dev)
+            grads = make_grads(torch, sub, 0, dev)
+            kw = dict(lr=wl.lr, momentum=wl.momentum, weight_decay=wl.weight_decay, ns_steps=wl.ns_steps,
+                      nesterov=wl.nesterov, workspace=plan.workspace(dev), stream=torch.cuda.current_stream(dev))
+            _, per = time_steps(plan, params, grads, moms, kw, 2, steps)
+            ms = percentile(per, 0.5)
+            base = ms if base is None else base
+            lines.append(f"| {rows} x {cols} | {b} | {ms:.3f} | {ms / b:.4f} | {ms / b / base:.3f} |")
+            log(f"[sweep] {rows}x{cols} b={b}: {ms:.3f} ms/step")
+            plan.close()
+            del params, moms, grads, plan
+            torch.cuda.empty_cache()
+    return "\n".join(lines)
+
+
 def gemm_algorithmic_bytes(plan, k: int, kind: str, kclass: str, param_bytes) -> float:
     """HBM bytes one muon_step must move for the launches of one GEMM kind and
     kernel class, each operand read once and each output written once:
@@ -271,6 +367,12 @@ def main(argv=None) -> int:
                     help="with --rocprof-summary: write profiles/traffic_summary.txt for these comma-separated "
                          "kernel keys")
     ap.add_argument("--traffic-command", default="", help="command recorded in the traffic summary")
+    ap.add_argument("--sweep", action="store_true",
+                    help="print the per-shape batch sweep (b = 1, 2, 4, 8, 16) as a table instead of the JSON line")
+    ap.add_argument("--owner-share", type=int, default=1, metavar="N",
+                    help="time one of N owners' shares of the set (LPT on algorithmic cost): the per-GPU work "
+                         "of an N-GPU run, as a diagnostic")
+    ap.add_argument("--owner", type=int, default=0, help="which owner's share with --owner-share")
     args = ap.parse_args(argv)
 
     if args.rocprof_summary:
@@ -295,6 +397,24 @@ def main(argv=None) -> int:
         return 1
     dev = "cuda:0"
     wl = get_workload(args.config)
+    if args.sweep:
+        print(batch_sweep(wl, args.precision, args.gram_min_aspect), flush=True)
+        return 0
+    share = None
+    if args.owner_share > 1:
+        import dataclasses
+        if not 0 <= args.owner < args.owner_share:
+            log("--owner must be in [0, --owner-share)")
+            return 2
+        costs = [ns_cost(m.rows, m.cols, wl.ns_steps, args.gram_min_aspect) for m in wl.matrices]
+        owners, loads = lpt_partition(costs, args.owner_share)
+        mine = owners[args.owner]
+        share = {"owners": args.owner_share, "owner": args.owner, "matrices": len(mine),
+                 "cost_share": round(loads[args.owner] / sum(costs), 4),
+                 "imbalance": round(max(loads) / (sum(loads) / len(loads)), 4)}
+        wl = dataclasses.replace(wl, key=f"{wl.key}/owner{args.owner}of{args.owner_share}",
+                                 description=f"{wl.description}; owner {args.owner} of {args.owner_share} (LPT)",
+                                 matrices=[wl.matrices[i] for i in mine])
     log(f"[bench] workload {wl.key}: {wl.description}; {wl.elements() / 1e9:.2f} G elements")
     plan = MuonPlan([(m.rows, m.cols, m.param, m.grad) for m in wl.matrices], precision=args.precision,
                     wave_bytes=args.wave_bytes, gram_min_aspect=args.gram_min_aspect)
@@ -324,15 +444,9 @@ def main(argv=None) -> int:
 
     plan.set_timing(True)
     plan.timing_read(reset=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        plan.step(params, grads, moms, **kw)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
+    ms_per_step, per_step = time_steps(plan, params, grads, moms, kw, 0, args.steps)
     plan.set_timing(False)
     stats = plan.timing_read(reset=True)
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
     log(f"[bench] {args.steps} timed steps: {ms_per_step:.3f} ms/step")
 
     # fp16 MFMA has the bf16 dense peak
@@ -409,10 +523,14 @@ def main(argv=None) -> int:
         "mfma_util_pct_ns_gemms": round(mfma_util, 2),
         "ns_gemm_tflops": round(ns_tflops, 2),
         "ns_gemm_ms_per_step": round(gemm_ms, 3),
+        "step_ms_median": round(percentile(per_step, 0.5), 3),
+        "step_ms_p10": round(percentile(per_step, 0.1), 3),
+        "step_ms_p90": round(percentile(per_step, 0.9), 3),
         "step_roofline_floor_ms": round(floor_ms, 3),
         "step_roofline_frac": round(floor_ms / ms_per_step, 4),
         "roofline": roof,
         "cpu_baseline": cpu,
+        "owner_share": share,
         "kernels": per_kernel,
     }
     print(json.dumps(out), flush=True)

@@ -1,9 +1,11 @@
-"""Host-side pieces of bench.py: the CLI contract for more than one GPU and
-the algorithmic byte counts used for the roofline, on host-only plans."""
+"""Host-side pieces of bench.py: the CLI contract for more than one GPU, the
+algorithmic byte counts used for the roofline, the per-matrix cost and the
+LPT split of the owner-share diagnostic, on host-only plans."""
 import os
 import subprocess
 import sys
 
+import numpy as np
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -11,6 +13,7 @@ sys.path.insert(0, ROOT)
 
 import bench  # noqa: E402
 from paper_2606_27153_amd.optim import MuonPlan  # noqa: E402
+from paper_2606_27153_amd.workloads import get_workload  # noqa: E402
 
 
 def test_more_than_one_gpu_is_refused():
@@ -68,3 +71,44 @@ def test_traffic_summary_round_trip(tmp_path):
     got = bench.read_traffic("symm:bf16_t256", path=str(out))
     assert got == pytest.approx((200.0 * 2 + 50.0 * 1) * 1024)
     assert bench.read_traffic("bx:bf16_t256", path=str(out)) is None
+
+
+def test_ns_cost_matches_the_plan_accounting():
+    # the LPT cost of each matrix is the algorithmic flops of the form the
+    # plan gives it (Eq. 4 or Eq. 2), summed as the plan reports them
+    for key in ("1b", "8b", "vla"):
+        wl = get_workload(key)
+        plan = MuonPlan([(m.rows, m.cols, m.param, m.grad) for m in wl.matrices], host_only=True)
+        info = plan.info()
+        want = info["ns_flops_fixed"] + 5 * info["ns_flops_step"]
+        got = sum(bench.ns_cost(m.rows, m.cols, 5) for m in wl.matrices)
+        assert abs(got - want) <= 1e-9 * want, key
+        plan.close()
+
+
+def test_lpt_partition_against_brute_force():
+    import itertools
+    rng = np.random.default_rng(5)
+    for trial in range(40):
+        n_items = int(rng.integers(1, 9))
+        n_owners = int(rng.integers(1, 4))
+        costs = [float(c) for c in rng.integers(1, 50, size=n_items)]
+        owners, loads = bench.lpt_partition(costs, n_owners)
+        assert sorted(i for o in owners for i in o) == list(range(n_items))
+        for r, o in enumerate(owners):
+            assert abs(loads[r] - sum(costs[i] for i in o)) < 1e-9
+        best = min(max(sum(costs[i] for i in range(n_items) if a[i] == r) for r in range(n_owners))
+                   for a in itertools.product(range(n_owners), repeat=n_items))
+        # Graham's bound for LPT: makespan <= (4/3 - 1/(3N)) * optimum
+        assert max(loads) <= (4 / 3 - 1 / (3 * n_owners)) * best + 1e-9
+
+
+def test_percentile_and_share_of_the_8b_set():
+    assert bench.percentile([3.0, 1.0, 2.0], 0.5) == 2.0
+    assert bench.percentile([1.0, 2.0], 0.9) == pytest.approx(1.9)
+    wl = get_workload("8b")
+    costs = [bench.ns_cost(m.rows, m.cols) for m in wl.matrices]
+    owners, loads = bench.lpt_partition(costs, 8)
+    # 224 matrices in three shapes split into 8 nearly equal shares
+    assert max(loads) / (sum(loads) / 8) < 1.02
+    assert sum(len(o) for o in owners) == 224
