@@ -373,6 +373,9 @@ def main(argv=None) -> int:
                     help="time one of N owners' shares of the set (LPT on algorithmic cost): the per-GPU work "
                          "of an N-GPU run, as a diagnostic")
     ap.add_argument("--owner", type=int, default=0, help="which owner's share with --owner-share")
+    ap.add_argument("--autotune", action="store_true",
+                    help="measure each shape's GEMM tile first (cached on disk, see --tune-cache) and plan with it")
+    ap.add_argument("--tune-cache", default=None, help="tile cache file for --autotune")
     args = ap.parse_args(argv)
 
     if args.rocprof_summary:
@@ -416,8 +419,19 @@ def main(argv=None) -> int:
                                  description=f"{wl.description}; owner {args.owner} of {args.owner_share} (LPT)",
                                  matrices=[wl.matrices[i] for i in mine])
     log(f"[bench] workload {wl.key}: {wl.description}; {wl.elements() / 1e9:.2f} G elements")
-    plan = MuonPlan([(m.rows, m.cols, m.param, m.grad) for m in wl.matrices], precision=args.precision,
-                    wave_bytes=args.wave_bytes, gram_min_aspect=args.gram_min_aspect)
+    descs = [(m.rows, m.cols, m.param, m.grad) for m in wl.matrices]
+    tuned = None
+    if args.autotune:
+        from paper_2606_27153_amd.autotune import tune
+        t0 = time.perf_counter()
+        hints = tune(descs, precision=args.precision, gram_min_aspect=args.gram_min_aspect, ns_steps=wl.ns_steps,
+                     cache_path=args.tune_cache)
+        descs = [d + (h,) for d, h in zip(descs, hints)]
+        tuned = {"seconds": round(time.perf_counter() - t0, 1),
+                 "tiles": sorted({f"{min(d[0], d[1])}x{max(d[0], d[1])}:{d[4]}" for d in descs})}
+        log(f"[bench] autotune: {tuned}")
+    plan = MuonPlan(descs, precision=args.precision, wave_bytes=args.wave_bytes,
+                    gram_min_aspect=args.gram_min_aspect)
     info = plan.info()
     log(f"[bench] plan: {info['n_waves']} waves, {info['n_buckets']} buckets, "
         f"{info['launches_per_step']} launches/step at max steps, workspace {info['workspace_bytes'] / 2**30:.2f} GiB")
@@ -519,7 +533,7 @@ def main(argv=None) -> int:
                    "elements": wl.elements(), "ns_steps": wl.ns_steps,
                    "params": sorted({m.param for m in wl.matrices}), "momentum": "f32",
                    "ns_operands": args.precision, "gram_space_matrices": info["n_gram"],
-                   "gram_min_aspect": args.gram_min_aspect, "parallelism": "single GPU"},
+                   "gram_min_aspect": args.gram_min_aspect, "autotune": tuned, "parallelism": "single GPU"},
         "mfma_util_pct_ns_gemms": round(mfma_util, 2),
         "ns_gemm_tflops": round(ns_tflops, 2),
         "ns_gemm_ms_per_step": round(gemm_ms, 3),

@@ -88,7 +88,12 @@ typedef struct muon_matrix_desc {
   int32_t param_dtype;
   int32_t grad_dtype;
   int32_t momentum_dtype;
-  int32_t reserved;                  /* must be 0 */
+  int32_t tile_hint;                 /* 0: the planner's cost model picks the GEMM tile; 64, 128 or
+                                        256: use that output tile for this matrix (a measured
+                                        choice, e.g. from an autotuner's cache; Sec. 3.3 tunes the
+                                        schedule per shape).  256 needs 16-bit operands: with fp32
+                                        NS (MUON_NS_FP32, or small m under bf16) it is UNSUPPORTED.
+                                        Anything else is INVALID_ARG. */
 } muon_matrix_desc;
 
 typedef struct muon_plan_opts {
@@ -159,7 +164,7 @@ MUON_API muon_status muon_plan_opts_default(muon_plan_opts* o);
  * tables, workspace layout).  Unless MUON_PLAN_HOST_ONLY is set, the plan is
  * bound to the current HIP device and uploads its tables there (the only
  * host-to-device copy outside muon_step).  opts may be NULL (defaults).
- * Errors: INVALID_ARG (null, n < 1, rows or cols < 1 or >= 2^31, reserved != 0,
+ * Errors: INVALID_ARG (null, n < 1, rows or cols < 1 or >= 2^31, bad tile_hint,
  * opts out of range), UNSUPPORTED (dtypes), OUT_OF_MEMORY, DEVICE. */
 MUON_API muon_status muon_plan_create(const muon_matrix_desc* mats, int32_t n,
                              const muon_plan_opts* opts, muon_plan* out);

@@ -36,7 +36,7 @@ MUON_PLAN_HOST_ONLY = 0x1
 class muon_matrix_desc(ctypes.Structure):
     _fields_ = [("rows", ctypes.c_int64), ("cols", ctypes.c_int64),
                 ("param_dtype", ctypes.c_int32), ("grad_dtype", ctypes.c_int32),
-                ("momentum_dtype", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("momentum_dtype", ctypes.c_int32), ("tile_hint", ctypes.c_int32)]
 
 
 class muon_plan_opts(ctypes.Structure):

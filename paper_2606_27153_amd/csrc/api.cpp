@@ -324,7 +324,8 @@ muon_status muon_plan_create(const muon_matrix_desc* mats, int32_t n, const muon
     const std::string who = "matrix " + std::to_string(i);
     if (d.rows < 1 || d.cols < 1 || d.rows >= (int64_t(1) << 31) || d.cols >= (int64_t(1) << 31))
       return fail(MUON_ERR_INVALID_ARG, who + ": rows and cols must be in [1, 2^31)");
-    if (d.reserved != 0) return fail(MUON_ERR_INVALID_ARG, who + ": reserved must be 0");
+    if (d.tile_hint != 0 && d.tile_hint != 64 && d.tile_hint != 128 && d.tile_hint != 256)
+      return fail(MUON_ERR_INVALID_ARG, who + ": tile_hint must be 0, 64, 128 or 256");
     if (!valid_dtype(d.param_dtype) || !valid_dtype(d.grad_dtype))
       return fail(MUON_ERR_UNSUPPORTED, who + ": param and grad dtypes must be MUON_F32 or MUON_BF16");
     if (d.momentum_dtype != MUON_F32) return fail(MUON_ERR_UNSUPPORTED, who + ": momentum must be MUON_F32");

@@ -45,12 +45,20 @@ double padded_cost(int64_t m, int64_t n, int32_t tile) {
   return 3.0 * mp * mp * np + mp * mp * mp;
 }
 
-int32_t choose_class(int64_t m, int64_t n, const muon_plan_opts& o) {
-  // fp16 keeps enough precision for every size; bf16 hands small m to fp32
+// Kernel class of an m x n matrix: the operand type follows the precision
+// (fp16 keeps enough precision for every size; bf16 hands small m to fp32),
+// the tile is the caller's hint or the cheapest by the padded cost model.
+// Returns -1 when the hinted tile does not exist for that operand type.
+int32_t choose_class(int64_t m, int64_t n, const muon_plan_opts& o, int32_t tile_hint) {
   const bool f16 = o.precision == MUON_NS_FP16;
   const bool fp32 = o.precision == MUON_NS_FP32 || (!f16 && m <= o.small_m_threshold);
   const int32_t lo = fp32 ? KC_F32_128 : f16 ? KC_F16_256 : KC_BF16_256;
   const int32_t hi = fp32 ? KC_F32_64 : f16 ? KC_F16_64 : KC_BF16_64;
+  if (tile_hint != 0) {
+    for (int32_t kc = lo; kc <= hi; ++kc)
+      if (kClasses[kc].tile == tile_hint) return kc;
+    return -1;
+  }
   int32_t best = hi;
   double best_cost = 0;
   for (int32_t kc = lo; kc <= hi; ++kc) {
@@ -196,7 +204,12 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
     h.param_dtype = d.param_dtype;
     h.grad_dtype = d.grad_dtype;
     h.momentum_dtype = d.momentum_dtype;
-    h.kclass = choose_class(h.m, h.n, o);
+    h.kclass = choose_class(h.m, h.n, o, d.tile_hint);
+    if (h.kclass < 0) {
+      err = "matrix " + std::to_string(i) + ": tile_hint " + std::to_string(d.tile_hint) +
+            " has no kernel class with fp32 operands";
+      return MUON_ERR_UNSUPPORTED;
+    }
     const ClassInfo& ci = kClasses[h.kclass];
     h.fp32_ns = ci.fp32;
     // Gram space (Eq. 4) pays off whenever n > m; nearly square matrices stay

@@ -29,25 +29,39 @@ def _dtype_code(t) -> int:
 
 
 class MuonPlan:
-    """A plan over matrix descriptors ``(rows, cols, param_dtype, grad_dtype)``.
+    """A plan over matrix descriptors ``(rows, cols, param_dtype, grad_dtype)``
+    or ``(rows, cols, param_dtype, grad_dtype, tile_hint)`` (0, 64, 128, 256).
 
     dtypes are 'f32' or 'bf16'; momentum is always fp32.  16-bit-path
     matrices with max(rows, cols) >= gram_min_aspect * min(rows, cols) run the
     Gram-space recurrence (Eq. 4); 0 keeps every matrix on Eq. 2.  ``abc`` is
     one (a, b, c) for every NS step or a list with one triple per step (the
     per-step coefficient sets of Sec. 5); a list sets max_ns_steps to its
-    length.
+    length.  ``autotune`` picks each shape's GEMM tile by measurement on
+    the GPU (see autotune.py), reading and filling the on-disk cache.
     """
 
     def __init__(self, descs: Sequence, *, precision: str = "bf16", max_ns_steps: int = 16,
                  abc: Optional[Sequence[float]] = None, eps: float = 1e-7,
                  small_m_threshold: int = 64, wave_bytes: int = 0, gram_min_aspect: float = 2.0,
-                 host_only: bool = False):
+                 host_only: bool = False, autotune: bool = False, tune_cache: Optional[str] = None,
+                 tune_ns_steps: int = 5):
         lib = L.load()
         n = len(descs)
+        if autotune:
+            # measured tile per shape (cached on disk) for descriptors without a hint
+            from .autotune import tune
+            todo = [i for i, d in enumerate(descs) if len(d) < 5 or not d[4]]
+            if todo:
+                hints = tune([descs[i] for i in todo], precision=precision, gram_min_aspect=gram_min_aspect,
+                             ns_steps=tune_ns_steps, cache_path=tune_cache)
+                descs = list(descs)
+                for i, h in zip(todo, hints):
+                    descs[i] = tuple(descs[i][:4]) + (h,)
         arr = (L.muon_matrix_desc * max(n, 1))()
         for i, d in enumerate(descs):
-            rows, cols, pd, gd = d
+            rows, cols, pd, gd = d[:4]
+            arr[i].tile_hint = int(d[4]) if len(d) > 4 else 0
             arr[i].rows, arr[i].cols = int(rows), int(cols)
             arr[i].param_dtype = _DT[pd] if isinstance(pd, str) else int(pd)
             arr[i].grad_dtype = _DT[gd] if isinstance(gd, str) else int(gd)
@@ -188,12 +202,13 @@ class Muon(_optimizer_base()):
 
     def __init__(self, params, lr: float = 0.02, momentum: float = 0.95, weight_decay: float = 0.01,
                  ns_steps: int = 5, nesterov: bool = True, precision: str = "bf16", gram_min_aspect: float = 2.0,
-                 ns_coefficients=None):
+                 ns_coefficients=None, autotune: bool = False, tune_cache: Optional[str] = None):
         defaults = dict(lr=lr, momentum=momentum, weight_decay=weight_decay, ns_steps=ns_steps,
                         nesterov=nesterov, precision=precision, gram_min_aspect=gram_min_aspect,
-                        ns_coefficients=ns_coefficients)
+                        ns_coefficients=ns_coefficients, autotune=autotune)
         super().__init__(params, defaults)
         self._plans = {}
+        self._tune_cache = tune_cache
 
     @staticmethod
     def _coef_key(abc):
@@ -204,10 +219,12 @@ class Muon(_optimizer_base()):
             return tuple(float(v) for v in abc)
         return tuple(tuple(float(v) for v in t) for t in abc)
 
-    def _plan_for(self, key, descs, precision, gram_min_aspect, abc):
+    def _plan_for(self, key, descs, group):
         plan = self._plans.get(key)
         if plan is None:
-            plan = MuonPlan(descs, precision=precision, gram_min_aspect=gram_min_aspect, abc=abc)
+            plan = MuonPlan(descs, precision=group["precision"], gram_min_aspect=group["gram_min_aspect"],
+                            abc=group.get("ns_coefficients"), autotune=group.get("autotune", False),
+                            tune_cache=self._tune_cache, tune_ns_steps=group["ns_steps"])
             self._plans[key] = plan
         return plan
 
@@ -226,8 +243,9 @@ class Muon(_optimizer_base()):
                     raise ValueError("Muon steps 2-D parameters only")
             descs = [(p.shape[0], p.shape[1], _dtype_code(p), _dtype_code(p.grad)) for p in ps]
             abc = group.get("ns_coefficients")
-            key = (id(group), tuple(descs), group["precision"], group["gram_min_aspect"], self._coef_key(abc))
-            plan = self._plan_for(key, descs, group["precision"], group["gram_min_aspect"], abc)
+            key = (id(group), tuple(descs), group["precision"], group["gram_min_aspect"], self._coef_key(abc),
+                   group.get("autotune", False))
+            plan = self._plan_for(key, descs, group)
             moms = []
             for p in ps:
                 st = self.state[p]

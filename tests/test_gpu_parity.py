@@ -217,6 +217,29 @@ def test_per_step_coefficients(precision, schedule):
     assert_parity(res, precision, f"schedule {precision}")
 
 
+def test_autotuned_tiles(tmp_path, monkeypatch):
+    # measured tile per shape (Sec. 3.3): the tuned plan is held to the same
+    # bar, and a second tuning of the same shapes is served by the cache
+    from paper_2606_27153_amd import autotune as T
+    shapes = [(300, 900), (900, 300), (1408, 2048), (64, 700), (1000, 1000)]
+    wl = custom_workload(shapes, seed=31)
+    descs = [(m.rows, m.cols, m.param, m.grad) for m in wl.matrices]
+    cache = str(tmp_path / "tiles.json")
+    hints = T.tune(descs, precision="bf16", cache_path=cache, steps=2)
+    _banner(f"autotune: tiles {hints}")
+    assert all(h in (64, 128, 256) for h in hints) and hints[3] in (64, 128)
+
+    def no_measure(*a, **k):
+        raise AssertionError("cached set measured again")
+    monkeypatch.setattr(T, "measure_set_ms", no_measure)
+    assert T.tune(descs, precision="bf16", cache_path=cache) == hints
+    plan = MuonPlan([d + (h,) for d, h in zip(descs, hints)])
+    assert [plan.matrix_info(i)["tile"] for i in range(wl.n)] == hints
+    res = run_parity(wl, precision="bf16", steps=2, plan=plan)
+    plan.close()
+    assert_parity(res, "bf16", "autotuned")
+
+
 def test_step_and_debug_step_are_bitwise_identical():
     wl = custom_workload([(300, 500), (500, 300), (2048, 512)], seed=6)
     descs = [(m.rows, m.cols, m.param, m.grad) for m in wl.matrices]
