@@ -165,7 +165,8 @@ MUON_API muon_status muon_plan_opts_default(muon_plan_opts* o);
  * bound to the current HIP device and uploads its tables there (the only
  * host-to-device copy outside muon_step).  opts may be NULL (defaults).
  * Errors: INVALID_ARG (null, n < 1, rows or cols < 1 or >= 2^31, bad tile_hint,
- * opts out of range), UNSUPPORTED (dtypes), OUT_OF_MEMORY, DEVICE. */
+ * opts out of range), UNSUPPORTED (dtypes, a dimension that reaches 2^31 once padded to its
+ * tile, a tile_hint of 256 with fp32 operands), OUT_OF_MEMORY, DEVICE. */
 MUON_API muon_status muon_plan_create(const muon_matrix_desc* mats, int32_t n,
                              const muon_plan_opts* opts, muon_plan* out);
 

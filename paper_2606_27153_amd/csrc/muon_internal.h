@@ -69,8 +69,8 @@ struct MatDev {
 
 // One output tile of a grouped GEMM launch.
 struct TileEntry {
-  int32_t mat;   // index into the MatDev array (global, wave order)
-  uint16_t ti, tj;
+  int32_t mat;     // index into the MatDev array (global, wave order)
+  int32_t ti, tj;  // output tile row and column
 };
 
 // Per-matrix device pointers, refreshed when the caller's buffers change.

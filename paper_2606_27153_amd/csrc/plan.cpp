@@ -92,13 +92,13 @@ void emit_full(std::vector<TileEntry>& t, int32_t mat, int64_t tm, int64_t tn) {
         const int64_t w = std::min<int64_t>(32, tn - c0);
         if (w % 4 != 0 || t.size() % 8 != 0) {
           for (int64_t tj = c0; tj < c0 + w; ++tj)
-            for (int64_t ti = g0; ti < g0 + 8; ++ti) t.push_back(TileEntry{mat, uint16_t(ti), uint16_t(tj)});
+            for (int64_t ti = g0; ti < g0 + 8; ++ti) t.push_back(TileEntry{mat, int32_t(ti), int32_t(tj)});
           continue;
         }
         for (int64_t b = 0; b < 8 * w; ++b) {
           const int64_t x = b % 8, k = b / 8;
           const int64_t r = 4 * (x % 2) + k % 4, c = (x / 2) * (w / 4) + k / 4;
-          t.push_back(TileEntry{mat, uint16_t(g0 + r), uint16_t(c0 + c)});
+          t.push_back(TileEntry{mat, int32_t(g0 + r), int32_t(c0 + c)});
         }
       }
     }
@@ -107,7 +107,7 @@ void emit_full(std::vector<TileEntry>& t, int32_t mat, int64_t tm, int64_t tn) {
   for (; g0 < tm; g0 += kGroup) {
     const int64_t g1 = std::min(tm, g0 + kGroup);
     for (int64_t tj = 0; tj < tn; ++tj)
-      for (int64_t ti = g0; ti < g1; ++ti) t.push_back(TileEntry{mat, uint16_t(ti), uint16_t(tj)});
+      for (int64_t ti = g0; ti < g1; ++ti) t.push_back(TileEntry{mat, int32_t(ti), int32_t(tj)});
   }
 }
 
@@ -124,11 +124,11 @@ void lower_units(std::vector<std::vector<TileEntry>>& units, int32_t mat, int64_
       for (int64_t h0 = r0; h0 < r1; h0 += 4) {
         units.emplace_back();
         for (int64_t ti = h0; ti < std::min(r1, h0 + 4); ++ti)
-          for (int64_t tj = c0; tj < c0 + 8; ++tj) units.back().push_back(TileEntry{mat, uint16_t(ti), uint16_t(tj)});
+          for (int64_t tj = c0; tj < c0 + 8; ++tj) units.back().push_back(TileEntry{mat, int32_t(ti), int32_t(tj)});
       }
     units.emplace_back();
     for (int64_t ti = r0; ti < r1; ++ti)
-      for (int64_t tj = r0; tj <= ti; ++tj) units.back().push_back(TileEntry{mat, uint16_t(ti), uint16_t(tj)});
+      for (int64_t tj = r0; tj <= ti; ++tj) units.back().push_back(TileEntry{mat, int32_t(ti), int32_t(tj)});
   }
 }
 
@@ -222,8 +222,8 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
     p.n_gram += h.gram;
     h.m_pad = round_up(h.m, ci.tile);
     h.n_pad = round_up(h.n, ci.tile);
-    if (h.n_pad / ci.tile > 65535) {
-      err = "matrix " + std::to_string(i) + " has too many tiles along one dimension";
+    if (h.n_pad >= (int64_t(1) << 31)) {
+      err = "matrix " + std::to_string(i) + ": padded to the tile, its larger dimension reaches 2^31";
       return MUON_ERR_UNSUPPORTED;
     }
     h.rows_pad = h.transposed ? h.n_pad : h.m_pad;

@@ -244,6 +244,17 @@ def test_schedule_form_choice_and_launch_count(lib):
     assert lib.muon_plan_destroy(h) == L.MUON_OK
 
 
+def test_padded_dimension_limit(lib):
+    # rows and cols may be up to 2^31 - 1, but the padded extent must stay
+    # below 2^31; tile indices are 32-bit, so 2^22 columns (65536 tiles of 64)
+    # plan fine
+    st, h = _create(lib, [(1, (1 << 31) - 1, 1, 1, 0)])
+    assert st == L.MUON_ERR_UNSUPPORTED and "2^31" in L.last_error()
+    st, h = _create(lib, [(1, 1 << 22, 1, 1, 0), ((1 << 22) + 5, 3, 1, 1, 0)])
+    assert st == L.MUON_OK
+    assert lib.muon_plan_destroy(h) == L.MUON_OK
+
+
 def test_null_arguments(lib):
     h = ctypes.c_void_p()
     assert lib.muon_plan_create(None, 1, None, ctypes.byref(h)) == L.MUON_ERR_INVALID_ARG

@@ -102,6 +102,17 @@ def test_gram_space_step_counts(ns_steps):
         assert r.o_rel <= max(TOL_O["bf16"], 1.25 * q.o_rel), (r.index, r.o_rel, q.o_rel)
 
 
+@pytest.mark.parametrize("precision", ["bf16", "fp16"])
+def test_long_thin_matrices(precision):
+    # extreme aspect ratios: one row or a few columns over millions of
+    # elements (65536 tiles of one matrix in one launch, 64-row padding)
+    wl = custom_workload([(1, 1 << 22), ((1 << 22) + 5, 3), (7, (1 << 20) - 1), (70, 1 << 18)], seed=13)
+    _banner(f"long-thin {precision}")
+    res = run_parity(wl, precision=precision, steps=2)
+    _banner(f"long-thin {precision}: worst O {res.worst('o_rel'):.3e}")
+    assert_parity(res, precision, "long-thin")
+
+
 def test_ragged_shapes_small_waves():
     # every matrix in a wave of its own: same results as the single-wave plan
     wl = custom_workload(RAGGED, seed=12)

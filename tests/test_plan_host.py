@@ -47,6 +47,8 @@ def test_ragged_and_random_plans(plan_check):
     _run(plan_check, ragged, precision=2)
     _run(plan_check, ragged, aspect=1.0)
     _run(plan_check, ragged, aspect=0.0)
+    # more than 65535 tiles along one dimension
+    _run(plan_check, [(1, 1 << 22), ((1 << 22) + 5, 3), (70, 1 << 18)])
     for trial in range(5):
         shapes = [(int(rng.integers(1, 3000)), int(rng.integers(1, 3000))) for _ in range(40)]
         _run(plan_check, shapes, wave_bytes=int(rng.integers(1, 4)) << 28)
