@@ -119,12 +119,47 @@ def rocprof_summary(root: str) -> str:
                          f"{100 * ns / total:.1f}% |")
         lines.append("")
     counters = {}
+    shader = {}   # pass directory -> kernel -> counter -> [dispatches, sum, sum of durations]
     for path in sorted(glob.glob(os.path.join(root, "**", "*counter_collection.csv"), recursive=True)):
         for r in csv.DictReader(open(path)):
             k = kernel_key(r["Kernel_Name"])
-            c = counters.setdefault(r["Counter_Name"], {}).setdefault(k, [0, 0.0])
-            c[0] += 1
-            c[1] += float(r["Counter_Value"])
+            cname = r["Counter_Name"]
+            if cname in ("FETCH_SIZE", "WRITE_SIZE"):
+                c = counters.setdefault(cname, {}).setdefault(k, [0, 0.0])
+                c[0] += 1
+                c[1] += float(r["Counter_Value"])
+            else:
+                dur = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9
+                c = shader.setdefault(os.path.relpath(os.path.dirname(path), root), {}).setdefault(k, {}) \
+                    .setdefault(cname, [0, 0.0, 0.0])
+                c[0] += 1
+                c[1] += float(r["Counter_Value"])
+                c[2] += dur
+    if shader:
+        lines += ["### Shader counters per dispatch (rocprofv3 --pmc)", "",
+                  "Clock = GRBM_GUI_ACTIVE / 8 XCDs / dispatch duration; MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / "
+                  "(GRBM_GUI_ACTIVE / 8 x 1024 SIMDs); L2 hit = TCC_HIT / (TCC_HIT + TCC_MISS).", "",
+                  "| pass | kernel | dispatches | mean ms | clock GHz | MFMA busy | L2 hit | counters (mean) |",
+                  "|---|---|---|---|---|---|---|---|"]
+        for pas, per in sorted(shader.items()):
+            for k, cs in sorted(per.items()):
+                if k.startswith("other") or k.startswith("copy"):
+                    continue
+                mean = {c: v[1] / v[0] for c, v in cs.items()}
+                n, _, dsum = next(iter(cs.values()))
+                ms = dsum / n * 1e3
+                clk = busy = hit = ""
+                if "GRBM_GUI_ACTIVE" in mean and ms > 0:
+                    cyc = mean["GRBM_GUI_ACTIVE"] / 8
+                    clk = f"{cyc / (ms * 1e-3) / 1e9:.2f}"
+                    if "SQ_VALU_MFMA_BUSY_CYCLES" in mean:
+                        busy = f"{100 * mean['SQ_VALU_MFMA_BUSY_CYCLES'] / (cyc * 1024):.1f}%"
+                hs = [mean.get(c) for c in ("TCC_HIT_sum", "TCC_MISS_sum")]
+                if all(v is not None for v in hs) and sum(hs) > 0:
+                    hit = f"{100 * hs[0] / sum(hs):.1f}%"
+                rest = ", ".join(f"{c} {v:.4g}" for c, v in sorted(mean.items()))
+                lines.append(f"| {pas} | {k} | {n} | {ms:.3f} | {clk} | {busy} | {hit} | {rest} |")
+        lines.append("")
     if counters:
         copy = "copy (device copy)"
         lines += ["### HBM traffic per dispatch (rocprofv3 --pmc, KiB per dispatch)", ""]

@@ -554,12 +554,26 @@ __device__ __forceinline__ i16x4 lds_tr16(const char* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p));
 }
 
-// Segment swizzle for row-major LDS rows of ROWB bytes.
+// Segment swizzle for row-major LDS rows of ROWB bytes: 32-byte segment s of
+// row r is stored at s ^ seg_swz(r).  A transposing read of one MFMA
+// fragment touches 4 consecutive rows (r & 3 = q) and two adjacent segments
+// (an even one and the next).  With rows of 256 or 512 bytes every row starts
+// on the same bank, so the stored segment alone picks the banks: the XOR
+// value 2q + (q >> 1) (0, 2, 5, 7) sends the 8 (row, segment) pairs to 8
+// different 32-byte bank groups of a 256-byte window, and the 4 rows of one
+// segment to 4 different groups of a 128-byte window, so the read is
+// conflict-free whether the LDS serves 16 or 32 lanes of a ds_read_b64 per
+// cycle.  (The plain r & 7 sent both segments of a pair to the same groups:
+// a 2-way conflict on every read, SQ_LDS_BANK_CONFLICT at 1 cycle per LDS
+// instruction.)  128-byte rows keep (r / 2) & 3.
 template <int ROWB>
 __device__ __forceinline__ int seg_swz(int row) {
-  constexpr int RPW = ROWB >= 256 ? 1 : 256 / ROWB;        // rows per 256-byte bank window
-  constexpr int SEGW = ROWB / 32 < 8 ? ROWB / 32 : 8;      // swizzle span in segments
-  return (row / RPW) & (SEGW - 1);
+  if constexpr (ROWB >= 256) {
+    const int q = row & 3;
+    return 2 * q + (q >> 1);
+  } else {
+    return (row / 2) & 3;
+  }
 }
 
 // Per-lane source of the direct-to-LDS loads of a row-major X slab: the
