@@ -391,7 +391,7 @@ def main(argv=None) -> int:
     ap.add_argument("--config", default="8b", choices=["tiny", "1b", "8b", "vla", "moe"])
     ap.add_argument("--precision", default="bf16", choices=["bf16", "fp16", "fp32"])
     ap.add_argument("--wave-bytes", type=int, default=0)
-    ap.add_argument("--gram-min-aspect", type=float, default=2.0,
+    ap.add_argument("--gram-min-aspect", type=float, default=None,
                     help="Gram-space recurrence (Eq. 4) for matrices with n >= this * m; 0 = Eq. 2 only")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle time to sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -413,6 +413,9 @@ def main(argv=None) -> int:
     ap.add_argument("--tune-cache", default=None, help="tile cache file for --autotune")
     args = ap.parse_args(argv)
 
+    if args.gram_min_aspect is None:
+        from paper_2606_27153_amd.optim import default_gram_min_aspect
+        args.gram_min_aspect = default_gram_min_aspect(args.precision)
     if args.rocprof_summary:
         print(rocprof_summary(args.rocprof_summary))
         if args.write_traffic:
