@@ -411,6 +411,8 @@ def main(argv=None) -> int:
     ap.add_argument("--autotune", action="store_true",
                     help="measure each shape's GEMM tile first (cached on disk, see --tune-cache) and plan with it")
     ap.add_argument("--tune-cache", default=None, help="tile cache file for --autotune")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time replays of one step captured in a HIP graph (graph_ms_per_step)")
     args = ap.parse_args(argv)
 
     if args.gram_min_aspect is None:
@@ -547,6 +549,23 @@ def main(argv=None) -> int:
         if traffic is not None:
             roof["traffic_vs_algorithmic"] = round(traffic / roof["algorithmic_bytes"], 2)
 
+    graph_ms = None
+    if args.graph:
+        # the eager steps above uploaded the pointer table for these buffers,
+        # so a step now only enqueues kernels and can be captured
+        kw_g = {k: v for k, v in kw.items() if k != "stream"}
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            plan.step(params, grads, moms, **kw_g)
+        graph.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            graph.replay()
+        torch.cuda.synchronize()
+        graph_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+        log(f"[bench] {args.steps} graph replays: {graph_ms:.3f} ms/step")
+        del graph
     floor_ms = (gemm_flops / (peak_mm * 1e12) + ew_bytes / (PEAK_HBM_GBS * 1e9)) * 1e3
     cpu = None
     if not args.no_cpu_baseline:
@@ -575,6 +594,7 @@ def main(argv=None) -> int:
         "mfma_util_pct_ns_gemms": round(mfma_util, 2),
         "ns_gemm_tflops": round(ns_tflops, 2),
         "ns_gemm_ms_per_step": round(gemm_ms, 3),
+        "graph_ms_per_step": None if graph_ms is None else round(graph_ms, 3),
         "step_ms_median": round(percentile(per_step, 0.5), 3),
         "step_ms_p10": round(percentile(per_step, 0.1), 3),
         "step_ms_p90": round(percentile(per_step, 0.9), 3),

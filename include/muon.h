@@ -198,7 +198,10 @@ MUON_API muon_status muon_plan_matrix_info(muon_plan plan, int32_t index, muon_m
  * The plan caches the device copy of the pointer arrays: when they differ
  * from the previous call, the new table is copied on the stream and the
  * stream is synchronised once before the step is enqueued.  Otherwise the
- * call only enqueues kernels and never synchronises or allocates.
+ * call only enqueues kernels and never synchronises or allocates, so such a
+ * call (with launch timing off) can be captured in a HIP graph and replayed;
+ * each replay is bitwise the step an eager call would make.  Capture a call
+ * whose pointers differ from the previous call's and the capture fails.
  * The plan must be used from the device it was created on. */
 MUON_API muon_status muon_step(muon_plan plan, void* const* params, const void* const* grads,
                       void* const* momentum, float lr, float momentum_coef,

@@ -121,3 +121,40 @@ def test_launch_timing_reports_every_kind(aspect):
             assert s["launches"] == per_class[s["kind"]], s
     assert plan.timing_read() == []     # records were dropped by the first read
     plan.close()
+
+
+def test_step_captured_in_a_graph_matches_eager():
+    # After one eager step with the same buffers (which uploads the plan's
+    # pointer table), muon_step only enqueues kernels on the stream, so it
+    # can be captured in a HIP graph.  Each replay, with new gradients copied
+    # in eagerly between replays, must match an eager step bit for bit.
+    wl = custom_workload([(256, 768), (768, 256), (300, 300), (64, 200), (512, 2048)], seed=41)
+    descs = [(m.rows, m.cols, m.param, m.grad) for m in wl.matrices]
+    dev = "cuda:0"
+    pe, me = make_state(torch, wl, dev)
+    pg, mg = make_state(torch, wl, dev)
+    eager, graphed = MuonPlan(descs), MuonPlan(descs)
+    we, wg = eager.workspace(dev), graphed.workspace(dev)
+    ge = make_grads(torch, wl, 0, dev)
+    gg = [g.clone() for g in ge]
+    kw = dict(lr=0.02, momentum=0.95, weight_decay=0.01, ns_steps=5)
+    eager.step(pe, ge, me, workspace=we, **kw)
+    graphed.step(pg, gg, mg, workspace=wg, **kw)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        graphed.step(pg, gg, mg, workspace=wg, **kw)
+    for step in range(1, 5):
+        new = make_grads(torch, wl, step, dev)
+        for a, b, g in zip(ge, gg, new):
+            a.copy_(g)
+            b.copy_(g)
+        eager.step(pe, ge, me, workspace=we, **kw)
+        graph.replay()
+        torch.cuda.synchronize()
+        for x, y in zip(pe, pg):
+            assert torch.equal(x, y), f"replay {step}: params differ"
+        for x, y in zip(me, mg):
+            assert torch.equal(x, y), f"replay {step}: momentum differs"
+    eager.close()
+    graphed.close()
