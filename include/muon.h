@@ -200,8 +200,10 @@ MUON_API muon_status muon_plan_matrix_info(muon_plan plan, int32_t index, muon_m
  * stream is synchronised once before the step is enqueued.  Otherwise the
  * call only enqueues kernels and never synchronises or allocates, so such a
  * call (with launch timing off) can be captured in a HIP graph and replayed;
- * each replay is bitwise the step an eager call would make.  Capture a call
- * whose pointers differ from the previous call's and the capture fails.
+ * each replay is bitwise the step an eager call would make.  The scalars
+ * (lr, momentum_coef, weight_decay, ns_steps, nesterov) are captured by
+ * value: a new value needs a new capture.  Capture a call whose pointers
+ * differ from the previous call's and the capture fails.
  * The plan must be used from the device it was created on. */
 MUON_API muon_status muon_step(muon_plan plan, void* const* params, const void* const* grads,
                       void* const* momentum, float lr, float momentum_coef,
