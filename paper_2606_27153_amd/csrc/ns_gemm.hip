@@ -763,8 +763,11 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
   // the one just read, and the first fragments of the next slab are read
   // right after it while the last MFMAs of the slab still drain.  (No early
   // exit inside the trip: a second loop exit would make the compiler copy the
-  // accumulators between register files.)
-  const int nk = int(K / C::BK);
+  // accumulators between register files.)  K (the padded extent) is the
+  // operands' leading dimension; the loop stops at the last slab that holds a
+  // real row or column, since the padding is zero and adds nothing.
+  const int64_t kreal = STAGE == ST_GRAM ? int64_t(d.rows > d.cols ? d.rows : d.cols) : int64_t(d.m);
+  const int nk = int((kreal + C::BK - 1) / C::BK);
   // a*X (B*X) and b*A (A*A, as b/c * A, the product is scaled by c at the
   // end) are folded in while the slab holding them is in LDS.
   const bool FUSE = (STAGE == ST_POLY || STAGE == ST_BX) && args.fcoef != 0.f;
