@@ -269,6 +269,40 @@ def ns_cost(rows: int, cols: int, k: int = 5, gram_min_aspect: float = 2.0) -> f
     return k * (3.0 * m * m * n + float(m) ** 3)
 
 
+def eq2_work_flops(rows: int, cols: int, k: int = 5) -> float:
+    """The NS work of one matrix as the method states it (Eq. 2, symmetry-aware:
+    per step m^2 n for X X^T, m^3 for A A and 2 m^2 n for B X), whichever form
+    the plan runs; a zero-gradient matrix has none."""
+    m, n = min(rows, cols), max(rows, cols)
+    return k * (3.0 * m * m * n + float(m) ** 3)
+
+
+def live_flop_share(plan, k: int, zero) -> dict:
+    """(kind, kernel class) -> the share of that launch group's algorithmic
+    flops that belongs to matrices with a nonzero gradient.  The library
+    counts every matrix of a launch; the tiles of a zero-gradient matrix exit
+    before their K loop, so only this share is executed.  Per matrix and step:
+    Eq. 2 runs Gram (m^2 n), A*A (m^3) and B*X (2 m^2 n) k times; the Gram-space
+    form runs Gram and B*X once, P_i k times and 3k - 3 symmetric m^3 products."""
+    from paper_2606_27153_amd import _lib as L
+    tot: dict = {}
+    live: dict = {}
+    for i in range(plan.n):
+        mi = plan.matrix_info(i)
+        cls = L.KERNEL_CLASSES[mi["kernel_class"]]
+        m, n = float(mi["m"]), float(mi["n"])
+        if mi["gram_space"]:
+            per = {"gram": m * m * n, "poly": k * m ** 3, "symm": (3 * k - 3 if k >= 2 else 0) * m ** 3,
+                   "bx": 2 * m * m * n}
+        else:
+            per = {"gram": k * m * m * n, "poly": k * m ** 3, "symm": 0.0, "bx": k * 2 * m * m * n}
+        for kind, f in per.items():
+            tot[(kind, cls)] = tot.get((kind, cls), 0.0) + f
+            if not zero[i]:
+                live[(kind, cls)] = live.get((kind, cls), 0.0) + f
+    return {key: (live.get(key, 0.0) / v if v > 0 else 1.0) for key, v in tot.items()}
+
+
 def lpt_partition(costs, n_owners: int):
     """Longest-processing-time assignment: matrices in decreasing cost, each
     to the owner with the least load so far (ties to the lowest rank).
@@ -502,6 +536,12 @@ def main(argv=None) -> int:
     plan.set_timing(False)
     stats = plan.timing_read(reset=True)
     log(f"[bench] {args.steps} timed steps: {ms_per_step:.3f} ms/step")
+    zero = [m.zero_grad for m in wl.matrices]
+    if any(zero):
+        flop_share = live_flop_share(plan, wl.ns_steps, zero)
+        for s in stats:
+            if s["kind"] in GEMM_KINDS:
+                s["algo_flops"] *= flop_share.get((s["kind"], s["kernel_class"]), 1.0)
 
     # fp16 MFMA has the bf16 dense peak
     peak_mm = PEAK_F32_TFLOPS if args.precision == "fp32" else PEAK_BF16_TFLOPS
@@ -524,6 +564,8 @@ def main(argv=None) -> int:
     ew_bytes = sum(s["algo_bytes"] for s in ew) / args.steps
     ns_tflops = gemm_flops / (gemm_ms * 1e-3) / 1e12 if gemm_ms > 0 else 0.0
     mfma_util = 100.0 * ns_tflops / peak_mm
+    eq2_flops = sum(eq2_work_flops(m.rows, m.cols, wl.ns_steps) for m in wl.matrices if not m.zero_grad)
+    eq2_tflops = eq2_flops / (gemm_ms * 1e-3) / 1e12 if gemm_ms > 0 else 0.0
 
     dom = max(stats, key=lambda s: s["total_ms"])
     dom_key = f"{dom['kind']}:{dom['kernel_class']}"
@@ -594,6 +636,8 @@ def main(argv=None) -> int:
         "mfma_util_pct_ns_gemms": round(mfma_util, 2),
         "ns_gemm_tflops": round(ns_tflops, 2),
         "ns_gemm_ms_per_step": round(gemm_ms, 3),
+        "ns_eq2_work_tflops": round(eq2_tflops, 2),
+        "ns_eq2_work_pct_of_peak": round(100.0 * eq2_tflops / peak_mm, 2),
         "graph_ms_per_step": None if graph_ms is None else round(graph_ms, 3),
         "step_ms_median": round(percentile(per_step, 0.5), 3),
         "step_ms_p10": round(percentile(per_step, 0.1), 3),

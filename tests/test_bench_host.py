@@ -112,3 +112,47 @@ def test_percentile_and_share_of_the_8b_set():
     # 224 matrices in three shapes split into 8 nearly equal shares
     assert max(loads) / (sum(loads) / 8) < 1.02
     assert sum(len(o) for o in owners) == 224
+
+
+def test_eq2_work_of_the_8b_and_moe_sets():
+    # Eq. 2 work, symmetry-aware: 5 (3 m^2 n + m^3) per matrix; 4.72e14 for
+    # the 8B set, and 2.67e14 for the MoE set once its zero-gradient experts
+    # are left out (they have no NS work at all)
+    wl = get_workload("8b")
+    ffn = 5 * (3 * 4096 ** 2 * 14336 + 4096 ** 3)
+    sq = 5 * 4 * 4096 ** 3
+    kv = 5 * (3 * 1024 ** 2 * 4096 + 1024 ** 3)
+    got = sum(bench.eq2_work_flops(m.rows, m.cols) for m in wl.matrices)
+    assert got == pytest.approx(96 * ffn + 64 * sq + 64 * kv, rel=1e-12)
+    assert got == pytest.approx(4.72e14, rel=2e-3)
+    moe = get_workload("moe")
+    live = sum(bench.eq2_work_flops(m.rows, m.cols) for m in moe.matrices if not m.zero_grad)
+    assert sum(m.zero_grad for m in moe.matrices) == 1152
+    assert live == pytest.approx(2.67e14, rel=3e-3)
+
+
+def test_live_flop_share():
+    # four equal matrices, one with a zero gradient: three quarters of every
+    # launch group's flops are executed
+    descs = [(1024, 4096, "bf16", "bf16")] * 4
+    plan = MuonPlan(descs, host_only=True)
+    share = bench.live_flop_share(plan, 5, [True, False, False, False])
+    assert sorted(k[0] for k in share) == ["bx", "gram", "poly", "symm"]
+    assert all(v == pytest.approx(0.75) for v in share.values())
+    assert bench.live_flop_share(plan, 5, [False] * 4) == {k: 1.0 for k in share}
+    assert bench.live_flop_share(plan, 5, [True] * 4) == {k: 0.0 for k in share}
+    plan.close()
+    # Gram-space (n >= 2m) and Eq. 2 matrices in one class: gram work is m^2 n
+    # once for the former, k m^2 n for the latter
+    descs = [(1024, 4096, "bf16", "bf16"), (1024, 1024, "bf16", "bf16")]
+    plan = MuonPlan(descs, host_only=True)
+    infos = [plan.matrix_info(i) for i in range(2)]
+    assert [i["gram_space"] for i in infos] == [1, 0] and infos[0]["kernel_class"] == infos[1]["kernel_class"]
+    from paper_2606_27153_amd import _lib as L
+    cls = L.KERNEL_CLASSES[infos[0]["kernel_class"]]
+    share = bench.live_flop_share(plan, 5, [False, True])
+    g_rect, g_sq = 1024 ** 2 * 4096, 5 * 1024 ** 3
+    assert share[("gram", cls)] == pytest.approx(g_rect / (g_rect + g_sq))
+    assert share[("symm", cls)] == pytest.approx(1.0)   # only the Gram-space matrix has symmetric products
+    assert share[("bx", cls)] == pytest.approx(2 * 1024 ** 2 * 4096 / (2 * 1024 ** 2 * 4096 + 5 * 2 * 1024 ** 3))
+    plan.close()
