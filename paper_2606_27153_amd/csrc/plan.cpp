@@ -40,9 +40,13 @@ constexpr int64_t kAlign = 256;
 
 int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 
-double padded_cost(int64_t m, int64_t n, int32_t tile) {
+// Flops of one Eq. 2 step as the kernels issue them: output tiles cover the
+// padded extent, while each K loop stops at the last slab of bk elements that
+// holds real data (Gram: K = n; A*A and B*X: K = m).
+double padded_cost(int64_t m, int64_t n, int32_t tile, int64_t bk) {
   const double mp = double(round_up(m, tile)), np = double(round_up(n, tile));
-  return 3.0 * mp * mp * np + mp * mp * mp;
+  const double km = double(round_up(m, bk)), kn = double(round_up(n, bk));
+  return mp * mp * kn + mp * mp * km + 2.0 * mp * np * km;
 }
 
 // Kernel class of an m x n matrix: the operand type follows the precision
@@ -62,7 +66,7 @@ int32_t choose_class(int64_t m, int64_t n, const muon_plan_opts& o, int32_t tile
   int32_t best = hi;
   double best_cost = 0;
   for (int32_t kc = lo; kc <= hi; ++kc) {
-    const double cost = padded_cost(m, n, kClasses[kc].tile) / kClassEfficiency[kc];
+    const double cost = padded_cost(m, n, kClasses[kc].tile, kClasses[kc].fp32 ? 32 : 64) / kClassEfficiency[kc];
     if (kc == lo || cost < best_cost) {
       best = kc;
       best_cost = cost;
@@ -398,8 +402,10 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
         const double t2 = double(tile) * double(tile);
         const int64_t tm = h.m_pad / tile;
         const double nl = double(tm * (tm + 1) / 2);
-        p.padded_flops += nl * 2.0 * t2 * double(h.n_pad) + nl * 2.0 * t2 * double(h.m_pad) +
-                          double(tm * (h.n_pad / tile)) * 2.0 * t2 * double(h.m_pad);
+        // the K loops stop at the last 128-byte slab holding real data
+        const int64_t bk = kClasses[kc].fp32 ? 32 : 64;
+        const double kn = double(round_up(h.n, bk)), km = double(round_up(h.m, bk));
+        p.padded_flops += nl * 2.0 * t2 * kn + nl * 2.0 * t2 * km + double(tm * (h.n_pad / tile)) * 2.0 * t2 * km;
       }
       if (full.empty()) continue;
       interleave_units(lower, units);

@@ -281,3 +281,16 @@ def test_step_on_host_only_plan_is_rejected_before_any_device_call(lib):
     cnt = ctypes.c_int32()
     assert lib.muon_plan_timing_read(h, None, 0, ctypes.byref(cnt), 1) == L.MUON_OK and cnt.value == 0
     assert lib.muon_plan_destroy(h) == L.MUON_OK
+
+
+def test_tile_choice_prices_the_k_loop_at_the_real_extent():
+    # Cost of one Eq. 2 step as issued: m_pad^2 kn + m_pad^2 km + 2 m_pad n_pad km,
+    # with km, kn = m, n rounded to the 64-element K slab, over the class
+    # efficiency (256: 1.0, 128: 0.8).
+    # 1152 x 1152: 256 tile 4 * 1280^2 * 1152 = 7.55e9; 128 tile 4 * 1152^3 / 0.8 = 7.64e9
+    # 640 x 640:   256 tile 4 * 768^2 * 640 = 1.51e9;   128 tile 4 * 640^3 / 0.8 = 1.31e9
+    # (pricing K at the padded extent, as the loops once ran, chose 128 for 1152)
+    plan = MuonPlan([(1152, 1152, "bf16", "bf16"), (3456, 1152, "bf16", "bf16"), (640, 640, "bf16", "bf16"),
+                     (4096, 4096, "bf16", "bf16")], host_only=True)
+    assert [plan.matrix_info(i)["tile"] for i in range(4)] == [256, 256, 128, 256]
+    plan.close()
