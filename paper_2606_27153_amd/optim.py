@@ -32,6 +32,50 @@ def default_gram_min_aspect(precision: str) -> float:
     return 1.4 if precision == "fp16" else 2.0
 
 
+def check_step_tensors(descs: Sequence, params: List, grads: List, moms: List, workspace=None,
+                       update_out: Optional[List] = None) -> None:
+    """Raises ValueError unless every buffer matches what the C ABI assumes of
+    it: matrix i's param, grad and momentum are contiguous (row-major,
+    leading dimension cols) tensors of descs[i]'s shape and dtypes (momentum
+    fp32), all on one GPU, like the workspace and any update_out buffer (fp32).
+    The library itself only sees pointers and cannot tell."""
+    n = len(descs)
+    if not (len(params) == len(grads) == len(moms) == n):
+        raise ValueError(f"expected {n} params, grads and momentum buffers")
+    if update_out is not None and len(update_out) != n:
+        raise ValueError(f"expected {n} update_out entries (None for no output)")
+    checked = []
+    for i, d in enumerate(descs):
+        rows, cols, pd, gd = d[:4]
+        shape = (int(rows), int(cols))
+        pc = _DT[pd] if isinstance(pd, str) else int(pd)
+        gc = _DT[gd] if isinstance(gd, str) else int(gd)
+        todo = [(params[i], "param", pc), (grads[i], "grad", gc), (moms[i], "momentum", L.MUON_F32)]
+        if update_out is not None and update_out[i] is not None:
+            todo.append((update_out[i], "update_out", L.MUON_F32))
+        for t, name, code in todo:
+            what = f"matrix {i} {name}"
+            if tuple(t.shape) != shape:
+                raise ValueError(f"{what} has shape {tuple(t.shape)}, the plan expects {shape}")
+            if _dtype_code(t) != code:
+                raise ValueError(f"{what} has dtype {t.dtype}, the plan expects "
+                                 f"{'float32' if code == L.MUON_F32 else 'bfloat16'}")
+            if not t.is_contiguous():
+                raise ValueError(f"{what} is not contiguous (the library reads row-major rows of cols elements)")
+            checked.append((t, what))
+    device = None
+    for t, what in checked:
+        if not t.is_cuda:
+            raise ValueError(f"{what} is not on a GPU")
+        if device is None:
+            device = t.device
+        elif t.device != device:
+            raise ValueError(f"{what} is on {t.device}, other buffers on {device}")
+    if workspace is not None:
+        if not workspace.is_contiguous() or not workspace.is_cuda or workspace.device != device:
+            raise ValueError(f"the workspace must be a contiguous tensor on {device}")
+
+
 def _dtype_code(t) -> int:
     import torch
     if t.dtype == torch.float32:
@@ -111,6 +155,7 @@ class MuonPlan:
         self.descs = list(descs)
         self.precision = precision
         self._workspace = None
+        self._checked = None
 
     # ------------------------------------------------------------ inspection
     @property
@@ -166,7 +211,12 @@ class MuonPlan:
     def step(self, params: List, grads: List, moms: List, *, lr: float, momentum: float,
              weight_decay: float, ns_steps: int = 5, nesterov: bool = True, workspace=None,
              stream=None, update_out: Optional[List] = None) -> None:
-        """Enqueues one Muon step on ``stream`` (default: torch's current stream)."""
+        """Enqueues one Muon step on ``stream`` (default: torch's current stream).
+
+        The buffers are checked against the plan (``check_step_tensors``:
+        shape, dtype, row-major layout, one GPU) whenever their addresses
+        differ from the previous call's; a failed check raises ValueError and
+        nothing is launched."""
         import torch
         n = self.n
         if not (len(params) == len(grads) == len(moms) == n):
@@ -176,9 +226,17 @@ class MuonPlan:
         if stream is None:
             stream = torch.cuda.current_stream(params[0].device)
         sp = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
-        pp = L.ptr_array([t.data_ptr() for t in params])
-        gp = L.ptr_array([t.data_ptr() for t in grads])
-        mp = L.ptr_array([t.data_ptr() for t in moms])
+        ptrs = ([t.data_ptr() for t in params], [t.data_ptr() for t in grads], [t.data_ptr() for t in moms],
+                None if update_out is None else [0 if t is None else t.data_ptr() for t in update_out],
+                workspace.data_ptr())
+        # The buffers are checked whenever their addresses change (the
+        # library then refreshes its pointer table too), not on every step.
+        if ptrs != self._checked:
+            check_step_tensors(self.descs, params, grads, moms, workspace, update_out)
+            self._checked = ptrs
+        pp = L.ptr_array(ptrs[0])
+        gp = L.ptr_array(ptrs[1])
+        mp = L.ptr_array(ptrs[2])
         args = (self._h, pp, gp, mp, float(lr), float(momentum), float(weight_decay),
                 int(ns_steps), 1 if nesterov else 0, ctypes.c_void_p(workspace.data_ptr()),
                 workspace.numel() * workspace.element_size(), ctypes.c_void_p(sp))
@@ -186,7 +244,7 @@ class MuonPlan:
         if update_out is None:
             L.check(lib.muon_step(*args))
         else:
-            op = L.ptr_array([0 if t is None else t.data_ptr() for t in update_out])
+            op = L.ptr_array(ptrs[3])
             L.check(lib.muon_step_debug(*args, op))
 
     def close(self) -> None:

@@ -294,3 +294,39 @@ def test_tile_choice_prices_the_k_loop_at_the_real_extent():
                      (4096, 4096, "bf16", "bf16")], host_only=True)
     assert [plan.matrix_info(i)["tile"] for i in range(4)] == [256, 256, 128, 256]
     plan.close()
+
+
+def test_step_buffers_are_checked_against_the_plan():
+    # the C ABI sees bare pointers, so the binding checks each buffer's shape,
+    # dtype, layout and device before they are handed over
+    import torch
+    from paper_2606_27153_amd.optim import check_step_tensors
+    descs = [(4, 8, "bf16", "f32"), (16, 2, "f32", "bf16")]
+
+    def bufs():
+        return ([torch.zeros(4, 8, dtype=torch.bfloat16), torch.zeros(16, 2)],
+                [torch.zeros(4, 8), torch.zeros(16, 2, dtype=torch.bfloat16)],
+                [torch.zeros(4, 8), torch.zeros(16, 2)])
+
+    p, g, m = bufs()
+    with pytest.raises(ValueError, match="not on a GPU"):
+        check_step_tensors(descs, p, g, m)
+    p, g, m = bufs()
+    p[1] = torch.zeros(2, 16)
+    with pytest.raises(ValueError, match=r"matrix 1 param has shape \(2, 16\)"):
+        check_step_tensors(descs, p, g, m)
+    p, g, m = bufs()
+    g[0] = torch.zeros(4, 8, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="matrix 0 grad has dtype torch.bfloat16, the plan expects float32"):
+        check_step_tensors(descs, p, g, m)
+    p, g, m = bufs()
+    m[1] = torch.zeros(2, 16).t()   # right shape, column-major
+    with pytest.raises(ValueError, match="matrix 1 momentum is not contiguous"):
+        check_step_tensors(descs, p, g, m)
+    p, g, m = bufs()
+    with pytest.raises(ValueError, match="matrix 0 update_out has dtype"):
+        check_step_tensors(descs, p, g, m, update_out=[torch.zeros(4, 8, dtype=torch.bfloat16), None])
+    with pytest.raises(ValueError, match="expected 2 params"):
+        check_step_tensors(descs, p[:1], g, m)
+    with pytest.raises(TypeError, match="unsupported dtype"):
+        check_step_tensors(descs, [torch.zeros(4, 8, dtype=torch.float16), p[1]], g, m)

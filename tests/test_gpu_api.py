@@ -1,6 +1,7 @@
 """GPU checks of the Python front end and the ABI extras: the torch.optim
-wrapper, checkpoint/resume equivalence, launch timing, and the pointer-table
-refresh when buffers move."""
+wrapper, checkpoint/resume equivalence, launch timing, the pointer-table
+refresh when buffers move, and the binding's refusal of buffers that do not
+match the plan."""
 import pytest
 import torch
 
@@ -158,3 +159,36 @@ def test_step_captured_in_a_graph_matches_eager():
             assert torch.equal(x, y), f"replay {step}: momentum differs"
     eager.close()
     graphed.close()
+
+
+@pytest.mark.gpu
+def test_bad_buffers_are_refused_before_launch(monkeypatch):
+    import paper_2606_27153_amd.optim as O
+    dev = "cuda:0"
+    descs = [(96, 160, "bf16", "bf16"), (200, 64, "f32", "f32")]
+    plan = MuonPlan(descs)
+    params = [torch.randn(96, 160, device=dev).to(torch.bfloat16), torch.randn(200, 64, device=dev)]
+    grads = [torch.randn(96, 160, device=dev).to(torch.bfloat16), torch.randn(200, 64, device=dev)]
+    moms = [torch.zeros(96, 160, device=dev), torch.zeros(200, 64, device=dev)]
+    kw = dict(lr=0.02, momentum=0.95, weight_decay=0.01)
+    before = [p.clone() for p in params]
+    bad = [params[0], torch.randn(64, 200, device=dev).t()]          # right shape, column-major
+    with pytest.raises(ValueError, match="matrix 1 param is not contiguous"):
+        plan.step(bad, grads, moms, **kw)
+    with pytest.raises(ValueError, match="matrix 0 grad is not on a GPU"):
+        plan.step(params, [grads[0].cpu(), grads[1]], moms, **kw)
+    with pytest.raises(ValueError, match="matrix 1 momentum has dtype"):
+        plan.step(params, grads, [moms[0], moms[1].to(torch.bfloat16)], **kw)
+    torch.cuda.synchronize()
+    assert all(torch.equal(a, b) for a, b in zip(params, before)), "a refused step changed a parameter"
+    calls = []
+    real = O.check_step_tensors
+    monkeypatch.setattr(O, "check_step_tensors", lambda *a, **k: (calls.append(1), real(*a, **k)))
+    plan.step(params, grads, moms, **kw)
+    plan.step(params, grads, moms, **kw)            # same buffers: not checked again
+    g2 = [g.clone() for g in grads]
+    plan.step(params, g2, moms, **kw)               # new addresses: checked
+    torch.cuda.synchronize()
+    assert len(calls) == 2
+    assert not any(torch.equal(a, b) for a, b in zip(params, before))
+    plan.close()
