@@ -204,11 +204,33 @@ MUON_API muon_status muon_plan_matrix_info(muon_plan plan, int32_t index, muon_m
  * (lr, momentum_coef, weight_decay, ns_steps, nesterov) are captured by
  * value: a new value needs a new capture.  Capture a call whose pointers
  * differ from the previous call's and the capture fails.
- * The plan must be used from the device it was created on. */
+ * The plan must be used from the device it was created on.  Whenever the
+ * buffer addresses change, muon_step also checks where the buffers live
+ * (muon_check_buffers) before the pointer table is refreshed; a buffer that
+ * is not device memory of the plan's device, or that ends before
+ * rows*cols elements, gives INVALID_ARG and nothing is enqueued. */
 MUON_API muon_status muon_step(muon_plan plan, void* const* params, const void* const* grads,
                       void* const* momentum, float lr, float momentum_coef,
                       float weight_decay, int32_t ns_steps, int32_t nesterov,
                       void* workspace, size_t workspace_bytes, void* hip_stream);
+
+/* The buffer checks of muon_step, without enqueuing anything.  Beyond the
+ * argument rules above (non-NULL, 16-byte aligned buffers, a 256-byte
+ * aligned workspace of at least muon_plan_workspace_bytes, the current
+ * device the plan's), every buffer must be device memory of the plan's
+ * device (or managed memory), and each of [params[i], + rows*cols*param
+ * size), [grads[i], ...), [momentum[i], + rows*cols*4), [update_out[i], ...)
+ * and the plan's workspace bytes must lie inside one allocation (where HIP
+ * reports the allocation; memory mapped through the virtual memory API may
+ * not be, and is then taken on trust).  muon_step
+ * makes these memory checks itself whenever its buffer addresses differ from
+ * the previous call's (so a step on the same buffers makes no extra HIP
+ * call); this entry point is for callers who want to vet buffers up front.
+ * update_out may be NULL.  Returns MUON_OK, INVALID_ARG or
+ * WORKSPACE_TOO_SMALL with the reason in muon_last_error(). */
+MUON_API muon_status muon_check_buffers(muon_plan plan, void* const* params, const void* const* grads,
+                                        void* const* momentum, void* workspace, size_t workspace_bytes,
+                                        float* const* update_out);
 
 /* muon_step plus, for every i with update_out[i] != NULL, the orthogonalised
  * update O_i (before lr and the shape scale) written as fp32 rows x cols

@@ -92,6 +92,7 @@ SIGNATURES = {
     "muon_plan_matrix_info": (ctypes.c_int, [_VP, ctypes.c_int32, ctypes.POINTER(muon_matrix_info)]),
     "muon_step": (ctypes.c_int, _STEP_ARGS),
     "muon_step_debug": (ctypes.c_int, _STEP_ARGS + [_PP]),
+    "muon_check_buffers": (ctypes.c_int, [_VP, _PP, _PP, _PP, _VP, ctypes.c_size_t, _PP]),
     "muon_plan_set_timing": (ctypes.c_int, [_VP, ctypes.c_int32]),
     "muon_plan_timing_read": (ctypes.c_int, [_VP, ctypes.POINTER(muon_kernel_stat), ctypes.c_int32,
                                              ctypes.POINTER(ctypes.c_int32), ctypes.c_int32]),

@@ -93,20 +93,47 @@ muon_status upload_tables(muon::Plan& p) {
 
 bool aligned(const void* ptr, uintptr_t a) { return (reinterpret_cast<uintptr_t>(ptr) & (a - 1)) == 0; }
 
-muon_status step_impl(muon_plan plan, void* const* params, const void* const* grads, void* const* momentum,
-                      float lr, float mu, float wd, int32_t ns_steps, int32_t nesterov, void* workspace,
-                      size_t workspace_bytes, void* stream, float* const* update_out) {
-  using namespace muon;
-  if (!plan) return fail(MUON_ERR_INVALID_ARG, "plan is NULL");
-  Plan& p = plan->p;
-  if (!p.d_block) return fail(MUON_ERR_INVALID_ARG, "plan was created host-only and cannot be stepped");
+// [ptr, ptr + bytes) must be device memory of the plan's device (or managed
+// memory) inside one allocation -- the latter where HIP can name the
+// allocation (memory mapped through the virtual memory API may not be
+// reported; it is then taken on trust).  A failed HIP query leaves its error
+// behind, so it is cleared before returning.
+muon_status check_memory(const void* ptr, size_t bytes, int device, const std::string& what) {
+  hipPointerAttribute_t a;
+  std::memset(&a, 0, sizeof(a));
+  hipError_t e = hipPointerGetAttributes(&a, ptr);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(MUON_ERR_INVALID_ARG, what + " is not memory the HIP runtime knows (a host pointer?)");
+  }
+  if (a.type != hipMemoryTypeDevice && a.type != hipMemoryTypeManaged)
+    return fail(MUON_ERR_INVALID_ARG, what + " is not device memory");
+  if (a.type == hipMemoryTypeDevice && a.device != device)
+    return fail(MUON_ERR_INVALID_ARG,
+                what + " is on device " + std::to_string(a.device) + ", the plan on device " + std::to_string(device));
+  hipDeviceptr_t base = nullptr;
+  size_t size = 0;
+  e = hipMemGetAddressRange(&base, &size, hipDeviceptr_t(const_cast<void*>(ptr)));
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return MUON_OK;
+  }
+  const uintptr_t end = uintptr_t(ptr) + bytes, aend = uintptr_t(base) + size;
+  if (uintptr_t(ptr) < uintptr_t(base) || end > aend)
+    return fail(MUON_ERR_INVALID_ARG, what + " needs " + std::to_string(bytes) + " bytes, its allocation ends " +
+                                          std::to_string(aend > uintptr_t(ptr) ? aend - uintptr_t(ptr) : 0) +
+                                          " bytes after it");
+  return MUON_OK;
+}
+
+// The buffer checks of a step: non-NULL, aligned, the workspace large
+// enough, the current device the plan's; with `memory`, also where each
+// buffer lives (check_memory) -- muon_step does that whenever its buffer
+// addresses change.
+muon_status check_buffers(const muon::Plan& p, void* const* params, const void* const* grads,
+                          void* const* momentum, const void* workspace, size_t workspace_bytes,
+                          float* const* update_out, bool memory) {
   if (!params || !grads || !momentum) return fail(MUON_ERR_INVALID_ARG, "params, grads and momentum must be non-NULL");
-  if (!std::isfinite(lr) || lr < 0.f) return fail(MUON_ERR_INVALID_ARG, "lr must be finite and >= 0");
-  if (!std::isfinite(wd) || wd < 0.f) return fail(MUON_ERR_INVALID_ARG, "weight_decay must be finite and >= 0");
-  if (!(mu >= 0.f && mu < 1.f)) return fail(MUON_ERR_INVALID_ARG, "momentum_coef must be in [0, 1)");
-  if (ns_steps < 0 || ns_steps > p.opts.max_ns_steps)
-    return fail(MUON_ERR_INVALID_ARG, "ns_steps must be in [0, max_ns_steps]");
-  if (nesterov != 0 && nesterov != 1) return fail(MUON_ERR_INVALID_ARG, "nesterov must be 0 or 1");
   if (!workspace) return fail(MUON_ERR_INVALID_ARG, "workspace is NULL");
   if (!aligned(workspace, 256)) return fail(MUON_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
   if (workspace_bytes < size_t(p.ws_bytes))
@@ -126,14 +153,51 @@ muon_status step_impl(muon_plan plan, void* const* params, const void* const* gr
   if (dev != p.device)
     return fail(MUON_ERR_INVALID_ARG, "current device " + std::to_string(dev) + " is not the plan's device " +
                                           std::to_string(p.device));
+  if (!memory) return MUON_OK;
+  muon_status st = check_memory(workspace, size_t(p.ws_bytes), dev, "the workspace");
+  for (size_t i = 0; i < n && st == MUON_OK; ++i) {
+    const muon::MatHost& h = p.mats[i];
+    const size_t el = size_t(h.rows) * size_t(h.cols);
+    const std::string at = "matrix " + std::to_string(i) + " ";
+    st = check_memory(params[i], el * (h.param_dtype == MUON_BF16 ? 2 : 4), dev, at + "param");
+    if (st == MUON_OK) st = check_memory(grads[i], el * (h.grad_dtype == MUON_BF16 ? 2 : 4), dev, at + "grad");
+    if (st == MUON_OK) st = check_memory(momentum[i], el * 4, dev, at + "momentum");
+    if (st == MUON_OK && update_out && update_out[i]) st = check_memory(update_out[i], el * 4, dev, at + "update_out");
+  }
+  return st;
+}
 
-  // Refresh the device pointer table if the caller's buffers moved.
+muon_status step_impl(muon_plan plan, void* const* params, const void* const* grads, void* const* momentum,
+                      float lr, float mu, float wd, int32_t ns_steps, int32_t nesterov, void* workspace,
+                      size_t workspace_bytes, void* stream, float* const* update_out) {
+  using namespace muon;
+  if (!plan) return fail(MUON_ERR_INVALID_ARG, "plan is NULL");
+  Plan& p = plan->p;
+  if (!p.d_block) return fail(MUON_ERR_INVALID_ARG, "plan was created host-only and cannot be stepped");
+  if (!std::isfinite(lr) || lr < 0.f) return fail(MUON_ERR_INVALID_ARG, "lr must be finite and >= 0");
+  if (!std::isfinite(wd) || wd < 0.f) return fail(MUON_ERR_INVALID_ARG, "weight_decay must be finite and >= 0");
+  if (!(mu >= 0.f && mu < 1.f)) return fail(MUON_ERR_INVALID_ARG, "momentum_coef must be in [0, 1)");
+  if (ns_steps < 0 || ns_steps > p.opts.max_ns_steps)
+    return fail(MUON_ERR_INVALID_ARG, "ns_steps must be in [0, max_ns_steps]");
+  if (nesterov != 0 && nesterov != 1) return fail(MUON_ERR_INVALID_ARG, "nesterov must be 0 or 1");
+  muon_status st = check_buffers(p, params, grads, momentum, workspace, workspace_bytes, update_out, false);
+  if (st != MUON_OK) return st;
+  const size_t n = p.mats.size();
+
+  // Refresh the device pointer table if the caller's buffers moved; buffers
+  // are vetted where they live whenever their addresses change.
   bool changed = !p.ptrs_valid;
   for (size_t i = 0; i < n && !changed; ++i) {
     const PtrEntry& h = p.h_ptrs[i];
     float* out = update_out ? update_out[i] : nullptr;
     changed = h.param != params[i] || h.grad != grads[i] || h.mom != momentum[i] || h.out != out;
   }
+  if (changed || workspace != p.ws_checked) {
+    st = check_buffers(p, params, grads, momentum, workspace, workspace_bytes, update_out, true);
+    if (st != MUON_OK) return st;
+    p.ws_checked = workspace;
+  }
+  hipError_t e = hipSuccess;
   if (changed) {
     for (size_t i = 0; i < n; ++i) {
       p.h_ptrs[i].param = params[i];
@@ -460,6 +524,14 @@ muon_status muon_step(muon_plan plan, void* const* params, const void* const* gr
                       void* workspace, size_t workspace_bytes, void* hip_stream) {
   return step_impl(plan, params, grads, momentum, lr, momentum_coef, weight_decay, ns_steps, nesterov, workspace,
                    workspace_bytes, hip_stream, nullptr);
+}
+
+muon_status muon_check_buffers(muon_plan plan, void* const* params, const void* const* grads, void* const* momentum,
+                               void* workspace, size_t workspace_bytes, float* const* update_out) {
+  if (!plan) return fail(MUON_ERR_INVALID_ARG, "plan is NULL");
+  if (!plan->p.d_block) return fail(MUON_ERR_INVALID_ARG, "plan was created host-only and cannot be stepped");
+  const muon_status st = check_buffers(plan->p, params, grads, momentum, workspace, workspace_bytes, update_out, true);
+  return st == MUON_OK ? ok() : st;
 }
 
 muon_status muon_step_debug(muon_plan plan, void* const* params, const void* const* grads, void* const* momentum,

@@ -147,6 +147,7 @@ struct Plan {
   PtrEntry* d_ptrs = nullptr;
   std::vector<PtrEntry> h_ptrs;     // host shadow of d_ptrs
   bool ptrs_valid = false;
+  const void* ws_checked = nullptr;  // workspace whose memory was last vetted
 
   // launch timing (muon_plan_set_timing)
   bool timing = false;

@@ -192,3 +192,62 @@ def test_bad_buffers_are_refused_before_launch(monkeypatch):
     assert len(calls) == 2
     assert not any(torch.equal(a, b) for a, b in zip(params, before))
     plan.close()
+
+
+@pytest.mark.gpu
+def test_abi_vets_where_buffers_live():
+    # the C ABI's own checks, for callers that bypass the binding: host
+    # memory, pinned host memory and allocations shorter than the matrix are
+    # refused by muon_check_buffers and by muon_step (before anything is
+    # enqueued); a view into a larger allocation is fine
+    import ctypes
+
+    import numpy as np
+
+    import paper_2606_27153_amd._lib as L
+    lib = L.load()
+    hip = ctypes.CDLL("libamdhip64.so.7")
+    dev = "cuda:0"
+    plan = MuonPlan([(96, 160, "f32", "f32")])
+    p, g, m = (torch.randn(96, 160, device=dev) for _ in range(3))
+    ws = plan.workspace(dev)
+
+    def check(pp, gp, mp, wsp=None):
+        st = lib.muon_check_buffers(plan.handle, L.ptr_array([pp]), L.ptr_array([gp]), L.ptr_array([mp]),
+                                    ctypes.c_void_p(ws.data_ptr() if wsp is None else wsp), ws.numel(), None)
+        return st, (L.last_error() if st else "")
+
+    assert check(p.data_ptr(), g.data_ptr(), m.data_ptr()) == (L.MUON_OK, "")
+    host = np.zeros(96 * 160 + 16, dtype=np.float32)
+    hp = (host.ctypes.data + 15) // 16 * 16
+    assert check(p.data_ptr(), hp, m.data_ptr()) == (L.MUON_ERR_INVALID_ARG, "matrix 0 grad is not device memory")
+    pinned = torch.zeros(96 * 160, pin_memory=True)
+    assert check(p.data_ptr(), g.data_ptr(), pinned.data_ptr())[1] == "matrix 0 momentum is not device memory"
+    raw = ctypes.c_void_p()
+    assert hip.hipMalloc(ctypes.byref(raw), ctypes.c_size_t(4096)) == 0
+    try:
+        st, msg = check(raw.value, g.data_ptr(), m.data_ptr())
+        assert st == L.MUON_ERR_INVALID_ARG and msg.startswith("matrix 0 param needs 61440 bytes"), msg
+        st, msg = check(p.data_ptr(), g.data_ptr(), m.data_ptr(), raw.value)
+        assert st == L.MUON_ERR_INVALID_ARG and msg.startswith("the workspace needs"), msg
+    finally:
+        assert hip.hipFree(raw) == 0
+    big = torch.zeros(4, 96, 160, device=dev)
+    assert check(big[2].data_ptr(), g.data_ptr(), m.data_ptr())[0] == L.MUON_OK
+
+    # muon_step makes the same checks when its buffer addresses change
+    before = p.clone()
+    stream = torch.cuda.current_stream(dev).cuda_stream
+
+    def step(gp):
+        return lib.muon_step(plan.handle, L.ptr_array([p.data_ptr()]), L.ptr_array([gp]),
+                             L.ptr_array([m.data_ptr()]), 0.02, 0.95, 0.01, 5, 1,
+                             ctypes.c_void_p(ws.data_ptr()), ws.numel(), ctypes.c_void_p(stream))
+
+    assert step(hp) == L.MUON_ERR_INVALID_ARG and L.last_error() == "matrix 0 grad is not device memory"
+    torch.cuda.synchronize()
+    assert torch.equal(p, before)
+    assert step(g.data_ptr()) == L.MUON_OK
+    torch.cuda.synchronize()
+    assert not torch.equal(p, before)
+    plan.close()
