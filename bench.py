@@ -303,6 +303,38 @@ def live_flop_share(plan, k: int, zero) -> dict:
     return {key: (live.get(key, 0.0) / v if v > 0 else 1.0) for key, v in tot.items()}
 
 
+def measure_peaks(torch, dev, copy_mib: int = 1024, reps: int = 5) -> dict:
+    """Rates the same box reaches outside this library, as context for the
+    vendor peaks: a device-to-device copy (HBM read + write) and the vendor
+    BLAS (torch.bmm, bf16, contiguous operands) on the B*X shape of the 8B
+    set's MLP matrices, a full product with no symmetry to exploit."""
+    def timed(fn):
+        fn()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        b.synchronize()
+        return a.elapsed_time(b) / reps * 1e-3
+    nb = copy_mib << 20
+    src = torch.ones(nb, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    t_copy = timed(lambda: dst.copy_(src))
+    del src, dst
+    batch, m, n, k = 8, 4096, 14336, 4096
+    x = torch.randn(batch, m, k, device=dev, dtype=torch.bfloat16)
+    y = torch.randn(batch, k, n, device=dev, dtype=torch.bfloat16)
+    z = torch.empty(batch, m, n, device=dev, dtype=torch.bfloat16)
+    t_mm = timed(lambda: torch.bmm(x, y, out=z))
+    del x, y, z
+    return {"hbm_device_copy_gbs": round(2.0 * nb / t_copy / 1e9, 1),
+            "bf16_bmm_tflops": round(2.0 * batch * m * n * k / t_mm / 1e12, 1),
+            "what": f"device-to-device copy of {copy_mib} MiB (read + write bytes); torch.bmm bf16 "
+                    f"{batch} x ({m}x{k} @ {k}x{n}), the vendor BLAS on the B*X shape"}
+
+
 def lpt_partition(costs, n_owners: int):
     """Longest-processing-time assignment: matrices in decreasing cost, each
     to the owner with the least load so far (ties to the lowest rank).
@@ -429,6 +461,7 @@ def main(argv=None) -> int:
                     help="Gram-space recurrence (Eq. 4) for matrices with n >= this * m; 0 = Eq. 2 only")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle time to sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-peaks", action="store_true", help="skip the copy and vendor-BLAS reference rates")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="run one device-to-device copy of this size first (HBM counter calibration)")
     ap.add_argument("--rocprof-summary", metavar="DIR", help="summarise rocprofv3 CSV output and exit")
@@ -609,6 +642,10 @@ def main(argv=None) -> int:
         log(f"[bench] {args.steps} graph replays: {graph_ms:.3f} ms/step")
         del graph
     floor_ms = (gemm_flops / (peak_mm * 1e12) + ew_bytes / (PEAK_HBM_GBS * 1e9)) * 1e3
+    peaks = None
+    if not args.no_peaks and args.copy_calibration_mib == 0:
+        peaks = measure_peaks(torch, dev)
+        log(f"[bench] measured on this box: {peaks}")
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] timing the fp64 oracle on a sample of the same set ...")
@@ -645,6 +682,7 @@ def main(argv=None) -> int:
         "step_roofline_floor_ms": round(floor_ms, 3),
         "step_roofline_frac": round(floor_ms / ms_per_step, 4),
         "roofline": roof,
+        "measured_peaks": peaks,
         "cpu_baseline": cpu,
         "owner_share": share,
         "kernels": per_kernel,
