@@ -103,6 +103,7 @@ struct ClassLaunch {
   int32_t n_lower;
   int64_t full_off;    // TileEntry offset of the full list
   int32_t n_full;
+  bool padded;         // some matrix is padded by a whole wave block (rows or columns)
 };
 
 struct WaveHost {

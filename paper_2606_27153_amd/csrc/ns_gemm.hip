@@ -700,7 +700,14 @@ __device__ __forceinline__ void fuse_input(const char* sb, int kt, int row0, int
   }
 }
 
-template <typename E, int TILE, int WGM, int WGN, int STAGE>
+// PAD: the launch holds matrices padded to the tile, and a wave whose output
+// block lies wholly in the padding (rows at or past m, or columns at or past
+// the real extent) skips its fragment reads and MFMAs -- its accumulators
+// stay zero, which is what the padding holds -- while it still loads its
+// share of each slab and meets every barrier.  The other wave on its SIMD
+// then has the matrix core to itself.  Launches without padding use the
+// PAD = false instantiation, whose loop has no such tests.
+template <typename E, int TILE, int WGM, int WGN, int STAGE, bool PAD = false>
 __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) {
   using C = Cfg<E, TILE, WGM, WGN>;
   // bf16 B*X takes its second operand from row-major X via transposing reads
@@ -773,6 +780,9 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
   const bool FUSE = (STAGE == ST_POLY || STAGE == ST_BX) && args.fcoef != 0.f;
   const float fcoef = args.fcoef;
   const int frow0 = ti * TILE + wm * C::WTM;
+  const bool live = !PAD || (int64_t(frow0) < d.m &&
+                             int64_t(tj) * TILE + wn * C::WTN <
+                                 (STAGE == ST_BX ? int64_t(d.rows > d.cols ? d.rows : d.cols) : int64_t(d.m)));
   if (!zero) {
     if constexpr (TRB) {
       const E* srca = lane_src<C>(opa, K, wid, lane);
@@ -786,31 +796,31 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
       load_slab_rows<C>(srcb, np, 0, stage0 + C::OPB, wid);
       wait_vm_all();
       __syncthreads();
-      read_frags_tr<C, E>(stage0, stage0 + C::OPB, oa[0], ot, 0, fa0, fb0);
+      if (live) read_frags_tr<C, E>(stage0, stage0 + C::OPB, oa[0], ot, 0, fa0, fb0);
       int kt = 0;
       for (; kt + 2 <= nk; kt += 2) {
         load_slab<C>(srca, K, kt + 1, stage1, wid);
         load_slab_rows<C>(srcb, np, kt + 1, stage1 + C::OPB, wid);
-        slab_body_tr<C, E>(stage0, oa, ot, fa0, fb0, fa1, fb1, acc);
-        if (FUSE) fuse_input<C, E, true>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
+        if (live) slab_body_tr<C, E>(stage0, oa, ot, fa0, fb0, fa1, fb1, acc);
+        if (FUSE && live) fuse_input<C, E, true>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
         wait_vm_all();
         __syncthreads();
-        read_frags_tr<C, E>(stage1, stage1 + C::OPB, oa[0], ot, 0, fa0, fb0);
+        if (live) read_frags_tr<C, E>(stage1, stage1 + C::OPB, oa[0], ot, 0, fa0, fb0);
         __builtin_amdgcn_sched_barrier(0);
         if (kt + 2 < nk) {
           load_slab<C>(srca, K, kt + 2, stage0, wid);
           load_slab_rows<C>(srcb, np, kt + 2, stage0 + C::OPB, wid);
         }
-        slab_body_tr<C, E>(stage1, oa, ot, fa0, fb0, fa1, fb1, acc);
-        if (FUSE) fuse_input<C, E, true>(stage1 + C::OPB, kt + 1, frow0, wn, lane, fcoef, acc);
+        if (live) slab_body_tr<C, E>(stage1, oa, ot, fa0, fb0, fa1, fb1, acc);
+        if (FUSE && live) fuse_input<C, E, true>(stage1 + C::OPB, kt + 1, frow0, wn, lane, fcoef, acc);
         wait_vm_all();
         __syncthreads();
-        if (kt + 2 < nk) read_frags_tr<C, E>(stage0, stage0 + C::OPB, oa[0], ot, 0, fa0, fb0);
+        if (kt + 2 < nk && live) read_frags_tr<C, E>(stage0, stage0 + C::OPB, oa[0], ot, 0, fa0, fb0);
         __builtin_amdgcn_sched_barrier(0);
       }
       if (kt < nk) {  // odd slab count: the last slab is in stage 0
-        slab_body_tr<C, E>(stage0, oa, ot, fa0, fb0, fa1, fb1, acc);
-        if (FUSE) fuse_input<C, E, true>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
+        if (live) slab_body_tr<C, E>(stage0, oa, ot, fa0, fb0, fa1, fb1, acc);
+        if (FUSE && live) fuse_input<C, E, true>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
         __syncthreads();
       }
     } else {
@@ -827,31 +837,31 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
       load_slab<C>(srcb, K, 0, stage0 + C::OPB, wid);
       wait_vm_all();
       __syncthreads();
-      read_frags<C, E>(stage0, stage0 + C::OPB, oa[0], ob[0], fa0, fb0);
+      if (live) read_frags<C, E>(stage0, stage0 + C::OPB, oa[0], ob[0], fa0, fb0);
       int kt = 0;
       for (; kt + 2 <= nk; kt += 2) {
         load_slab<C>(srca, K, kt + 1, stage1, wid);
         load_slab<C>(srcb, K, kt + 1, stage1 + C::OPB, wid);
-        slab_body<C, E>(stage0, oa, ob, fa0, fb0, fa1, fb1, acc);
-        if (FUSE) fuse_input<C, E, false>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
+        if (live) slab_body<C, E>(stage0, oa, ob, fa0, fb0, fa1, fb1, acc);
+        if (FUSE && live) fuse_input<C, E, false>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
         wait_vm_all();
         __syncthreads();
-        read_frags<C, E>(stage1, stage1 + C::OPB, oa[0], ob[0], fa0, fb0);
+        if (live) read_frags<C, E>(stage1, stage1 + C::OPB, oa[0], ob[0], fa0, fb0);
         __builtin_amdgcn_sched_barrier(0);
         if (kt + 2 < nk) {
           load_slab<C>(srca, K, kt + 2, stage0, wid);
           load_slab<C>(srcb, K, kt + 2, stage0 + C::OPB, wid);
         }
-        slab_body<C, E>(stage1, oa, ob, fa0, fb0, fa1, fb1, acc);
-        if (FUSE) fuse_input<C, E, false>(stage1 + C::OPB, kt + 1, frow0, wn, lane, fcoef, acc);
+        if (live) slab_body<C, E>(stage1, oa, ob, fa0, fb0, fa1, fb1, acc);
+        if (FUSE && live) fuse_input<C, E, false>(stage1 + C::OPB, kt + 1, frow0, wn, lane, fcoef, acc);
         wait_vm_all();
         __syncthreads();
-        if (kt + 2 < nk) read_frags<C, E>(stage0, stage0 + C::OPB, oa[0], ob[0], fa0, fb0);
+        if (kt + 2 < nk && live) read_frags<C, E>(stage0, stage0 + C::OPB, oa[0], ob[0], fa0, fb0);
         __builtin_amdgcn_sched_barrier(0);
       }
       if (kt < nk) {  // odd slab count: the last slab is in stage 0
-        slab_body<C, E>(stage0, oa, ob, fa0, fb0, fa1, fb1, acc);
-        if (FUSE) fuse_input<C, E, false>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
+        if (live) slab_body<C, E>(stage0, oa, ob, fa0, fb0, fa1, fb1, acc);
+        if (FUSE && live) fuse_input<C, E, false>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
         __syncthreads();
       }
     }
@@ -922,21 +932,21 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
   }
 }
 
-template <typename E, int TILE, int WGM, int WGN>
+template <typename E, int TILE, int WGM, int WGN, bool PAD = false>
 int launch_stage(int32_t stage, unsigned nblocks, const GemmArgs& g, hipStream_t st) {
   constexpr int NT = WGM * WGN * 64;
   switch (stage) {
     case ST_GRAM:
-      hipLaunchKernelGGL((ns_gemm_kernel<E, TILE, WGM, WGN, ST_GRAM>), dim3(nblocks), dim3(NT), 0, st, g);
+      hipLaunchKernelGGL((ns_gemm_kernel<E, TILE, WGM, WGN, ST_GRAM, PAD>), dim3(nblocks), dim3(NT), 0, st, g);
       break;
     case ST_POLY:
-      hipLaunchKernelGGL((ns_gemm_kernel<E, TILE, WGM, WGN, ST_POLY>), dim3(nblocks), dim3(NT), 0, st, g);
+      hipLaunchKernelGGL((ns_gemm_kernel<E, TILE, WGM, WGN, ST_POLY, PAD>), dim3(nblocks), dim3(NT), 0, st, g);
       break;
     case ST_BX:
-      hipLaunchKernelGGL((ns_gemm_kernel<E, TILE, WGM, WGN, ST_BX>), dim3(nblocks), dim3(NT), 0, st, g);
+      hipLaunchKernelGGL((ns_gemm_kernel<E, TILE, WGM, WGN, ST_BX, PAD>), dim3(nblocks), dim3(NT), 0, st, g);
       break;
     default:
-      hipLaunchKernelGGL((ns_gemm_kernel<E, TILE, WGM, WGN, ST_SYM>), dim3(nblocks), dim3(NT), 0, st, g);
+      hipLaunchKernelGGL((ns_gemm_kernel<E, TILE, WGM, WGN, ST_SYM, PAD>), dim3(nblocks), dim3(NT), 0, st, g);
       break;
   }
   return hipGetLastError() == hipSuccess ? 0 : -1;
@@ -974,12 +984,18 @@ int launch_ns_gemm(const Plan& p, const WaveHost& w, const ClassLaunch& cl, int3
   if (nblocks == 0) return 0;
   hipStream_t st = hipStream_t(stream);
   switch (cl.kclass) {
-    case KC_BF16_256: return launch_stage<__bf16, 256, 2, 4>(stage, grid, g, st);
+    // the 256 tile puts two waves on each SIMD, so a skipped wave speeds up
+    // its partner; with one wave per SIMD (the 4-wave classes) nothing would
+    case KC_BF16_256:
+      return cl.padded ? launch_stage<__bf16, 256, 2, 4, true>(stage, grid, g, st)
+                       : launch_stage<__bf16, 256, 2, 4>(stage, grid, g, st);
     case KC_BF16_128: return launch_stage<__bf16, 128, 2, 2>(stage, grid, g, st);
     case KC_BF16_64: return launch_stage<__bf16, 64, 2, 2>(stage, grid, g, st);
     case KC_F32_128: return launch_stage<float, 128, 2, 2>(stage, grid, g, st);
     case KC_F32_64: return launch_stage<float, 64, 2, 2>(stage, grid, g, st);
-    case KC_F16_256: return launch_stage<_Float16, 256, 2, 4>(stage, grid, g, st);
+    case KC_F16_256:
+      return cl.padded ? launch_stage<_Float16, 256, 2, 4, true>(stage, grid, g, st)
+                       : launch_stage<_Float16, 256, 2, 4>(stage, grid, g, st);
     case KC_F16_128: return launch_stage<_Float16, 128, 2, 2>(stage, grid, g, st);
     case KC_F16_64: return launch_stage<_Float16, 64, 2, 2>(stage, grid, g, st);
     default: return -1;

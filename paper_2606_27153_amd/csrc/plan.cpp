@@ -389,11 +389,14 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
       std::vector<std::vector<TileEntry>> units;
       const int64_t tile = kClasses[kc].tile;
       double fg = 0, fp = 0, fb = 0;
+      bool padded = false;
       for (int32_t s = 0; s < w.count; ++s) {
         const MatHost& h = p.mats[size_t(p.order[size_t(w.first + s)])];
         if (h.kclass != kc || h.gram != gram) continue;
         const int32_t pos = w.first + s;
         const double m = double(h.m), nn = double(h.n);
+        // a wave block of the 256 tile is 128 rows x 64 columns
+        padded = padded || h.m_pad - h.m >= 64 || h.n_pad - h.n >= 64;
         fg += m * m * nn;
         fp += m * m * m;
         fb += 2 * m * m * nn;
@@ -415,6 +418,7 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
       cl.flops_gram = fg;
       cl.flops_poly = fp;
       cl.flops_bx = fb;
+      cl.padded = padded;
       cl.lower_off = int64_t(p.h_tiles.size());
       cl.n_lower = int32_t(lower.size());
       p.h_tiles.insert(p.h_tiles.end(), lower.begin(), lower.end());
