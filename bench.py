@@ -646,6 +646,10 @@ def main(argv=None) -> int:
     if not args.no_peaks and args.copy_calibration_mib == 0:
         peaks = measure_peaks(torch, dev)
         log(f"[bench] measured on this box: {peaks}")
+        if roof["bound"] == "mfma" and args.precision != "fp32":
+            # the dominant kernel against the vendor BLAS on the same box
+            # (box-to-box clock differences move both alike)
+            roof["vs_vendor_bf16_bmm"] = round(roof["achieved"] / peaks["bf16_bmm_tflops"], 3)
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] timing the fp64 oracle on a sample of the same set ...")
