@@ -192,21 +192,26 @@ __device__ __forceinline__ void read_frags(const char* sa, const char* sb, int o
   for (int i = 0; i < C::NBM; ++i) fa[i] = *reinterpret_cast<const typename Frag<E>::T*>(sa + oa + i * 4096);
 }
 
-template <class C, typename E>
+// MASK: only the 32 x 32 blocks (i, j) with bit i * NBN + j of `mask` set are
+// multiplied (the mask is wave-uniform).
+template <class C, typename E, bool MASK = false>
 __device__ __forceinline__ void mfma_frags(const typename Frag<E>::T (&fa)[C::NBM],
-                                           const typename Frag<E>::T (&fb)[C::NBN], f32x16 (&acc)[C::NBM][C::NBN]) {
+                                           const typename Frag<E>::T (&fb)[C::NBN], f32x16 (&acc)[C::NBM][C::NBN],
+                                           uint32_t mask = 0) {
   if constexpr (__is_same(E, __bf16)) {
 #pragma unroll
     for (int i = 0; i < C::NBM; ++i)
 #pragma unroll
       for (int j = 0; j < C::NBN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+        if (!MASK || ((mask >> (i * C::NBN + j)) & 1u))
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
   } else if constexpr (__is_same(E, _Float16)) {
 #pragma unroll
     for (int i = 0; i < C::NBM; ++i)
 #pragma unroll
       for (int j = 0; j < C::NBN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+        if (!MASK || ((mask >> (i * C::NBN + j)) & 1u))
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[i], fb[j], acc[i][j], 0, 0, 0);
   } else {
     // fp32: lane half h holds k = 4*(2*ks + h) + q for element q, and the
     // same mapping on both operands, so the four 32x32x2 MFMAs cover 8 k.
@@ -237,25 +242,30 @@ __device__ __forceinline__ void interleave() {
 // MFMA work of one 128-byte K slab held in LDS stage st.  On entry the
 // fragments of sub-step 0 are in (fa0, fb0); each sub-step reads the next
 // sub-step's fragments while its own MFMAs run.
-template <class C, typename E>
+template <class C, typename E, bool MASK = false>
 __device__ __forceinline__ void slab_body(const char* st, const int (&oa)[4], const int (&ob)[4],
                                           typename Frag<E>::T (&fa0)[C::NBM], typename Frag<E>::T (&fb0)[C::NBN],
                                           typename Frag<E>::T (&fa1)[C::NBM], typename Frag<E>::T (&fb1)[C::NBN],
-                                          f32x16 (&acc)[C::NBM][C::NBN]) {
+                                          f32x16 (&acc)[C::NBM][C::NBN], uint32_t mask = 0) {
   constexpr int NR = C::NBM + C::NBN;
   constexpr int NM = C::NBM * C::NBN * (sizeof(E) == 2 ? 1 : 4);
   read_frags<C, E>(st, st + C::OPB, oa[1], ob[1], fa1, fb1);
-  mfma_frags<C, E>(fa0, fb0, acc);
+  mfma_frags<C, E, MASK>(fa0, fb0, acc, mask);
   interleave<NR, NM>();
   read_frags<C, E>(st, st + C::OPB, oa[2], ob[2], fa0, fb0);
-  mfma_frags<C, E>(fa1, fb1, acc);
+  mfma_frags<C, E, MASK>(fa1, fb1, acc, mask);
   interleave<NR, NM>();
   read_frags<C, E>(st, st + C::OPB, oa[3], ob[3], fa1, fb1);
-  mfma_frags<C, E>(fa0, fb0, acc);
+  mfma_frags<C, E, MASK>(fa0, fb0, acc, mask);
   interleave<NR, NM>();
-  mfma_frags<C, E>(fa1, fb1, acc);
+  mfma_frags<C, E, MASK>(fa1, fb1, acc, mask);
   __builtin_amdgcn_sched_barrier(0);
 }
+
+template <bool B>
+struct BoolTag {
+  static constexpr bool value = B;
+};
 
 __device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
@@ -274,9 +284,10 @@ struct Vec4<float> { typedef f32x4 T; };
 // non-temporal stores (full lines; the outputs are far larger than the
 // caches and would otherwise evict operand panels other blocks still read).  Rows are
 // processed in passes that fit the region.
-template <class C, typename OUT>
+template <class C, typename OUT, bool MASK = false>
 __device__ __forceinline__ void store_rows_via_lds(const f32x16 (&acc)[C::NBM][C::NBN], char* region,
-                                                   OUT* out, int64_t ld, int64_t row0, int64_t col0, int lane) {
+                                                   OUT* out, int64_t ld, int64_t row0, int64_t col0, int lane,
+                                                   uint32_t mask = 0) {
   constexpr int ESZ = int(sizeof(OUT));
   constexpr int ROWB = C::WTN * ESZ;                   // bytes of one sub-tile row in LDS
   constexpr int PASS = C::WAVE_LDS / ROWB < C::WTM ? C::WAVE_LDS / ROWB : C::WTM;
@@ -302,6 +313,7 @@ __device__ __forceinline__ void store_rows_via_lds(const f32x16 (&acc)[C::NBM][C
     for (int it = 0; it < PASS * CPR / 64; ++it) {
       const int piece = lane + 64 * it;
       const int r = piece / CPR, pc = piece % CPR;
+      if (MASK && !((mask >> (((p0 + r) / 32) * C::NBN + pc * EPP / 32)) & 1u)) continue;
       const f32x4 v = *reinterpret_cast<const f32x4*>(region + r * ROWB + pc * 16);
       __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(out + (row0 + p0 + r) * ld + col0 + pc * EPP));
     }
@@ -330,9 +342,10 @@ struct TLay {
 
 // Writes this wave's accumulator tile transposed: out[(col0 + j) * ld + row0
 // + i] = acc(i, j), through LDS in TLay layout and full-line 16-byte stores.
-template <class C, typename OUT>
+template <class C, typename OUT, bool MASK = false>
 __device__ __forceinline__ void store_t_via_lds(const f32x16 (&acc)[C::NBM][C::NBN], char* region, OUT* out,
-                                                int64_t ld, int64_t row0, int64_t col0, int lane) {
+                                                int64_t ld, int64_t row0, int64_t col0, int lane,
+                                                uint32_t mask = 0) {
   using L = TLay<C, OUT>;
   constexpr int N = C::WTN * L::PPR;
   constexpr int EPP = 16 / L::ESZ;
@@ -363,6 +376,7 @@ __device__ __forceinline__ void store_t_via_lds(const f32x16 (&acc)[C::NBM][C::N
     for (int it = 0; it < N / 64; ++it) {
       const int piece = lane + 64 * it;
       const int r = piece / L::PPR, pc = piece % L::PPR;
+      if (MASK && !((mask >> (((p0 + pc * EPP) / 32) * C::NBN + r / 32)) & 1u)) continue;
       const f32x4 v = *reinterpret_cast<const f32x4*>(region + L::off(r, pc * 16));
       __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(out + (col0 + r) * ld + row0 + p0 + pc * EPP));
     }
@@ -728,8 +742,41 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
-  const int wm = wid / WGN, wn = wid % WGN;
   const int ti = te.ti, tj = te.tj;
+  // A diagonal tile of a symmetric product needs only the 32 x 32 blocks on
+  // or below the diagonal (36 of 64 for the 256 tile).  They lie in six
+  // 128 x 64 wave pieces, which go to the waves so that no SIMD (waves w and
+  // w + 4 share one) carries more than 11 block streams instead of 16; waves
+  // 6 and 7 only load and meet the barriers.  Such a tile runs its own copy of
+  // the K loop, with the blocks masked; each computed block is stored
+  // transposed in its mirror position, and a block below the diagonal also as
+  // computed, so the stored tile is symmetric like every off-diagonal pair.
+  constexpr bool DSPLIT = TILE == 256 && WGM == 2 && WGN == 4 && sizeof(E) == 2 && STAGE != ST_BX;
+  const bool dtile = DSPLIT && ti == tj;
+  int wm = wid / WGN, wn = wid % WGN;
+  uint32_t bmask = 0, rmask = 0;  // diagonal tile: blocks to compute / to store as computed
+  bool dlive = true;
+  if (dtile) {
+    switch (wid) {  // wave -> (row piece, column piece)
+      case 0: wm = 1; wn = 0; break;
+      case 1: wm = 1; wn = 1; break;
+      case 2: wm = 0; wn = 0; break;
+      case 3: wm = 1; wn = 2; break;
+      case 4: wm = 0; wn = 1; break;
+      case 5: wm = 1; wn = 3; break;
+      default: wm = 0; wn = 0; dlive = false; break;
+    }
+    if (dlive) {
+#pragma unroll
+      for (int i = 0; i < C::NBM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::NBN; ++j) {
+          const int rb = wm * C::NBM + i, cb = wn * C::NBN + j;
+          if (rb >= cb) bmask |= 1u << (i * C::NBN + j);
+          if (rb > cb) rmask |= 1u << (i * C::NBN + j);
+        }
+    }
+  }
   const int64_t mp = d.m_pad, np = d.n_pad;
 
   const E* opa;
@@ -833,37 +880,44 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
         ob[ks] = frag_off(wn * C::WTN, lane, ks);
       }
       typename Frag<E>::T fa0[C::NBM], fb0[C::NBN], fa1[C::NBM], fb1[C::NBN];
-      load_slab<C>(srca, K, 0, stage0, wid);
-      load_slab<C>(srcb, K, 0, stage0 + C::OPB, wid);
-      wait_vm_all();
-      __syncthreads();
-      if (live) read_frags<C, E>(stage0, stage0 + C::OPB, oa[0], ob[0], fa0, fb0);
-      int kt = 0;
-      for (; kt + 2 <= nk; kt += 2) {
-        load_slab<C>(srca, K, kt + 1, stage1, wid);
-        load_slab<C>(srcb, K, kt + 1, stage1 + C::OPB, wid);
-        if (live) slab_body<C, E>(stage0, oa, ob, fa0, fb0, fa1, fb1, acc);
-        if (FUSE && live) fuse_input<C, E, false>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
+      auto kloop = [&](auto masked) {
+        constexpr bool M = decltype(masked)::value;
+        load_slab<C>(srca, K, 0, stage0, wid);
+        load_slab<C>(srcb, K, 0, stage0 + C::OPB, wid);
         wait_vm_all();
         __syncthreads();
-        if (live) read_frags<C, E>(stage1, stage1 + C::OPB, oa[0], ob[0], fa0, fb0);
-        __builtin_amdgcn_sched_barrier(0);
-        if (kt + 2 < nk) {
-          load_slab<C>(srca, K, kt + 2, stage0, wid);
-          load_slab<C>(srcb, K, kt + 2, stage0 + C::OPB, wid);
+        if (live) read_frags<C, E>(stage0, stage0 + C::OPB, oa[0], ob[0], fa0, fb0);
+        int kt = 0;
+        for (; kt + 2 <= nk; kt += 2) {
+          load_slab<C>(srca, K, kt + 1, stage1, wid);
+          load_slab<C>(srcb, K, kt + 1, stage1 + C::OPB, wid);
+          if (live) slab_body<C, E, M>(stage0, oa, ob, fa0, fb0, fa1, fb1, acc, bmask);
+          if (FUSE && live) fuse_input<C, E, false>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
+          wait_vm_all();
+          __syncthreads();
+          if (live) read_frags<C, E>(stage1, stage1 + C::OPB, oa[0], ob[0], fa0, fb0);
+          __builtin_amdgcn_sched_barrier(0);
+          if (kt + 2 < nk) {
+            load_slab<C>(srca, K, kt + 2, stage0, wid);
+            load_slab<C>(srcb, K, kt + 2, stage0 + C::OPB, wid);
+          }
+          if (live) slab_body<C, E, M>(stage1, oa, ob, fa0, fb0, fa1, fb1, acc, bmask);
+          if (FUSE && live) fuse_input<C, E, false>(stage1 + C::OPB, kt + 1, frow0, wn, lane, fcoef, acc);
+          wait_vm_all();
+          __syncthreads();
+          if (kt + 2 < nk && live) read_frags<C, E>(stage0, stage0 + C::OPB, oa[0], ob[0], fa0, fb0);
+          __builtin_amdgcn_sched_barrier(0);
         }
-        if (live) slab_body<C, E>(stage1, oa, ob, fa0, fb0, fa1, fb1, acc);
-        if (FUSE && live) fuse_input<C, E, false>(stage1 + C::OPB, kt + 1, frow0, wn, lane, fcoef, acc);
-        wait_vm_all();
-        __syncthreads();
-        if (kt + 2 < nk && live) read_frags<C, E>(stage0, stage0 + C::OPB, oa[0], ob[0], fa0, fb0);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-      if (kt < nk) {  // odd slab count: the last slab is in stage 0
-        if (live) slab_body<C, E>(stage0, oa, ob, fa0, fb0, fa1, fb1, acc);
-        if (FUSE && live) fuse_input<C, E, false>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
-        __syncthreads();
-      }
+        if (kt < nk) {  // odd slab count: the last slab is in stage 0
+          if (live) slab_body<C, E, M>(stage0, oa, ob, fa0, fb0, fa1, fb1, acc, bmask);
+          if (FUSE && live) fuse_input<C, E, false>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
+          __syncthreads();
+        }
+      };
+      if (dtile)
+        kloop(BoolTag<true>{});
+      else
+        kloop(BoolTag<false>{});
     }
   }
 
@@ -925,6 +979,11 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
         apply_via_lds<C, true, float>(acc, region, pe, d, lrs, args.decay, row0, col0, lane);
       else
         apply_via_lds<C, false, float>(acc, region, pe, d, lrs, args.decay, row0, col0, lane);
+    }
+  } else if (dtile) {
+    if (dlive) {
+      store_t_via_lds<C, E, true>(acc, region, out_t, mp, row0, col0, lane, bmask);
+      if (rmask) store_rows_via_lds<C, E, true>(acc, region, out_r, ld_r, row0, col0, lane, rmask);
     }
   } else {
     if (!TRB) store_t_via_lds<C, E>(acc, region, out_t, mp, row0, col0, lane);
