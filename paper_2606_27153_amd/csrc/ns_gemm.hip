@@ -751,8 +751,10 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
   // the K loop, with the blocks masked; each computed block is stored
   // transposed in its mirror position, and a block below the diagonal also as
   // computed, so the stored tile is symmetric like every off-diagonal pair.
+  // (A matrix one tile wide is left whole: in its short, latency-bound
+  // launches the second store pass costs more than the skipped blocks save.)
   constexpr bool DSPLIT = TILE == 256 && WGM == 2 && WGN == 4 && sizeof(E) == 2 && STAGE != ST_BX;
-  const bool dtile = DSPLIT && ti == tj;
+  const bool dtile = DSPLIT && ti == tj && args.mats[te.mat].m_pad > TILE;
   int wm = wid / WGN, wn = wid % WGN;
   uint32_t bmask = 0, rmask = 0;  // diagonal tile: blocks to compute / to store as computed
   bool dlive = true;
