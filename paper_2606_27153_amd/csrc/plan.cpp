@@ -30,10 +30,7 @@ constexpr ClassInfo kClasses[KC_COUNT] = {
 
 // Relative throughput assumed for each class when choosing a tile: larger
 // tiles re-use each loaded byte more often.
-#ifndef MUON_EFF128
-#define MUON_EFF128 0.8
-#endif
-constexpr double kClassEfficiency[KC_COUNT] = {1.0, MUON_EFF128, 0.45, 1.0, 0.6, 1.0, MUON_EFF128, 0.45};
+constexpr double kClassEfficiency[KC_COUNT] = {1.0, 0.8, 0.45, 1.0, 0.6, 1.0, 0.8, 0.45};
 
 constexpr int64_t kDefaultWaveBytes = int64_t(12) << 30;  // 12 GiB
 constexpr int64_t kAlign = 256;
@@ -75,10 +72,6 @@ int32_t choose_class(int64_t m, int64_t n, const muon_plan_opts& o, int32_t tile
   return best;
 }
 
-#ifndef MUON_TILE_ORDER
-#define MUON_TILE_ORDER 1
-#endif
-
 // Full tile list of one matrix (tm x tn output tiles) in dispatch order.
 //
 // Blocks are dispatched round-robin over the 8 XCDs (block b runs on XCD
@@ -90,20 +83,18 @@ int32_t choose_class(int64_t m, int64_t n, const muon_plan_opts& o, int32_t tile
 // not fit that pattern fall back to column-major order in groups of 4 rows.
 void emit_full(std::vector<TileEntry>& t, int32_t mat, int64_t tm, int64_t tn) {
   int64_t g0 = 0;
-  if (MUON_TILE_ORDER == 1) {
-    for (; g0 + 8 <= tm; g0 += 8) {
-      for (int64_t c0 = 0; c0 < tn; c0 += 32) {
-        const int64_t w = std::min<int64_t>(32, tn - c0);
-        if (w % 4 != 0 || t.size() % 8 != 0) {
-          for (int64_t tj = c0; tj < c0 + w; ++tj)
-            for (int64_t ti = g0; ti < g0 + 8; ++ti) t.push_back(TileEntry{mat, int32_t(ti), int32_t(tj)});
-          continue;
-        }
-        for (int64_t b = 0; b < 8 * w; ++b) {
-          const int64_t x = b % 8, k = b / 8;
-          const int64_t r = 4 * (x % 2) + k % 4, c = (x / 2) * (w / 4) + k / 4;
-          t.push_back(TileEntry{mat, int32_t(g0 + r), int32_t(c0 + c)});
-        }
+  for (; g0 + 8 <= tm; g0 += 8) {
+    for (int64_t c0 = 0; c0 < tn; c0 += 32) {
+      const int64_t w = std::min<int64_t>(32, tn - c0);
+      if (w % 4 != 0 || t.size() % 8 != 0) {
+        for (int64_t tj = c0; tj < c0 + w; ++tj)
+          for (int64_t ti = g0; ti < g0 + 8; ++ti) t.push_back(TileEntry{mat, int32_t(ti), int32_t(tj)});
+        continue;
+      }
+      for (int64_t b = 0; b < 8 * w; ++b) {
+        const int64_t x = b % 8, k = b / 8;
+        const int64_t r = 4 * (x % 2) + k % 4, c = (x / 2) * (w / 4) + k / 4;
+        t.push_back(TileEntry{mat, int32_t(g0 + r), int32_t(c0 + c)});
       }
     }
   }
