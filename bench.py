@@ -260,12 +260,23 @@ def cpu_baseline(wl, budget_s: float):
                        + "; ".join(sampled) + "), scaled by bucket counts to the whole set")}
 
 
-def ns_cost(rows: int, cols: int, k: int = 5, gram_min_aspect: float = 2.0) -> float:
+GRAM_MIN_M = 256      # smaller matrices stay on Eq. 2
+GRAM_RESTART = 2     # NS steps per Gram-space segment (the library's default)
+
+
+def gram_segments(k: int, restart: int = GRAM_RESTART) -> list:
+    """Lengths of the Gram-space segments of k NS steps."""
+    return [min(restart, k - s0) for s0 in range(0, k, restart)]
+
+
+def ns_cost(rows: int, cols: int, k: int = 5, gram_min_aspect: float = 2.0, restart: int = GRAM_RESTART) -> float:
     """Algorithmic NS flops of one matrix in the form the plan gives it
-    (16-bit classes; Eq. 4 when n >= aspect * m and m > 64, else Eq. 2)."""
+    (16-bit classes; Eq. 4 when n >= aspect * m and m >= 256, else Eq. 2).
+    Eq. 4 restarts every ``restart`` steps; a segment of L steps costs
+    3 m^2 n + (4L - 3) m^3."""
     m, n = min(rows, cols), max(rows, cols)
-    if gram_min_aspect > 0 and n >= gram_min_aspect * m and m > 64:
-        return 3.0 * m * m * n + (4 * k - 3) * float(m) ** 3
+    if gram_min_aspect > 0 and n >= gram_min_aspect * m and m >= GRAM_MIN_M:
+        return sum(3.0 * m * m * n + (4 * L - 3) * float(m) ** 3 for L in gram_segments(k, restart))
     return k * (3.0 * m * m * n + float(m) ** 3)
 
 
@@ -283,7 +294,8 @@ def live_flop_share(plan, k: int, zero) -> dict:
     counts every matrix of a launch; the tiles of a zero-gradient matrix exit
     before their K loop, so only this share is executed.  Per matrix and step:
     Eq. 2 runs Gram (m^2 n), A*A (m^3) and B*X (2 m^2 n) k times; the Gram-space
-    form runs Gram and B*X once, P_i k times and 3k - 3 symmetric m^3 products."""
+    form runs, per segment of L steps, Gram and B*X once, P_i L times and
+    3L - 3 symmetric m^3 products."""
     from paper_2606_27153_amd import _lib as L
     tot: dict = {}
     live: dict = {}
@@ -292,8 +304,9 @@ def live_flop_share(plan, k: int, zero) -> dict:
         cls = L.KERNEL_CLASSES[mi["kernel_class"]]
         m, n = float(mi["m"]), float(mi["n"])
         if mi["gram_space"]:
-            per = {"gram": m * m * n, "poly": k * m ** 3, "symm": (3 * k - 3 if k >= 2 else 0) * m ** 3,
-                   "bx": 2 * m * m * n}
+            segs = gram_segments(k, plan.info()["gram_restart"])
+            per = {"gram": len(segs) * m * m * n, "poly": k * m ** 3,
+                   "symm": sum(3 * L - 3 for L in segs) * m ** 3, "bx": len(segs) * 2 * m * m * n}
         else:
             per = {"gram": k * m * m * n, "poly": k * m ** 3, "symm": 0.0, "bx": k * 2 * m * m * n}
         for kind, f in per.items():

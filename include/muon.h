@@ -12,11 +12,13 @@
  *      with the Gram product computed on lower-triangular tiles only and
  *      mirrored (the symmetric kernel of Sec. 3.3), the polynomial fused into
  *      the A*A product and a*X fused into B*X.  Wide enough matrices
- *      (n >= gram_min_aspect * m) instead carry the iteration in Gram space
- *      (Sec. 3.3, Eq. 4): G0 = X0 X0^T, P_i = a I + b G_i + c G_i^2,
- *      G_{i+1} = P_i (G_i P_i), Q = P_{k-1} ... P_0, X_k = Q X0 -- every
- *      m x m product symmetric (lower tiles, mirrored), one m x n product at
- *      each end: 3 m^2 n + (4k - 3) m^3 flops instead of k (3 m^2 n + m^3)
+ *      (n >= gram_min_aspect * m, m >= 256) instead carry the iteration in
+ *      Gram space (Sec. 3.3, Eq. 4): G0 = X0 X0^T, P_i = a I + b G_i +
+ *      c G_i^2, G_{i+1} = P_i (G_i P_i), Q = P_{j-1} ... P_0, X_j = Q X0 --
+ *      every m x m product symmetric (lower tiles, mirrored), one m x n
+ *      product at each end -- restarted from X_j every gram_restart steps:
+ *      per segment of L steps 3 m^2 n + (4L - 3) m^3 flops instead of
+ *      L (3 m^2 n + m^3)
  *   5. O = X^T (tall) or X (wide) -- the orthogonalised update NS_k(M_t)
  *   6. Eq. 1 with decoupled weight decay and the shape scale:
  *        W <- W*(1 - lr*wd) - lr*sqrt(max(1, rows/cols))*O
@@ -45,7 +47,7 @@
 extern "C" {
 #endif
 
-#define MUON_ABI_VERSION 3
+#define MUON_ABI_VERSION 4
 
 #if defined(__GNUC__)
 #define MUON_API __attribute__((visibility("default")))
@@ -69,7 +71,7 @@ typedef enum muon_dtype { MUON_F32 = 0, MUON_BF16 = 1 } muon_dtype;
  * min(rows, cols) <= small_m_threshold still use fp32).  MUON_NS_FP32: fp32
  * operands and fp32 matrix-core arithmetic for every matrix (validation).
  * MUON_NS_FP16: fp16 operands, fp32 accumulation, for every matrix size (the
- * NS precision of the paper's implementation, Sec. 5 "Configurations"): the
+ * NS precision of the paper's implementation, Sec. 4 "Configurations"): the
  * same matrix-core rate as bf16 and about 8x less rounding error.  Its range
  * is fp16's: the Nesterov input u = G + mu*M is stored in fp16 before it is
  * normalised, so |u| must stay below 65504, and entries below 2^-24 round to
@@ -79,6 +81,9 @@ typedef enum muon_ns_precision { MUON_NS_BF16 = 0, MUON_NS_FP32 = 1, MUON_NS_FP1
 /* Plan flags. */
 #define MUON_PLAN_HOST_ONLY 0x1u     /* build host metadata only: no device memory is
                                         touched; such a plan can be inspected but not stepped */
+#define MUON_PLAN_CHECK_BUFFERS 0x2u /* muon_step also vets where its buffers live (the memory
+                                        checks of muon_check_buffers, two HIP queries per buffer)
+                                        whenever their addresses differ from the previous call's */
 
 /* One weight matrix: stored shape and dtypes.  param in {F32, BF16},
  * grad in {F32, BF16}, momentum must be F32. */
@@ -107,14 +112,21 @@ typedef struct muon_plan_opts {
   uint32_t flags;                    /* MUON_PLAN_* */
   int64_t wave_bytes;                /* cap on the NS working set of one group ("wave")
                                         of matrices processed together; 0 = default */
-  float gram_min_aspect;             /* 16-bit NS matrices with n >= gram_min_aspect * m run the
-                                        Gram-space recurrence (Eq. 4); 0 = never.  Must be 0 or
-                                        >= 1; ignored when c = 0 at some step.  The default 2 suits
+  float gram_min_aspect;             /* 16-bit NS matrices with m >= 256 and n >= gram_min_aspect * m
+                                        run the Gram-space recurrence (Eq. 4); 0 = never.  Must be 0
+                                        or >= 1; ignored when c = 0 at some step.  The default 2 suits
                                         bf16; fp16 keeps its accuracy down to about 1.4 */
-  int32_t reserved;                  /* must be 0 */
+  int32_t gram_restart;              /* NS steps per Gram-space segment: after that many steps the
+                                        iterate X = Q X0 is formed and the recurrence restarts from
+                                        a fresh Gram matrix X X^T.  0 = the default, 2.  Without
+                                        restarts (a value >= ns_steps), 16-bit rounding of the Gram
+                                        matrix is amplified from step to step wherever the input
+                                        has small singular values, and the result can be far off;
+                                        restarting every 2 steps keeps it as accurate as Eq. 2.
+                                        Must be >= 0 */
   const float* abc_per_step;         /* NULL (a, b, c above at every step), or 3 * max_ns_steps
                                         floats: NS step i uses (a, b, c) = abc_per_step[3i],
-                                        [3i + 1], [3i + 2] (a per-step coefficient set, Sec. 5
+                                        [3i + 1], [3i + 2] (a per-step coefficient set, Sec. 4
                                         "Configurations").  Read once by muon_plan_create, which
                                         keeps a copy; every triple obeys the rule for a, b, c.  A
                                         cubic step (c = 0) keeps every matrix on Eq. 2. */
@@ -133,12 +145,8 @@ typedef struct muon_plan_info {
   double ns_flops_per_ns_step;       /* algorithmic flops of one NS step of Eq. 2 over all
                                         matrices: sum of 3 m^2 n + m^3 (symmetry-aware) */
   double padded_flops_per_ns_step;   /* flops those steps issue on padded tiles */
-  double ns_flops_fixed;             /* the plan's own algorithmic NS flops for k >= 1 steps
-                                        are ns_flops_fixed + k * ns_flops_step: Eq. 2 matrices */
-  double ns_flops_step;              /*   add 3 m^2 n + m^3 per step, Gram-space ones
-                                          3 m^2 n - 3 m^3 once and 4 m^3 per step */
   int32_t n_gram;                    /* matrices that run the Gram-space recurrence */
-  int32_t reserved;
+  int32_t gram_restart;              /* NS steps per Gram-space segment (the effective value) */
 } muon_plan_info;
 
 /* Placement of one matrix in the plan. */
@@ -157,7 +165,7 @@ typedef struct muon_matrix_info {
 
 /* Fills *o with the defaults: precision BF16, max_ns_steps 16,
  * (a,b,c) = (3.4445, -4.7750, 2.0315), eps 1e-7, small_m_threshold 64,
- * flags 0, wave_bytes 0, gram_min_aspect 2, abc_per_step NULL.  Returns
+ * flags 0, wave_bytes 0, gram_min_aspect 2, gram_restart 0 (2), abc_per_step NULL.  Returns
  * INVALID_ARG if o is NULL. */
 MUON_API muon_status muon_plan_opts_default(muon_plan_opts* o);
 
@@ -179,12 +187,23 @@ MUON_API muon_status muon_plan_destroy(muon_plan plan);
 MUON_API muon_status muon_plan_workspace_bytes(muon_plan plan, size_t* bytes);
 
 MUON_API muon_status muon_plan_get_info(muon_plan plan, muon_plan_info* info);
+
+/* The plan's own algorithmic NS flops for ns_steps steps (symmetry-aware),
+ * into *flops: an Eq. 2 matrix does 3 m^2 n + m^3 per step; a Gram-space
+ * matrix, per segment of L steps, 3 m^2 n (the Gram product and the final
+ * m x m x n product) and (4L - 3) m^3 (L polynomials P_i and 3 (L - 1)
+ * further products of the recurrence).  INVALID_ARG for a NULL argument or
+ * ns_steps outside [0, max_ns_steps]. */
+MUON_API muon_status muon_plan_ns_flops(muon_plan plan, int32_t ns_steps, double* flops);
 MUON_API muon_status muon_plan_matrix_info(muon_plan plan, int32_t index, muon_matrix_info* info);
 
 /* One Muon step over every matrix of the plan (Eq. 1, Eq. 2).
  *
  * params[i]   device, rows x cols of param_dtype, updated in place
- * grads[i]    device, rows x cols of grad_dtype, read only
+ * grads[i]    device, rows x cols of grad_dtype, read only; NULL skips
+ *             matrix i for this step: its param and momentum are left
+ *             untouched (no momentum update, no weight decay), as an
+ *             optimizer skips a parameter that received no gradient
  * momentum[i] device, rows x cols fp32, updated in place
  *   (arrays of n device pointers on the host, in descriptor order; buffers of
  *   different matrices must not overlap)
@@ -195,37 +214,48 @@ MUON_API muon_status muon_plan_matrix_info(muon_plan plan, int32_t index, muon_m
  *   concurrently need distinct workspaces and distinct plans.
  * hip_stream: hipStream_t (NULL = default stream).
  *
- * The plan caches the device copy of the pointer arrays: when they differ
- * from the previous call, the new table is copied on the stream and the
- * stream is synchronised once before the step is enqueued.  Otherwise the
- * call only enqueues kernels and never synchronises or allocates, so such a
- * call (with launch timing off) can be captured in a HIP graph and replayed;
+ * The call only enqueues work on hip_stream; it never allocates and never
+ * waits for the stream.  The plan keeps a device copy of the pointer arrays:
+ * when they differ from the previous call's, the new table is written into
+ * the next slot of a pinned host ring the plan owns (8 slots) and copied to
+ * the device on hip_stream ahead of the kernels.  The host waits only when
+ * that slot's copy from 8 refreshes earlier has not yet run on the GPU.
+ * Successive steps on one plan must be ordered on the GPU (one stream, or
+ * ordered by the caller): each refresh overwrites the device table the
+ * previous step's kernels read.
+ * A call on the same buffers as the previous call (with launch timing off)
+ * enqueues kernels only, so it can be captured in a HIP graph and replayed;
  * each replay is bitwise the step an eager call would make.  The scalars
  * (lr, momentum_coef, weight_decay, ns_steps, nesterov) are captured by
- * value: a new value needs a new capture.  Capture a call whose pointers
- * differ from the previous call's and the capture fails.
- * The plan must be used from the device it was created on.  Whenever the
- * buffer addresses change, muon_step also checks where the buffers live
- * (muon_check_buffers) before the pointer table is refreshed; a buffer that
- * is not device memory of the plan's device, or that ends before
- * rows*cols elements, gives INVALID_ARG and nothing is enqueued. */
+ * value: a new value needs a new capture.  A call whose pointers differ
+ * from the previous call's returns INVALID_ARG while its stream is being
+ * captured (the copy from the ring could not be replayed safely).  A replay
+ * reads the device table as it is at replay time: step eagerly on other
+ * buffers in between, and replays use those.
+ * The plan must be used from the device it was created on.  The step checks
+ * the arguments (NULL param or momentum, alignment, workspace size, current
+ * device) and, when the workspace address changes, that the workspace is
+ * device memory of the plan's device large enough for the plan; the other
+ * buffers' memory is vetted (muon_check_buffers) only on plans created with
+ * MUON_PLAN_CHECK_BUFFERS, whenever the addresses change.  On an error
+ * nothing is enqueued. */
 MUON_API muon_status muon_step(muon_plan plan, void* const* params, const void* const* grads,
                       void* const* momentum, float lr, float momentum_coef,
                       float weight_decay, int32_t ns_steps, int32_t nesterov,
                       void* workspace, size_t workspace_bytes, void* hip_stream);
 
 /* The buffer checks of muon_step, without enqueuing anything.  Beyond the
- * argument rules above (non-NULL, 16-byte aligned buffers, a 256-byte
- * aligned workspace of at least muon_plan_workspace_bytes, the current
- * device the plan's), every buffer must be device memory of the plan's
- * device (or managed memory), and each of [params[i], + rows*cols*param
- * size), [grads[i], ...), [momentum[i], + rows*cols*4), [update_out[i], ...)
- * and the plan's workspace bytes must lie inside one allocation (where HIP
- * reports the allocation; memory mapped through the virtual memory API may
- * not be, and is then taken on trust).  muon_step
- * makes these memory checks itself whenever its buffer addresses differ from
- * the previous call's (so a step on the same buffers makes no extra HIP
- * call); this entry point is for callers who want to vet buffers up front.
+ * argument rules above (non-NULL params and momentum, 16-byte aligned
+ * buffers, a 256-byte aligned workspace of at least
+ * muon_plan_workspace_bytes, the current device the plan's), every buffer
+ * must be device memory of the plan's device (or managed memory), and each
+ * of [params[i], + rows*cols*param size), [grads[i], ...) (unless NULL),
+ * [momentum[i], + rows*cols*4), [update_out[i], ...) and the plan's
+ * workspace bytes must lie inside one allocation (where HIP reports the
+ * allocation; memory mapped through the virtual memory API may not be, and
+ * is then taken on trust).  The kernels trust the pointers they are given,
+ * so a caller that cannot vouch for its buffers calls this once per new set
+ * of addresses, or creates the plan with MUON_PLAN_CHECK_BUFFERS.
  * update_out may be NULL.  Returns MUON_OK, INVALID_ARG or
  * WORKSPACE_TOO_SMALL with the reason in muon_last_error(). */
 MUON_API muon_status muon_check_buffers(muon_plan plan, void* const* params, const void* const* grads,
@@ -235,7 +265,8 @@ MUON_API muon_status muon_check_buffers(muon_plan plan, void* const* params, con
 /* muon_step plus, for every i with update_out[i] != NULL, the orthogonalised
  * update O_i (before lr and the shape scale) written as fp32 rows x cols
  * row-major to update_out[i] (device, 16-byte aligned).  W and M are
- * bitwise identical to muon_step's.  update_out may be NULL (no output). */
+ * bitwise identical to muon_step's.  update_out may be NULL (no output); a
+ * matrix skipped for a NULL gradient leaves its update_out untouched. */
 MUON_API muon_status muon_step_debug(muon_plan plan, void* const* params, const void* const* grads,
                             void* const* momentum, float lr, float momentum_coef,
                             float weight_decay, int32_t ns_steps, int32_t nesterov,

@@ -15,7 +15,7 @@ What is computed, per matrix (DMuon, Sec. 2.1, Eq. 1 and Eq. 2):
      (this is X <- aX + bXX^TX + c(XX^T)^2 X regrouped; the paper leaves
      (a,b,c) open, the quintic set used is (3.4445, -4.7750, 2.0315)).  A
      schedule of one (a_i, b_i, c_i) per step may replace the fixed triple
-     (Sec. 5, "Configurations": the paper's default is a per-step set):
+     (Sec. 4, "Configurations": the paper's default is a per-step set):
      step i then uses its own triple.
   5. O = X^T if transposed else X
   6. Eq. 1 with decoupled weight decay and the shape scale:
@@ -129,7 +129,7 @@ def step_coefficients(abc, steps: int):
     """The (a, b, c) of each of ``steps`` NS steps.
 
     ``abc`` is either one triple, used for every step, or a schedule of at
-    least ``steps`` triples, step i taking the i-th (Sec. 5,
+    least ``steps`` triples, step i taking the i-th (Sec. 4,
     "Configurations").
     """
     seq = list(abc)
@@ -160,24 +160,31 @@ def newton_schulz(x, steps: int, abc=QUINTIC_ABC):
     return x
 
 
-def newton_schulz_gram(x, steps: int, abc=QUINTIC_ABC):
+def newton_schulz_gram(x, steps: int, abc=QUINTIC_ABC, restart=None):
     """The same iteration carried in Gram space (Eq. 4).
 
     With G_0 = X_0 X_0^T and P_i = a I + b G_i + c G_i^2, the Gram matrix
     obeys G_{i+1} = P_i G_i P_i and X_k = P_{k-1} ... P_0 X_0.  In exact
     arithmetic this equals ``newton_schulz``.  With a per-step schedule, P_i
-    takes step i's (a_i, b_i, c_i).
+    takes step i's (a_i, b_i, c_i).  ``restart`` (a step count, or None for
+    never) ends a segment after that many steps: X_j = P_{j-1} ... X_0 is
+    formed and the recurrence starts again from G = X_j X_j^T -- in exact
+    arithmetic the same G_j, so the result is unchanged.
     """
     x = np.asarray(x, dtype=np.float64)
     m = x.shape[0]
     eye = np.eye(m)
-    gram = x @ x.T
-    q = eye.copy()
-    for a, b, c in step_coefficients(abc, steps):
-        p = a * eye + b * gram + c * (gram @ gram)
-        gram = p @ gram @ p
-        q = p @ q
-    return q @ x
+    coefs = step_coefficients(abc, steps)
+    seg = len(coefs) if restart is None else int(restart)
+    for s0 in range(0, len(coefs), max(1, seg)):
+        gram = x @ x.T
+        q = eye.copy()
+        for a, b, c in coefs[s0:s0 + seg]:
+            p = a * eye + b * gram + c * (gram @ gram)
+            gram = p @ gram @ p
+            q = p @ q
+        x = q @ x
+    return x
 
 
 def orthogonalize(u, steps: int, abc=QUINTIC_ABC, eps: float = DEFAULT_EPS):

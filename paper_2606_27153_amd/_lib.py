@@ -31,6 +31,7 @@ MUON_NS_FP32 = 1
 MUON_NS_FP16 = 2
 
 MUON_PLAN_HOST_ONLY = 0x1
+MUON_PLAN_CHECK_BUFFERS = 0x2
 
 
 class muon_matrix_desc(ctypes.Structure):
@@ -44,7 +45,7 @@ class muon_plan_opts(ctypes.Structure):
                 ("a", ctypes.c_float), ("b", ctypes.c_float), ("c", ctypes.c_float),
                 ("eps", ctypes.c_float), ("small_m_threshold", ctypes.c_int32),
                 ("flags", ctypes.c_uint32), ("wave_bytes", ctypes.c_int64),
-                ("gram_min_aspect", ctypes.c_float), ("reserved", ctypes.c_int32),
+                ("gram_min_aspect", ctypes.c_float), ("gram_restart", ctypes.c_int32),
                 ("abc_per_step", ctypes.POINTER(ctypes.c_float))]
 
 
@@ -54,8 +55,7 @@ class muon_plan_info(ctypes.Structure):
                 ("workspace_bytes", ctypes.c_int64), ("launches_per_step", ctypes.c_int64),
                 ("ns_flops_per_ns_step", ctypes.c_double),
                 ("padded_flops_per_ns_step", ctypes.c_double),
-                ("ns_flops_fixed", ctypes.c_double), ("ns_flops_step", ctypes.c_double),
-                ("n_gram", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("n_gram", ctypes.c_int32), ("gram_restart", ctypes.c_int32)]
 
 
 class muon_matrix_info(ctypes.Structure):
@@ -89,6 +89,7 @@ SIGNATURES = {
     "muon_plan_destroy": (ctypes.c_int, [_VP]),
     "muon_plan_workspace_bytes": (ctypes.c_int, [_VP, ctypes.POINTER(ctypes.c_size_t)]),
     "muon_plan_get_info": (ctypes.c_int, [_VP, ctypes.POINTER(muon_plan_info)]),
+    "muon_plan_ns_flops": (ctypes.c_int, [_VP, ctypes.c_int32, ctypes.POINTER(ctypes.c_double)]),
     "muon_plan_matrix_info": (ctypes.c_int, [_VP, ctypes.c_int32, ctypes.POINTER(muon_matrix_info)]),
     "muon_step": (ctypes.c_int, _STEP_ARGS),
     "muon_step_debug": (ctypes.c_int, _STEP_ARGS + [_PP]),

@@ -2,6 +2,7 @@
 // tables, and the per-step launch sequence.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -55,11 +56,12 @@ muon_status check_opts(const muon_plan_opts& o) {
   }
   if (!std::isfinite(o.eps) || o.eps < 0.f) return fail(MUON_ERR_INVALID_ARG, "opts.eps must be finite and >= 0");
   if (o.small_m_threshold < 0) return fail(MUON_ERR_INVALID_ARG, "opts.small_m_threshold must be >= 0");
-  if (o.flags & ~uint32_t(MUON_PLAN_HOST_ONLY)) return fail(MUON_ERR_INVALID_ARG, "opts.flags has unknown bits");
+  if (o.flags & ~uint32_t(MUON_PLAN_HOST_ONLY | MUON_PLAN_CHECK_BUFFERS))
+    return fail(MUON_ERR_INVALID_ARG, "opts.flags has unknown bits");
   if (o.wave_bytes < 0) return fail(MUON_ERR_INVALID_ARG, "opts.wave_bytes must be >= 0");
   if (!std::isfinite(o.gram_min_aspect) || (o.gram_min_aspect != 0.f && o.gram_min_aspect < 1.f))
     return fail(MUON_ERR_INVALID_ARG, "opts.gram_min_aspect must be 0 or a finite value >= 1");
-  if (o.reserved != 0) return fail(MUON_ERR_INVALID_ARG, "opts.reserved must be 0");
+  if (o.gram_restart < 0) return fail(MUON_ERR_INVALID_ARG, "opts.gram_restart must be >= 0");
   return MUON_OK;
 }
 
@@ -88,7 +90,38 @@ muon_status upload_tables(muon::Plan& p) {
   if (e == hipSuccess && !p.h_tiles.empty())
     e = hipMemcpy(p.d_tiles, p.h_tiles.data(), p.h_tiles.size() * sizeof(TileEntry), hipMemcpyHostToDevice);
   if (e != hipSuccess) return hip_fail(e, "upload of plan tables");
+  // the pinned ring the step refreshes the pointer table from
+  e = hipHostMalloc(reinterpret_cast<void**>(&p.h_ring), size_t(Plan::kRing) * p.mats.size() * sizeof(PtrEntry),
+                    hipHostMallocDefault);
+  if (e != hipSuccess) {
+    p.h_ring = nullptr;
+    return e == hipErrorOutOfMemory ? fail(MUON_ERR_OUT_OF_MEMORY, "hipHostMalloc of the pointer ring failed")
+                                    : hip_fail(e, "hipHostMalloc of the pointer ring");
+  }
+  for (int k = 0; k < Plan::kRing; ++k) {
+    hipEvent_t ev = nullptr;
+    e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+    if (e != hipSuccess) return hip_fail(e, "hipEventCreateWithFlags");
+    p.ring_events[k] = ev;
+  }
   return MUON_OK;
+}
+
+// Frees what upload_tables allocated (each part only if it exists).
+hipError_t release_device(muon::Plan& p) {
+  hipError_t first = hipSuccess;
+  auto keep = [&](hipError_t e) {
+    if (first == hipSuccess) first = e;
+  };
+  for (int k = 0; k < muon::Plan::kRing; ++k) {
+    if (p.ring_events[k]) keep(hipEventDestroy(hipEvent_t(p.ring_events[k])));
+    p.ring_events[k] = nullptr;
+  }
+  if (p.h_ring) keep(hipHostFree(p.h_ring));
+  p.h_ring = nullptr;
+  if (p.d_block) keep(hipFree(p.d_block));
+  p.d_block = nullptr;
+  return first;
 }
 
 bool aligned(const void* ptr, uintptr_t a) { return (reinterpret_cast<uintptr_t>(ptr) & (a - 1)) == 0; }
@@ -126,10 +159,11 @@ muon_status check_memory(const void* ptr, size_t bytes, int device, const std::s
   return MUON_OK;
 }
 
-// The buffer checks of a step: non-NULL, aligned, the workspace large
-// enough, the current device the plan's; with `memory`, also where each
-// buffer lives (check_memory) -- muon_step does that whenever its buffer
-// addresses change.
+// The buffer checks of a step: non-NULL (a NULL gradient skips its matrix),
+// aligned, the workspace large enough, the current device the plan's; with
+// `memory`, also where each buffer lives (check_memory) -- muon_check_buffers
+// always, muon_step when its buffer addresses change on a plan created with
+// MUON_PLAN_CHECK_BUFFERS.
 muon_status check_buffers(const muon::Plan& p, void* const* params, const void* const* grads,
                           void* const* momentum, const void* workspace, size_t workspace_bytes,
                           float* const* update_out, bool memory) {
@@ -141,8 +175,8 @@ muon_status check_buffers(const muon::Plan& p, void* const* params, const void* 
                 "workspace has " + std::to_string(workspace_bytes) + " bytes, plan needs " + std::to_string(p.ws_bytes));
   const size_t n = p.mats.size();
   for (size_t i = 0; i < n; ++i) {
-    if (!params[i] || !grads[i] || !momentum[i])
-      return fail(MUON_ERR_INVALID_ARG, "NULL buffer pointer for matrix " + std::to_string(i));
+    if (!params[i] || !momentum[i])
+      return fail(MUON_ERR_INVALID_ARG, "NULL param or momentum pointer for matrix " + std::to_string(i));
     if (!aligned(params[i], 16) || !aligned(grads[i], 16) || !aligned(momentum[i], 16) ||
         (update_out && update_out[i] && !aligned(update_out[i], 16)))
       return fail(MUON_ERR_INVALID_ARG, "buffers of matrix " + std::to_string(i) + " must be 16-byte aligned");
@@ -160,7 +194,8 @@ muon_status check_buffers(const muon::Plan& p, void* const* params, const void* 
     const size_t el = size_t(h.rows) * size_t(h.cols);
     const std::string at = "matrix " + std::to_string(i) + " ";
     st = check_memory(params[i], el * (h.param_dtype == MUON_BF16 ? 2 : 4), dev, at + "param");
-    if (st == MUON_OK) st = check_memory(grads[i], el * (h.grad_dtype == MUON_BF16 ? 2 : 4), dev, at + "grad");
+    if (st == MUON_OK && grads[i])
+      st = check_memory(grads[i], el * (h.grad_dtype == MUON_BF16 ? 2 : 4), dev, at + "grad");
     if (st == MUON_OK) st = check_memory(momentum[i], el * 4, dev, at + "momentum");
     if (st == MUON_OK && update_out && update_out[i]) st = check_memory(update_out[i], el * 4, dev, at + "update_out");
   }
@@ -183,33 +218,58 @@ muon_status step_impl(muon_plan plan, void* const* params, const void* const* gr
   muon_status st = check_buffers(p, params, grads, momentum, workspace, workspace_bytes, update_out, false);
   if (st != MUON_OK) return st;
   const size_t n = p.mats.size();
+  const bool timing = p.timing;
 
-  // Refresh the device pointer table if the caller's buffers moved; buffers
-  // are vetted where they live whenever their addresses change.
+  // Refresh the device pointer table if the caller's buffers moved: the new
+  // table goes into the next slot of the plan's pinned ring and is copied on
+  // the caller's stream, ahead of the step's kernels.  The host waits only if
+  // that slot's previous copy (kRing refreshes ago) has not run yet.  The
+  // workspace's memory is vetted when it changes (two HIP queries); the other
+  // buffers' only on plans created with MUON_PLAN_CHECK_BUFFERS.
   bool changed = !p.ptrs_valid;
   for (size_t i = 0; i < n && !changed; ++i) {
     const PtrEntry& h = p.h_ptrs[i];
     float* out = update_out ? update_out[i] : nullptr;
     changed = h.param != params[i] || h.grad != grads[i] || h.mom != momentum[i] || h.out != out;
   }
-  if (changed || workspace != p.ws_checked) {
+  if (changed && (p.opts.flags & MUON_PLAN_CHECK_BUFFERS)) {
     st = check_buffers(p, params, grads, momentum, workspace, workspace_bytes, update_out, true);
     if (st != MUON_OK) return st;
     p.ws_checked = workspace;
   }
+  if (workspace != p.ws_checked) {
+    st = check_memory(workspace, size_t(p.ws_bytes), p.device, "the workspace");
+    if (st != MUON_OK) return st;
+    p.ws_checked = workspace;
+  }
   hipError_t e = hipSuccess;
+  hipStream_t hs = hipStream_t(stream);
   if (changed) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(hs, &cs) != hipSuccess) {
+      (void)hipGetLastError();
+      cs = hipStreamCaptureStatusNone;
+    }
+    if (cs != hipStreamCaptureStatusNone)
+      return fail(MUON_ERR_INVALID_ARG,
+                  "buffer addresses differ from the previous step's while the stream is being captured; "
+                  "step once on these buffers before the capture");
+    const int k = p.ring_next;
+    if (p.ring_busy[k]) {
+      e = hipEventSynchronize(hipEvent_t(p.ring_events[k]));
+      if (e != hipSuccess) return hip_fail(e, "waiting for a pointer-ring slot");
+    }
+    PtrEntry* slot = p.h_ring + size_t(k) * n;
     for (size_t i = 0; i < n; ++i) {
-      p.h_ptrs[i].param = params[i];
-      p.h_ptrs[i].grad = grads[i];
-      p.h_ptrs[i].mom = static_cast<float*>(momentum[i]);
-      p.h_ptrs[i].out = update_out ? update_out[i] : nullptr;
+      slot[i] = PtrEntry{params[i], grads[i], static_cast<float*>(momentum[i]), update_out ? update_out[i] : nullptr};
+      p.h_ptrs[i] = slot[i];
     }
     p.ptrs_valid = false;
-    e = hipMemcpyAsync(p.d_ptrs, p.h_ptrs.data(), n * sizeof(PtrEntry), hipMemcpyHostToDevice,
-                       hipStream_t(stream));
-    if (e == hipSuccess) e = hipStreamSynchronize(hipStream_t(stream));
+    e = hipMemcpyAsync(p.d_ptrs, slot, n * sizeof(PtrEntry), hipMemcpyHostToDevice, hs);
+    if (e == hipSuccess) e = hipEventRecord(hipEvent_t(p.ring_events[k]), hs);
     if (e != hipSuccess) return hip_fail(e, "upload of buffer pointers");
+    p.ring_busy[k] = true;
+    p.ring_next = (k + 1) % Plan::kRing;
     p.ptrs_valid = true;
   }
 
@@ -222,11 +282,10 @@ muon_status step_impl(muon_plan plan, void* const* params, const void* const* gr
   s.nesterov = nesterov;
   s.ns_steps = ns_steps;
   char* ws = static_cast<char*>(workspace);
-  hipStream_t hs = hipStream_t(stream);
   // Runs one launch, bracketed by timing events when timing is enabled.
   auto run = [&](int32_t kind, int32_t kclass, double flops, double bytes, auto&& launch) -> hipError_t {
     size_t ev = 0;
-    if (p.timing) {
+    if (timing) {
       ev = p.records.size() * 2;
       while (p.events.size() < ev + 2) {
         hipEvent_t e;
@@ -241,7 +300,7 @@ muon_status step_impl(muon_plan plan, void* const* params, const void* const* gr
       hipError_t er = hipGetLastError();
       return er == hipSuccess ? hipErrorLaunchFailure : er;
     }
-    if (p.timing) {
+    if (timing) {
       hipError_t er = hipEventRecord(hipEvent_t(p.events[ev + 1]), hs);
       if (er != hipSuccess) return er;
       p.records.push_back(TimingRecord{kind, kclass, flops, bytes, ev});
@@ -283,39 +342,48 @@ muon_status step_impl(muon_plan plan, void* const* params, const void* const* gr
         if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
       }
     }
-    // Gram space (Eq. 4): G0 = s^2 X0 X0^T; per step P_i = a_i I + b_i G +
-    // c_i G^2 (as c_i (G G + b_i/c_i G + a_i/c_i I); the plan takes this form
-    // only when no c_i is 0); Q_{i+1} = P_i Q_i (Q_1 = P_0, which is
-    // written straight into Q0); R = G P_i and G <- P_i R except after the
-    // last step; finally O = s Q_k X0.  P Q and G P only need P_i, so they
-    // share one launch.
+    // Gram space (Eq. 4), in segments of at most gram_restart steps.  A
+    // segment starting from X (X0 = s u in the first) forms G = X X^T; per
+    // step P_i = a_i I + b_i G + c_i G^2 (as c_i (G G + b_i/c_i G + a_i/c_i
+    // I); the plan takes this form only when no c_i is 0); Q_{i+1} = P_i Q_i
+    // (the segment's first P is written straight into Q0); R = G P_i and
+    // G <- P_i R except after the segment's last step; then X <- Q X, which
+    // after the last segment is O and goes into the update.  P Q and G P
+    // only need P_i, so they share one launch.
     for (const ClassLaunch& cl : w.launches) {
-      if (!cl.gram || ns_steps == 0) continue;
-      e = gemm(cl, ST_GRAM, MUON_KERNEL_GRAM, GemmStep{1, 0, 0, SQ_A, SQ_A, SQ_A, 0.f, 0.f, 1.f});
-      if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
-      for (int32_t it = 0; it < ns_steps; ++it) {
-        const int32_t pbuf = it == 0 ? SQ_Q0 : SQ_B;
-        const float a = p.abc[size_t(3 * it)], b = p.abc[size_t(3 * it + 1)], c = p.abc[size_t(3 * it + 2)];
-        e = gemm(cl, ST_POLY, MUON_KERNEL_POLY, GemmStep{0, 0, 0, SQ_A, SQ_A, pbuf, b / c, a / c, c});
-        const GemmStep qu{0, 0, 0, SQ_B, (it - 1) & 1 ? SQ_Q1 : SQ_Q0, it & 1 ? SQ_Q1 : SQ_Q0, 0.f, 0.f, 1.f};
-        GemmStep gr{0, 0, 0, SQ_A, pbuf, SQ_R, 0.f, 0.f, 1.f};
-        const bool need_qu = it > 0, need_gr = it + 1 < ns_steps;
-        if (e == hipSuccess && need_qu && need_gr) {
-          gr.pair = 1;
-          gr.l2 = qu.l;
-          gr.r2 = qu.r;
-          gr.out2 = qu.out;
-          e = gemm(cl, ST_SYM, MUON_KERNEL_SYMM, gr);
-        } else if (e == hipSuccess && (need_qu || need_gr)) {
-          e = gemm(cl, ST_SYM, MUON_KERNEL_SYMM, need_qu ? qu : gr);
-        }
-        if (e == hipSuccess && need_gr)
-          e = gemm(cl, ST_SYM, MUON_KERNEL_SYMM, GemmStep{0, 0, 0, pbuf, SQ_R, SQ_A, 0.f, 0.f, 1.f});
+      if (!cl.gram) continue;
+      int32_t pin = 0;
+      for (int32_t s0 = 0; s0 < ns_steps; s0 += p.gram_restart) {
+        const int32_t len = std::min(p.gram_restart, ns_steps - s0);
+        const int32_t first = s0 == 0, last = s0 + len == ns_steps;
+        e = gemm(cl, ST_GRAM, MUON_KERNEL_GRAM, GemmStep{first, pin, 0, SQ_A, SQ_A, SQ_A, 0.f, 0.f, 1.f});
         if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
+        for (int32_t j = 0; j < len; ++j) {
+          const int32_t it = s0 + j;
+          const int32_t pbuf = j == 0 ? SQ_Q0 : SQ_B;
+          const float a = p.abc[size_t(3 * it)], b = p.abc[size_t(3 * it + 1)], c = p.abc[size_t(3 * it + 2)];
+          e = gemm(cl, ST_POLY, MUON_KERNEL_POLY, GemmStep{0, 0, 0, SQ_A, SQ_A, pbuf, b / c, a / c, c});
+          const GemmStep qu{0, 0, 0, SQ_B, (j - 1) & 1 ? SQ_Q1 : SQ_Q0, j & 1 ? SQ_Q1 : SQ_Q0, 0.f, 0.f, 1.f};
+          GemmStep gr{0, 0, 0, SQ_A, pbuf, SQ_R, 0.f, 0.f, 1.f};
+          const bool need_qu = j > 0, need_gr = j + 1 < len;
+          if (e == hipSuccess && need_qu && need_gr) {
+            gr.pair = 1;
+            gr.l2 = qu.l;
+            gr.r2 = qu.r;
+            gr.out2 = qu.out;
+            e = gemm(cl, ST_SYM, MUON_KERNEL_SYMM, gr);
+          } else if (e == hipSuccess && (need_qu || need_gr)) {
+            e = gemm(cl, ST_SYM, MUON_KERNEL_SYMM, need_qu ? qu : gr);
+          }
+          if (e == hipSuccess && need_gr)
+            e = gemm(cl, ST_SYM, MUON_KERNEL_SYMM, GemmStep{0, 0, 0, pbuf, SQ_R, SQ_A, 0.f, 0.f, 1.f});
+          if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
+        }
+        const int32_t qk = (len - 1) & 1 ? SQ_Q1 : SQ_Q0;
+        e = gemm(cl, ST_BX, MUON_KERNEL_BX, GemmStep{first, pin, last, qk, qk, qk, 0.f, 0.f, 1.f});
+        if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
+        pin ^= 1;
       }
-      const int32_t qk = (ns_steps - 1) & 1 ? SQ_Q1 : SQ_Q0;
-      e = gemm(cl, ST_BX, MUON_KERNEL_BX, GemmStep{1, 0, 1, qk, qk, qk, 0.f, 0.f, 1.f});
-      if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
     }
     // With k >= 1 the last B*X launch applied the update (zero-gradient
     // matrices included); with k = 0 the update is O = s*u.
@@ -366,7 +434,7 @@ muon_status muon_plan_opts_default(muon_plan_opts* o) {
   o->flags = 0;
   o->wave_bytes = 0;
   o->gram_min_aspect = 2.f;
-  o->reserved = 0;
+  o->gram_restart = 0;
   o->abc_per_step = nullptr;
   return ok();
 }
@@ -417,7 +485,7 @@ muon_status muon_plan_create(const muon_matrix_desc* mats, int32_t n, const muon
     st = upload_tables(plan->p);
     if (st != MUON_OK) {
       const std::string msg = g_last_error;
-      if (plan->p.d_block) (void)hipFree(plan->p.d_block);
+      (void)release_device(plan->p);
       delete plan;
       return fail(st, msg);
     }
@@ -430,10 +498,8 @@ muon_status muon_plan_destroy(muon_plan plan) {
   if (!plan) return ok();
   muon_status st = MUON_OK;
   release_events(plan->p);
-  if (plan->p.d_block) {
-    hipError_t e = hipFree(plan->p.d_block);
-    if (e != hipSuccess) st = hip_fail(e, "hipFree of plan tables");
-  }
+  const hipError_t e = release_device(plan->p);
+  if (e != hipSuccess) st = hip_fail(e, "releasing the plan's device tables");
   delete plan;
   return st == MUON_OK ? ok() : st;
 }
@@ -456,9 +522,16 @@ muon_status muon_plan_get_info(muon_plan plan, muon_plan_info* info) {
   info->launches_per_step = muon::launches_per_step(p, p.opts.max_ns_steps);
   info->ns_flops_per_ns_step = p.ns_flops;
   info->padded_flops_per_ns_step = p.padded_flops;
-  info->ns_flops_fixed = p.ns_flops_fixed;
-  info->ns_flops_step = p.ns_flops_step;
   info->n_gram = p.n_gram;
+  info->gram_restart = p.gram_restart;
+  return ok();
+}
+
+muon_status muon_plan_ns_flops(muon_plan plan, int32_t ns_steps, double* flops) {
+  if (!plan || !flops) return fail(MUON_ERR_INVALID_ARG, "plan and flops must be non-NULL");
+  if (ns_steps < 0 || ns_steps > plan->p.opts.max_ns_steps)
+    return fail(MUON_ERR_INVALID_ARG, "ns_steps must be in [0, max_ns_steps]");
+  *flops = muon::plan_ns_flops(plan->p, ns_steps);
   return ok();
 }
 

@@ -6,7 +6,9 @@
 //                   matrix); the fp32 classes also keep X^T.
 //  finalize_kernel  per matrix, a fixed-order sum of the tile partials and the
 //                   Frobenius scale 1 / (||u||_F + eps) (deterministic; no
-//                   float atomics).  A zero sum marks the matrix as skipped.
+//                   float atomics).  A zero sum marks the matrix's products
+//                   as skipped (O = 0); a NULL gradient marks the whole
+//                   matrix as skipped for this step.
 //  apply_kernel     W <- W*(1 - lr*wd) - lr*sqrt(max(1, rows/cols))*O  (Eq. 1
 //                   with decoupled weight decay), rounded to the param dtype,
 //                   for k = 0 (O = s*u); otherwise the last B*X launch applies
@@ -64,6 +66,10 @@ __global__ __launch_bounds__(256) void momentum_kernel(const MatDev* __restrict_
   const int tr = local / d.ew_tiles_c, tc = local - tr * d.ew_tiles_c;
   const PtrEntry pe = ptrs[d.index];
   const int t = threadIdx.x;
+  if (!pe.grad) {  // no gradient this step: M and X are left alone
+    if (t == 0) reinterpret_cast<float*>(ws + d.partial_off)[local] = 0.f;
+    return;
+  }
   const int cg = t & 15, rr = t >> 4;
   const int r0 = tr * EW_TILE, c0 = tc * EW_TILE;
   const int rows = d.rows, cols = d.cols;
@@ -123,7 +129,8 @@ __global__ __launch_bounds__(256) void momentum_kernel(const MatDev* __restrict_
 }
 
 __global__ __launch_bounds__(256) void finalize_kernel(const MatDev* __restrict__ mats,
-                                                       const int32_t* __restrict__ prefix, char* __restrict__ ws,
+                                                       const int32_t* __restrict__ prefix,
+                                                       const PtrEntry* __restrict__ ptrs, char* __restrict__ ws,
                                                        float* __restrict__ scale, int32_t* __restrict__ flag,
                                                        float eps) {
   __shared__ double red[4];
@@ -140,7 +147,7 @@ __global__ __launch_bounds__(256) void finalize_kernel(const MatDev* __restrict_
   if (threadIdx.x == 0) {
     const double sum = (red[0] + red[1]) + (red[2] + red[3]);
     scale[s] = float(1.0 / (sqrt(sum) + double(eps)));
-    flag[s] = sum == 0.0 ? 1 : 0;
+    flag[s] = !ptrs[d.index].grad ? FLAG_SKIP : sum == 0.0 ? FLAG_ZERO : FLAG_LIVE;
   }
 }
 
@@ -161,7 +168,8 @@ __global__ __launch_bounds__(256) void apply_kernel(const MatDev* __restrict__ m
   const int cg = t & 15, rr = t >> 4;
   const int rows = d.rows, cols = d.cols;
   const bool vec = (cols & 3) == 0;
-  const bool zero = flag[s] != 0;
+  if (flag[s] == FLAG_SKIP) return;
+  const bool zero = flag[s] != FLAG_LIVE;
   const float sc = scale[s];
   const float lrs = update_lr(lr, rows, cols);
   // u is read from X (transposed for a tall 16-bit matrix, whose
@@ -215,7 +223,7 @@ int launch_momentum(const Plan& p, const WaveHost& w, char* ws, const StepScalar
 
 int launch_finalize(const Plan& p, const WaveHost& w, char* ws, const StepScalars& s, void* stream) {
   hipLaunchKernelGGL(finalize_kernel, dim3(unsigned(w.count)), dim3(256), 0, hipStream_t(stream),
-                     p.d_mats + w.first, p.d_prefix + w.prefix_off, ws,
+                     p.d_mats + w.first, p.d_prefix + w.prefix_off, p.d_ptrs, ws,
                      reinterpret_cast<float*>(ws + w.scale_off), reinterpret_cast<int32_t*>(ws + w.flag_off), s.eps);
   return check_launch();
 }

@@ -76,10 +76,16 @@ struct TileEntry {
 // Per-matrix device pointers, refreshed when the caller's buffers change.
 struct PtrEntry {
   void* param;
-  const void* grad;
+  const void* grad;  // null: the matrix is skipped this step (W and M unchanged)
   float* mom;
-  float* out;    // debug output of O, may be null
+  float* out;        // debug output of O, may be null
 };
+
+// Per-matrix state flag written by the finalize kernel: the NS products run
+// (LIVE), are skipped because the NS input is all zero (ZERO: O = 0, the
+// weight decay is still applied), or the matrix has no gradient this step
+// and is left untouched (SKIP).
+enum MatFlag : int32_t { FLAG_LIVE = 0, FLAG_ZERO = 1, FLAG_SKIP = 2 };
 
 struct MatHost {
   int64_t rows, cols, m, n;
@@ -135,9 +141,12 @@ struct Plan {
   std::vector<int32_t> h_prefix;
   std::vector<TileEntry> h_tiles;
   int32_t n_buckets = 0, n_gram = 0;
+  int32_t gram_restart = 2;         // NS steps per Gram-space segment
   int64_t ws_bytes = 0;
   double ns_flops = 0, padded_flops = 0;     // per NS step of Eq. 2 over all matrices
-  double ns_flops_fixed = 0, ns_flops_step = 0;  // the plan's own: fixed + k * step
+  // the plan's own algorithmic flops (plan_ns_flops): sum of 3 m^2 n + m^3
+  // over Eq. 2 matrices, of 3 m^2 n and of m^3 over Gram-space ones
+  double flops_eq2 = 0, flops_gram_mn = 0, flops_gram_m3 = 0;
 
   // device side
   int32_t device = -1;
@@ -149,6 +158,14 @@ struct Plan {
   std::vector<PtrEntry> h_ptrs;     // host shadow of d_ptrs
   bool ptrs_valid = false;
   const void* ws_checked = nullptr;  // workspace whose memory was last vetted
+  // Pinned host ring of pointer tables: a step whose buffers moved fills the
+  // next slot and copies it to d_ptrs on the caller's stream; the slot's
+  // event marks when that copy has read it.
+  static constexpr int kRing = 8;
+  PtrEntry* h_ring = nullptr;       // kRing * n entries (hipHostMalloc)
+  void* ring_events[kRing] = {};
+  bool ring_busy[kRing] = {};
+  int ring_next = 0;
 
   // launch timing (muon_plan_set_timing)
   bool timing = false;
@@ -160,6 +177,11 @@ struct Plan {
 muon_status build_plan(const muon_matrix_desc* mats, int32_t n, const muon_plan_opts& o, Plan& p,
                        std::string& err);
 int64_t launches_per_step(const Plan& p, int32_t ns_steps);
+double plan_ns_flops(const Plan& p, int32_t ns_steps);
+// Gram-space matrices advance in segments of at most gram_restart steps: a
+// fresh Gram product, the segment's polynomials and products, and X = Q X
+// (the update itself after the last segment).
+constexpr int32_t kGramMinM = 256;   // smaller m stays on Eq. 2
 
 // Per-launch arguments shared by the kernel launchers.
 struct StepScalars {

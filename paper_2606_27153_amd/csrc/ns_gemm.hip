@@ -735,10 +735,12 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
   const TileEntry te = args.tiles[second ? int(blockIdx.x) - args.split : int(blockIdx.x)];
   const int32_t bl = second ? args.l2 : args.l, br = second ? args.r2 : args.r, bo = second ? args.out2 : args.out;
   const MatDev& d = args.mats[te.mat];
-  // An all-zero gradient has O = 0: its products are skipped, and the last
-  // B*X only applies the weight decay.
-  const bool zero = args.flag[d.slot] != 0;
-  if (zero && !(STAGE == ST_BX && args.last)) return;
+  // An all-zero NS input has O = 0: its products are skipped, and the last
+  // B*X only applies the weight decay.  A matrix without a gradient this
+  // step is not touched at all.
+  const int32_t mflag = args.flag[d.slot];
+  const bool zero = mflag != FLAG_LIVE;
+  if (mflag == FLAG_SKIP || (zero && !(STAGE == ST_BX && args.last))) return;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
@@ -882,8 +884,39 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
         ob[ks] = frag_off(wn * C::WTN, lane, ks);
       }
       typename Frag<E>::T fa0[C::NBM], fb0[C::NBN], fa1[C::NBM], fb1[C::NBN];
-      auto kloop = [&](auto masked) {
+      // fp32 operands: each slab's products are summed into a zeroed partial
+      // accumulator, which is added to acc after the slab.  This two-level
+      // sum keeps the rounding error of long K loops (K = n up to 14336 for
+      // the Gram product) near sqrt(K / 32) + sqrt(32) roundings instead of
+      // sqrt(K / 2), the chain of one accumulator through every
+      // 32x32x2 step.  The 16-bit classes accumulate directly.
+      f32x16 part[C::NBM][C::NBN];
+      if constexpr (sizeof(E) == 4) {
+#pragma unroll
+        for (int i = 0; i < C::NBM; ++i)
+#pragma unroll
+          for (int j = 0; j < C::NBN; ++j)
+#pragma unroll
+            for (int q = 0; q < 16; ++q) part[i][j][q] = 0.f;
+      }
+      auto body = [&](const char* st, auto masked) {
         constexpr bool M = decltype(masked)::value;
+        if constexpr (sizeof(E) == 4) {
+          slab_body<C, E, M>(st, oa, ob, fa0, fb0, fa1, fb1, part, bmask);
+#pragma unroll
+          for (int i = 0; i < C::NBM; ++i)
+#pragma unroll
+            for (int j = 0; j < C::NBN; ++j)
+#pragma unroll
+              for (int q = 0; q < 16; ++q) {
+                acc[i][j][q] += part[i][j][q];
+                part[i][j][q] = 0.f;
+              }
+        } else {
+          slab_body<C, E, M>(st, oa, ob, fa0, fb0, fa1, fb1, acc, bmask);
+        }
+      };
+      auto kloop = [&](auto masked) {
         load_slab<C>(srca, K, 0, stage0, wid);
         load_slab<C>(srcb, K, 0, stage0 + C::OPB, wid);
         wait_vm_all();
@@ -893,7 +926,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
         for (; kt + 2 <= nk; kt += 2) {
           load_slab<C>(srca, K, kt + 1, stage1, wid);
           load_slab<C>(srcb, K, kt + 1, stage1 + C::OPB, wid);
-          if (live) slab_body<C, E, M>(stage0, oa, ob, fa0, fb0, fa1, fb1, acc, bmask);
+          if (live) body(stage0, masked);
           if (FUSE && live) fuse_input<C, E, false>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
           wait_vm_all();
           __syncthreads();
@@ -903,7 +936,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
             load_slab<C>(srca, K, kt + 2, stage0, wid);
             load_slab<C>(srcb, K, kt + 2, stage0 + C::OPB, wid);
           }
-          if (live) slab_body<C, E, M>(stage1, oa, ob, fa0, fb0, fa1, fb1, acc, bmask);
+          if (live) body(stage1, masked);
           if (FUSE && live) fuse_input<C, E, false>(stage1 + C::OPB, kt + 1, frow0, wn, lane, fcoef, acc);
           wait_vm_all();
           __syncthreads();
@@ -911,7 +944,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
           __builtin_amdgcn_sched_barrier(0);
         }
         if (kt < nk) {  // odd slab count: the last slab is in stage 0
-          if (live) slab_body<C, E, M>(stage0, oa, ob, fa0, fb0, fa1, fb1, acc, bmask);
+          if (live) body(stage0, masked);
           if (FUSE && live) fuse_input<C, E, false>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
           __syncthreads();
         }

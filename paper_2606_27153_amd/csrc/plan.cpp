@@ -159,19 +159,31 @@ void interleave_units(std::vector<TileEntry>& out, const std::vector<std::vector
 const ClassInfo& class_info(int32_t kc) { return kClasses[kc]; }
 
 int64_t launches_per_step(const Plan& p, int32_t ns_steps) {
-  // Eq. 2: Gram, A*A and B*X per step.  Gram space: the Gram product and
-  // B*X once, P_i per step, P Q and G P (one launch when both are due) and
-  // P (G P) on all but one step: 3k + 1 launches for k >= 2.
-  // A cubic step (c = 0) of Eq. 2 has no A*A launch.
+  // Eq. 2: Gram, A*A and B*X per step.  Gram space, per segment of L steps:
+  // the Gram product and B*X once, P_i per step, P Q and G P (one launch
+  // when both are due) and P (G P) on all but the last step: 3L + 1
+  // launches, 3 for L = 1.  A cubic step (c = 0) of Eq. 2 has no A*A launch.
   int64_t n = 0;
   const int64_t k = ns_steps;
-  int64_t eq2 = 0;
+  int64_t eq2 = 0, gram = 0;
   for (int32_t it = 0; it < ns_steps; ++it) eq2 += p.abc[size_t(3 * it + 2)] != 0.f ? 3 : 2;
+  for (int64_t s0 = 0; s0 < k; s0 += p.gram_restart) {
+    const int64_t len = std::min<int64_t>(p.gram_restart, k - s0);
+    gram += len > 1 ? 3 * len + 1 : 3;
+  }
   for (const auto& w : p.waves) {
     n += k > 0 ? 2 : 3;  // momentum, finalize (and apply when no NS step runs)
-    for (const auto& cl : w.launches) n += cl.gram ? (k > 1 ? 3 * k + 1 : 3 * k) : eq2;
+    for (const auto& cl : w.launches) n += cl.gram ? gram : eq2;
   }
   return n;
+}
+
+double plan_ns_flops(const Plan& p, int32_t ns_steps) {
+  // a segment of L steps: 3 m^2 n and (4L - 3) m^3; summed over segments,
+  // 3 m^2 n per segment and 4k - 3 * segments times m^3
+  const double k = ns_steps;
+  const double segs = double((ns_steps + p.gram_restart - 1) / p.gram_restart);
+  return k * p.flops_eq2 + segs * p.flops_gram_mn + (4.0 * k - 3.0 * segs) * p.flops_gram_m3;
 }
 
 muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan_opts& o, Plan& p,
@@ -185,6 +197,7 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
       p.abc[size_t(3 * i + j)] = o.abc_per_step ? o.abc_per_step[3 * i + j] : (j == 0 ? o.a : j == 1 ? o.b : o.c);
     p.quintic_every_step = p.quintic_every_step && p.abc[size_t(3 * i + 2)] != 0.f;
   }
+  p.gram_restart = o.gram_restart > 0 ? o.gram_restart : 2;
   p.mats.resize(size_t(n));
   std::map<std::tuple<int32_t, int64_t, int64_t>, int32_t> buckets;
 
@@ -208,9 +221,10 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
     const ClassInfo& ci = kClasses[h.kclass];
     h.fp32_ns = ci.fp32;
     // Gram space (Eq. 4) pays off whenever n > m; nearly square matrices stay
-    // on Eq. 2, where bf16 rounding in the m x m chain costs more accuracy
-    // (the Gram matrix squares their conditioning).
-    h.gram = !ci.fp32 && o.gram_min_aspect > 0.f && p.quintic_every_step &&
+    // on Eq. 2, where 16-bit rounding in the m x m chain costs more accuracy
+    // (the Gram matrix squares their conditioning), and so do small ones,
+    // whose products are latency-bound anyway.
+    h.gram = !ci.fp32 && o.gram_min_aspect > 0.f && p.quintic_every_step && h.m >= kGramMinM &&
                      double(h.n) >= double(o.gram_min_aspect) * double(h.m)
                  ? 1
                  : 0;
@@ -238,10 +252,10 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
     };
     // X in both layouts for the fp32 classes; the bf16 classes read X^T
     // straight from X with LDS transposing reads and keep X only.  The
-    // Gram-space form reads X0 alone (no ping-pong) and keeps five square
-    // buffers instead of two.
+    // Gram-space form needs the ping-pong pair only when it restarts, and
+    // keeps five square buffers instead of two.
     for (int pp = 0; pp < 2; ++pp) {
-      const bool need = pp == 0 || !h.gram;
+      const bool need = pp == 0 || !h.gram || p.gram_restart < o.max_ns_steps;
       h.x_off[pp] = need ? take(h.m_pad * h.n_pad * esz) : -1;
       h.xt_off[pp] = need && ci.fp32 ? take(h.m_pad * h.n_pad * esz) : -1;
     }
@@ -252,10 +266,10 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
     const double m = double(h.m), nn = double(h.n);
     p.ns_flops += 3.0 * m * m * nn + m * m * m;
     if (h.gram) {
-      p.ns_flops_fixed += 3.0 * m * m * nn - 3.0 * m * m * m;
-      p.ns_flops_step += 4.0 * m * m * m;
+      p.flops_gram_mn += 3.0 * m * m * nn;
+      p.flops_gram_m3 += m * m * m;
     } else {
-      p.ns_flops_step += 3.0 * m * m * nn + m * m * m;
+      p.flops_eq2 += 3.0 * m * m * nn + m * m * m;
     }
   }
   p.n_buckets = int32_t(buckets.size());

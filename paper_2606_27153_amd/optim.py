@@ -15,7 +15,7 @@ from . import _lib as L
 
 _DT = {"f32": L.MUON_F32, "bf16": L.MUON_BF16}
 # NS arithmetic: bf16 (the default), fp16 (the paper's implementation
-# choice, Sec. 5) or fp32 (validation)
+# choice, Sec. 4) or fp32 (validation)
 PRECISIONS = {"bf16": L.MUON_NS_BF16, "fp32": L.MUON_NS_FP32, "fp16": L.MUON_NS_FP16}
 
 
@@ -33,24 +33,29 @@ def default_gram_min_aspect(precision: str) -> float:
 
 
 def check_step_tensors(descs: Sequence, params: List, grads: List, moms: List, workspace=None,
-                       update_out: Optional[List] = None) -> None:
+                       update_out: Optional[List] = None, only: Optional[Sequence[int]] = None) -> None:
     """Raises ValueError unless every buffer matches what the C ABI assumes of
     it: matrix i's param, grad and momentum are contiguous (row-major,
     leading dimension cols) tensors of descs[i]'s shape and dtypes (momentum
     fp32), all on one GPU, like the workspace and any update_out buffer (fp32).
-    The library itself only sees pointers and cannot tell."""
+    A grad may be None (the matrix is skipped for the step).  ``only``
+    restricts the per-matrix checks to those indices.  The library itself
+    only sees pointers and cannot tell."""
     n = len(descs)
     if not (len(params) == len(grads) == len(moms) == n):
         raise ValueError(f"expected {n} params, grads and momentum buffers")
     if update_out is not None and len(update_out) != n:
         raise ValueError(f"expected {n} update_out entries (None for no output)")
     checked = []
-    for i, d in enumerate(descs):
+    for i in (range(n) if only is None else only):
+        d = descs[i]
         rows, cols, pd, gd = d[:4]
         shape = (int(rows), int(cols))
         pc = _DT[pd] if isinstance(pd, str) else int(pd)
         gc = _DT[gd] if isinstance(gd, str) else int(gd)
-        todo = [(params[i], "param", pc), (grads[i], "grad", gc), (moms[i], "momentum", L.MUON_F32)]
+        todo = [(params[i], "param", pc), (moms[i], "momentum", L.MUON_F32)]
+        if grads[i] is not None:
+            todo.insert(1, (grads[i], "grad", gc))
         if update_out is not None and update_out[i] is not None:
             todo.append((update_out[i], "update_out", L.MUON_F32))
         for t, name, code in todo:
@@ -63,7 +68,7 @@ def check_step_tensors(descs: Sequence, params: List, grads: List, moms: List, w
             if not t.is_contiguous():
                 raise ValueError(f"{what} is not contiguous (the library reads row-major rows of cols elements)")
             checked.append((t, what))
-    device = None
+    device = params[0].device if n else None
     for t, what in checked:
         if not t.is_cuda:
             raise ValueError(f"{what} is not on a GPU")
@@ -94,15 +99,20 @@ class MuonPlan:
     Gram-space recurrence (Eq. 4); 0 keeps every matrix on Eq. 2; None takes
     ``default_gram_min_aspect(precision)`` (2 for bf16, 1.4 for fp16).  ``abc`` is
     one (a, b, c) for every NS step or a list with one triple per step (the
-    per-step coefficient sets of Sec. 5); a list sets max_ns_steps to its
+    per-step coefficient sets of Sec. 4); a list sets max_ns_steps to its
     length.  ``autotune`` picks each shape's GEMM tile by measurement on
     the GPU (see autotune.py), reading and filling the on-disk cache.
+    ``check_buffers`` makes the library vet where the buffers of a step live
+    whenever their addresses change (MUON_PLAN_CHECK_BUFFERS).
+    ``gram_restart`` is the number of NS steps per Gram-space segment (0:
+    the library's default of 2).
     """
 
     def __init__(self, descs: Sequence, *, precision: str = "bf16", max_ns_steps: int = 16,
                  abc: Optional[Sequence[float]] = None, eps: float = 1e-7,
                  small_m_threshold: int = 64, wave_bytes: int = 0, gram_min_aspect: Optional[float] = None,
-                 host_only: bool = False, autotune: bool = False, tune_cache: Optional[str] = None,
+                 host_only: bool = False, check_buffers: bool = False, autotune: bool = False,
+                 tune_cache: Optional[str] = None, gram_restart: int = 0,
                  tune_ns_steps: int = 5):
         lib = L.load()
         n = len(descs)
@@ -147,7 +157,8 @@ class MuonPlan:
         opts.small_m_threshold = int(small_m_threshold)
         opts.wave_bytes = int(wave_bytes)
         opts.gram_min_aspect = float(gram_min_aspect)
-        opts.flags = L.MUON_PLAN_HOST_ONLY if host_only else 0
+        opts.gram_restart = int(gram_restart)
+        opts.flags = (L.MUON_PLAN_HOST_ONLY if host_only else 0) | (L.MUON_PLAN_CHECK_BUFFERS if check_buffers else 0)
         h = ctypes.c_void_p()
         L.check(lib.muon_plan_create(arr, n, ctypes.byref(opts), ctypes.byref(h)))
         self._h = h
@@ -155,7 +166,7 @@ class MuonPlan:
         self.descs = list(descs)
         self.precision = precision
         self._workspace = None
-        self._checked = None
+        self._checked = None     # buffer addresses of the last checked call
 
     # ------------------------------------------------------------ inspection
     @property
@@ -172,6 +183,12 @@ class MuonPlan:
         v = L.muon_plan_info()
         L.check(L.load().muon_plan_get_info(self._h, ctypes.byref(v)))
         return {f: getattr(v, f) for f, _ in v._fields_}
+
+    def ns_flops(self, ns_steps: int) -> float:
+        """The plan's own algorithmic NS flops for ``ns_steps`` steps."""
+        v = ctypes.c_double()
+        L.check(L.load().muon_plan_ns_flops(self._h, int(ns_steps), ctypes.byref(v)))
+        return float(v.value)
 
     def matrix_info(self, i: int) -> dict:
         v = L.muon_matrix_info()
@@ -213,10 +230,11 @@ class MuonPlan:
              stream=None, update_out: Optional[List] = None) -> None:
         """Enqueues one Muon step on ``stream`` (default: torch's current stream).
 
-        The buffers are checked against the plan (``check_step_tensors``:
-        shape, dtype, row-major layout, one GPU) whenever their addresses
-        differ from the previous call's; a failed check raises ValueError and
-        nothing is launched."""
+        A grad may be None: that matrix is skipped (its param and momentum
+        stay as they are).  The buffers whose addresses differ from the
+        previous call's are checked against the plan (``check_step_tensors``:
+        shape, dtype, row-major layout, one GPU); a failed check raises
+        ValueError and nothing is launched."""
         import torch
         n = self.n
         if not (len(params) == len(grads) == len(moms) == n):
@@ -226,26 +244,28 @@ class MuonPlan:
         if stream is None:
             stream = torch.cuda.current_stream(params[0].device)
         sp = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
-        ptrs = ([t.data_ptr() for t in params], [t.data_ptr() for t in grads], [t.data_ptr() for t in moms],
-                None if update_out is None else [0 if t is None else t.data_ptr() for t in update_out],
-                workspace.data_ptr())
-        # The buffers are checked whenever their addresses change (the
-        # library then refreshes its pointer table too), not on every step.
-        if ptrs != self._checked:
-            check_step_tensors(self.descs, params, grads, moms, workspace, update_out)
-            self._checked = ptrs
-        pp = L.ptr_array(ptrs[0])
-        gp = L.ptr_array(ptrs[1])
-        mp = L.ptr_array(ptrs[2])
-        args = (self._h, pp, gp, mp, float(lr), float(momentum), float(weight_decay),
-                int(ns_steps), 1 if nesterov else 0, ctypes.c_void_p(workspace.data_ptr()),
+        pp = [t.data_ptr() for t in params]
+        gp = [0 if t is None else t.data_ptr() for t in grads]
+        mp = [t.data_ptr() for t in moms]
+        op = None if update_out is None else [0 if t is None else t.data_ptr() for t in update_out]
+        wsp = workspace.data_ptr()
+        last = self._checked
+        if last is None or last[4] != wsp or (last[3] is None) != (op is None):
+            todo = None   # everything
+        else:
+            todo = [i for i in range(n) if pp[i] != last[0][i] or gp[i] != last[1][i] or mp[i] != last[2][i]
+                    or (op is not None and op[i] != last[3][i])]
+        if todo is None or todo:
+            check_step_tensors(self.descs, params, grads, moms, workspace, update_out, only=todo)
+        self._checked = (pp, gp, mp, op, wsp)
+        args = (self._h, L.ptr_array(pp), L.ptr_array(gp), L.ptr_array(mp), float(lr), float(momentum),
+                float(weight_decay), int(ns_steps), 1 if nesterov else 0, ctypes.c_void_p(wsp),
                 workspace.numel() * workspace.element_size(), ctypes.c_void_p(sp))
         lib = L.load()
         if update_out is None:
             L.check(lib.muon_step(*args))
         else:
-            op = L.ptr_array(ptrs[3])
-            L.check(lib.muon_step_debug(*args, op))
+            L.check(lib.muon_step_debug(*args, L.ptr_array(op)))
 
     def close(self) -> None:
         if getattr(self, "_h", None) is not None and self._h.value:
@@ -267,9 +287,13 @@ def _optimizer_base():
 class Muon(_optimizer_base()):
     """torch.optim-style Muon over 2-D parameters (fp32 or bf16).
 
-    Per-parameter state: ``momentum_buffer`` (fp32).  Parameters without a
-    gradient are skipped for that step (a new plan is built when the set of
-    stepped parameters changes).  ``ns_coefficients`` is None (the quintic
+    Per-parameter state: ``momentum_buffer`` (fp32).  Each param group has
+    one plan over all of its parameters, built at the first step and kept
+    while the group's shapes and dtypes stay the same; a parameter without a
+    gradient is passed to the library as a skipped matrix (its param and
+    momentum stay as they are), so a changing set of routed MoE experts
+    reuses the same plan.  The plans of all groups share one workspace per
+    device, sized to the largest.  ``ns_coefficients`` is None (the quintic
     (3.4445, -4.7750, 2.0315) at every step), one (a, b, c), or one triple
     per NS step.
     """
@@ -282,7 +306,8 @@ class Muon(_optimizer_base()):
                         nesterov=nesterov, precision=precision, gram_min_aspect=gram_min_aspect,
                         ns_coefficients=ns_coefficients, autotune=autotune)
         super().__init__(params, defaults)
-        self._plans = {}
+        self._plans = {}       # id(group) -> (key, MuonPlan)
+        self._workspaces = {}  # device -> shared uint8 workspace
         self._tune_cache = tune_cache
 
     @staticmethod
@@ -294,17 +319,32 @@ class Muon(_optimizer_base()):
             return tuple(float(v) for v in abc)
         return tuple(tuple(float(v) for v in t) for t in abc)
 
-    def _plan_for(self, key, descs, group):
-        plan = self._plans.get(key)
-        if plan is None:
-            aspect = group["gram_min_aspect"]
-            if aspect is None:
-                aspect = default_gram_min_aspect(group["precision"])
-            plan = MuonPlan(descs, precision=group["precision"], gram_min_aspect=aspect,
-                            abc=group.get("ns_coefficients"), autotune=group.get("autotune", False),
-                            tune_cache=self._tune_cache, tune_ns_steps=group["ns_steps"])
-            self._plans[key] = plan
+    def _plan_for(self, group, descs):
+        key = (tuple(descs), group["precision"], group["gram_min_aspect"],
+               self._coef_key(group.get("ns_coefficients")), group.get("autotune", False))
+        held = self._plans.get(id(group))
+        if held is not None and held[0] == key:
+            return held[1]
+        if held is not None:
+            held[1].close()
+        aspect = group["gram_min_aspect"]
+        if aspect is None:
+            aspect = default_gram_min_aspect(group["precision"])
+        plan = MuonPlan(descs, precision=group["precision"], gram_min_aspect=aspect,
+                        abc=group.get("ns_coefficients"), autotune=group.get("autotune", False),
+                        tune_cache=self._tune_cache, tune_ns_steps=group["ns_steps"])
+        self._plans[id(group)] = (key, plan)
         return plan
+
+    def _workspace(self, device, need: int):
+        import torch
+        ws = self._workspaces.get(device)
+        if ws is None or ws.numel() < need:
+            self._workspaces[device] = None
+            del ws
+            ws = torch.empty(max(need, 256), dtype=torch.uint8, device=device)
+            self._workspaces[device] = ws
+        return ws
 
     def step(self, closure=None):
         import torch
@@ -313,17 +353,22 @@ class Muon(_optimizer_base()):
             with torch.enable_grad():
                 loss = closure()
         for group in self.param_groups:
-            ps = [p for p in group["params"] if p.grad is not None]
-            if not ps:
+            ps = list(group["params"])
+            if not any(p.grad is not None for p in ps):
                 continue
             for p in ps:
                 if p.ndim != 2:
                     raise ValueError("Muon steps 2-D parameters only")
-            descs = [(p.shape[0], p.shape[1], _dtype_code(p), _dtype_code(p.grad)) for p in ps]
-            abc = group.get("ns_coefficients")
-            key = (id(group), tuple(descs), group["precision"], group["gram_min_aspect"], self._coef_key(abc),
-                   group.get("autotune", False))
-            plan = self._plan_for(key, descs, group)
+            descs = []
+            for p in ps:
+                st = self.state[p]
+                # a parameter's grad dtype is remembered from the last step
+                # that had one (the param dtype until then)
+                if p.grad is not None:
+                    st["grad_dtype"] = _dtype_code(p.grad)
+                gd = st.get("grad_dtype", _dtype_code(p))
+                descs.append((p.shape[0], p.shape[1], _dtype_code(p), gd))
+            plan = self._plan_for(group, descs)
             moms = []
             for p in ps:
                 st = self.state[p]
@@ -332,8 +377,9 @@ class Muon(_optimizer_base()):
                                                              memory_format=torch.contiguous_format)
                 moms.append(st["momentum_buffer"])
             params = [p.data for p in ps]
-            grads = [p.grad.contiguous() for p in ps]
+            grads = [None if p.grad is None else p.grad.contiguous() for p in ps]
+            ws = self._workspace(ps[0].device, plan.workspace_bytes)
             plan.step(params, grads, moms, lr=group["lr"], momentum=group["momentum"],
                       weight_decay=group["weight_decay"], ns_steps=group["ns_steps"],
-                      nesterov=group["nesterov"])
+                      nesterov=group["nesterov"], workspace=ws)
         return loss

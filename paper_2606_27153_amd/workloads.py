@@ -179,3 +179,23 @@ def make_state(torch, wl: Workload, device, indices: Optional[Sequence[int]] = N
 def make_grads(torch, wl: Workload, step: int, device, indices: Optional[Sequence[int]] = None):
     idx = range(wl.n) if indices is None else indices
     return [make_grad(torch, wl, i, step, device) for i in idx]
+
+
+def planted_matrix(rows: int, cols: int, spectrum: Sequence[float], seed: int):
+    """A rows x cols matrix with a chosen spectrum: U diag(spectrum) V^T with
+    seeded random orthonormal U (rows x r) and V (cols x r), r = len(spectrum)
+    <= min(rows, cols).  Returns (matrix, U, spectrum, V), all fp64 numpy.
+    Input generation only (a QR of a Gaussian draw for each factor)."""
+    s = np.asarray(spectrum, dtype=np.float64)
+    r = len(s)
+    if r > min(rows, cols):
+        raise ValueError("spectrum longer than min(rows, cols)")
+    rng = np.random.default_rng(seed)
+
+    def orthonormal(n):
+        q, t = np.linalg.qr(rng.standard_normal((n, r)))
+        return q * np.sign(np.diag(t))
+
+    u = orthonormal(rows)
+    v = orthonormal(cols)
+    return (u * s) @ v.T, u, s, v

@@ -76,9 +76,13 @@ int main(int argc, char** argv) {
       if (class_info(h.kclass).fp32 != int(want_f32) || class_info(h.kclass).f16 != int(want_f16) ||
           h.fp32_ns != int(want_f32) || d.x_f32 != int(want_f32) || d.x_f16 != int(want_f16))
         return fail("operand type of the kernel class");
-      const bool want_gram = !h.fp32_ns && aspect > 0 && double(h.n) >= double(aspect) * double(h.m);
+      const bool want_gram =
+          !h.fp32_ns && aspect > 0 && h.m >= kGramMinM && double(h.n) >= double(aspect) * double(h.m);
       if (h.gram != int(want_gram) || d.gram != h.gram) return fail("Gram-space choice");
-      if ((h.x_off[1] < 0) != bool(h.gram)) return fail("second X buffer must exist exactly for Eq. 2");
+      // the Gram-space form needs the second X buffer when it restarts
+      // (gram_restart steps per segment, below max_ns_steps)
+      const bool want_x1 = !h.gram || p.gram_restart < p.opts.max_ns_steps;
+      if ((h.x_off[1] < 0) == want_x1) return fail("second X buffer must exist exactly when it is used");
       if ((h.xt_off[0] < 0) != (h.fp32_ns == 0) || (h.xt_off[1] < 0) != (h.fp32_ns == 0 || h.gram))
         return fail("X^T buffers must exist exactly for the fp32 classes");
       for (int q = 0; q < SQ_COUNT; ++q)
@@ -140,7 +144,9 @@ int main(int argc, char** argv) {
       groups.insert({h.kclass, h.gram});
     }
     launches += 2;
-    for (const auto& g : groups) launches += g.second ? 16 : 15;
+    // k = 5: Eq. 2 runs 3 launches per step; the Gram-space form, in
+    // segments of 2, 2 and 1 steps, 7 + 7 + 3
+    for (const auto& g : groups) launches += g.second ? 17 : 15;
   }
   if (launches != launches_per_step(p, 5)) return fail("launches per step");
   std::printf("OK %zu matrices %zu waves %zu tiles\n", descs.size(), p.waves.size(), p.h_tiles.size());

@@ -27,7 +27,7 @@ def test_every_declared_symbol_is_exported(lib):
     for name in names:
         assert hasattr(lib, name), name
         assert name in L.SIGNATURES, name
-    assert lib.muon_abi_version() == 3
+    assert lib.muon_abi_version() == 4
 
 
 def test_struct_layout_matches_c_compiler(tmp_path):
@@ -116,7 +116,8 @@ def test_fp16_precision_uses_fp16_everywhere():
         mi = plan.matrix_info(i)
         assert mi["fp32_ns"] == 0
         assert L.KERNEL_CLASSES[mi["kernel_class"]].startswith("f16_")
-        assert mi["gram_space"] == int(mi["n"] >= 1.4 * mi["m"])   # the fp16 default threshold
+        # the fp16 default threshold, and the Gram-space minimum m of 256
+        assert mi["gram_space"] == int(mi["n"] >= 1.4 * mi["m"] and mi["m"] >= 256)
     plan.close()
 
 
@@ -226,13 +227,14 @@ def test_schedule_form_choice_and_launch_count(lib):
     st, h = _create(lib, descs, opts)
     assert st == L.MUON_OK
     info = _info(lib, h)
-    # every c != 0: the wide matrix takes the Gram-space form (3k + 1 = 16
-    # launches), the square one Eq. 2 (3 per step)
-    assert info.n_gram == 1
-    assert info.launches_per_step == 2 + 16 + 15
+    # every c != 0: the wide matrix takes the Gram-space form (segments of 2,
+    # 2 and 1 steps: 3L + 1 launches for L = 2, 3 for L = 1, 17 in all), the
+    # square one Eq. 2 (3 per step)
+    assert info.n_gram == 1 and info.gram_restart == 2
+    assert info.launches_per_step == 2 + 17 + 15
     # the plan keeps its own copy of the schedule
     arr[3 * 4 + 2] = 0.0
-    assert _info(lib, h).launches_per_step == 2 + 16 + 15
+    assert _info(lib, h).launches_per_step == 2 + 17 + 15
     assert lib.muon_plan_destroy(h) == L.MUON_OK
     # a cubic step keeps every matrix on Eq. 2 and drops that step's A*A
     opts, arr = _schedule_opts(lib, [QUINTIC, QUINTIC, QUINTIC, CUBIC, CLASSIC])
@@ -330,3 +332,22 @@ def test_step_buffers_are_checked_against_the_plan():
         check_step_tensors(descs, p[:1], g, m)
     with pytest.raises(TypeError, match="unsupported dtype"):
         check_step_tensors(descs, [torch.zeros(4, 8, dtype=torch.float16), p[1]], g, m)
+
+
+def test_plan_create_accepts_the_buffer_check_flag(lib):
+    opts = L.muon_plan_opts()
+    lib.muon_plan_opts_default(ctypes.byref(opts))
+    opts.flags = L.MUON_PLAN_HOST_ONLY | L.MUON_PLAN_CHECK_BUFFERS
+    st, h = _create(lib, [(8, 8, 1, 1, 0)], opts)
+    assert st == L.MUON_OK
+    assert lib.muon_plan_destroy(h) == L.MUON_OK
+
+
+def test_step_path_never_waits_for_the_stream():
+    # the step refreshes its pointer table with a stream-ordered copy; no
+    # stream or device synchronisation anywhere in the step's code
+    src = open(os.path.join(ROOT, "paper_2606_27153_amd", "csrc", "api.cpp")).read()
+    body = src[src.index("muon_status step_impl("):src.index("void release_events(")]
+    for call in ("hipStreamSynchronize", "hipDeviceSynchronize", "hipMemcpy(", "hipMalloc", "hipHostMalloc",
+                 "hipFree"):
+        assert call not in body, call

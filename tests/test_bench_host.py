@@ -80,7 +80,7 @@ def test_ns_cost_matches_the_plan_accounting():
         wl = get_workload(key)
         plan = MuonPlan([(m.rows, m.cols, m.param, m.grad) for m in wl.matrices], host_only=True)
         info = plan.info()
-        want = info["ns_flops_fixed"] + 5 * info["ns_flops_step"]
+        want = plan.ns_flops(5)
         got = sum(bench.ns_cost(m.rows, m.cols, 5) for m in wl.matrices)
         assert abs(got - want) <= 1e-9 * want, key
         plan.close()
@@ -142,8 +142,9 @@ def test_live_flop_share():
     assert bench.live_flop_share(plan, 5, [False] * 4) == {k: 1.0 for k in share}
     assert bench.live_flop_share(plan, 5, [True] * 4) == {k: 0.0 for k in share}
     plan.close()
-    # Gram-space (n >= 2m) and Eq. 2 matrices in one class: gram work is m^2 n
-    # once for the former, k m^2 n for the latter
+    # Gram-space (n >= 2m) and Eq. 2 matrices in one class: with restarts
+    # every 2 steps (segments 2, 2, 1) the former's Gram and B*X run 3 times,
+    # the latter's k = 5 times
     descs = [(1024, 4096, "bf16", "bf16"), (1024, 1024, "bf16", "bf16")]
     plan = MuonPlan(descs, host_only=True)
     infos = [plan.matrix_info(i) for i in range(2)]
@@ -151,8 +152,8 @@ def test_live_flop_share():
     from paper_2606_27153_amd import _lib as L
     cls = L.KERNEL_CLASSES[infos[0]["kernel_class"]]
     share = bench.live_flop_share(plan, 5, [False, True])
-    g_rect, g_sq = 1024 ** 2 * 4096, 5 * 1024 ** 3
+    g_rect, g_sq = 3 * 1024 ** 2 * 4096, 5 * 1024 ** 3
     assert share[("gram", cls)] == pytest.approx(g_rect / (g_rect + g_sq))
     assert share[("symm", cls)] == pytest.approx(1.0)   # only the Gram-space matrix has symmetric products
-    assert share[("bx", cls)] == pytest.approx(2 * 1024 ** 2 * 4096 / (2 * 1024 ** 2 * 4096 + 5 * 2 * 1024 ** 3))
+    assert share[("bx", cls)] == pytest.approx(3 * 2 * 1024 ** 2 * 4096 / (3 * 2 * 1024 ** 2 * 4096 + 5 * 2 * 1024 ** 3))
     plan.close()

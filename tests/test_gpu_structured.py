@@ -1,0 +1,136 @@
+"""GPU parity on structured gradients: planted spectra with a known SVD.
+
+For G = U diag(s) V^T and zero momentum, one Nesterov step gives u = (1 +
+mu) G, and Eq. 2 maps every singular value on its own, so the update has the
+closed form O = U p^{o5}(s / ||s||) V^T (p(x) = a x + b x^3 + c x^5).  The
+gradients are stored in fp32, so the input the GPU reads is the planted one to
+about 1e-7.  Each case checks
+  * the oracle against that closed form (which pins the oracle on the input);
+  * the GPU's O against the oracle -- over the whole matrix, and for a
+    rank-deficient input also on the signal subspace U^T O V, since the rest
+    of O is the input's rounding noise amplified by up to p'(0)^5 ~ 485
+    (any finite precision amplifies it; only its size can be bounded);
+  * the Gram-space form (Eq. 4, restarted every 2 steps) against Eq. 2 on the
+    same input: it may not be markedly less accurate.
+
+Spectra: "mild" (uniform in [0.5, 1]), "wide" (log-spaced from 1 to 1e-3),
+"power" (1 / i) and "rank8" (rank m / 8, the rest exactly zero).  The 16-bit
+bars for the last three come from an fp32-accumulate emulation of the same
+arithmetic (16-bit stores at every stored matrix), with margin: Eq. 2 in bf16
+gives 3-5e-2 (wide), 3e-2 (power), 0.2 over the whole matrix and 7e-3 on the
+signal subspace (rank8); the restarted Gram form 4e-2, 2.7e-2, 0.16 and
+1.7e-2; fp16 about 8x less.  Without restarts the bf16 Gram form gave 0.5
+(wide) and 11-21 (power): the 16-bit rounding of small eigenvalues of the
+Gram matrix grows step by step.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import muon_ref as R
+from paper_2606_27153_amd.optim import MuonPlan
+from paper_2606_27153_amd.workloads import custom_workload, planted_matrix
+
+from parity_utils import assert_parity, rel, run_parity
+
+pytestmark = pytest.mark.gpu
+
+# three take the Gram-space form by default (aspect >= 2, m >= 256), the
+# square one Eq. 2
+SHAPES = [(384, 1024), (1024, 384), (640, 640), (512, 2048)]
+SPECTRA = ("mild", "wide", "power", "rank8")
+MU = 0.95
+
+# (whole matrix, signal subspace) bars per precision and spectrum; None: the
+# contract bar of the precision, checked through assert_parity
+BARS = {
+    "bf16": {"mild": None, "wide": (8e-2, None), "power": (5e-2, None), "rank8": (0.3, 3e-2)},
+    "fp16": {"mild": None, "wide": (1e-2, None), "power": (7e-3, None), "rank8": (4e-2, 4e-3)},
+    "fp32": {"mild": None, "wide": None, "power": None, "rank8": (1e-4, 1e-5)},
+}
+
+
+def _spectrum(name, m, rng):
+    if name == "mild":
+        return np.sort(rng.uniform(0.5, 1.0, m))[::-1]
+    if name == "wide":
+        return np.logspace(0, -3, m)
+    if name == "power":
+        return 1.0 / np.arange(1, m + 1)
+    r = m // 8
+    return np.concatenate([np.sort(rng.uniform(0.5, 1.0, r))[::-1], np.zeros(m - r)])
+
+
+def _closed_form(u, s, v, abc=R.QUINTIC_ABC, k=5):
+    a, b, c = (float(np.float32(t)) for t in abc)
+    x = s / np.linalg.norm(s)
+    for _ in range(k):
+        x = a * x + b * x ** 3 + c * x ** 5
+    return (u * x) @ v.T
+
+
+def _planted_set(name, seed):
+    rng = np.random.default_rng(seed)
+    mats = []
+    for i, (r, c) in enumerate(SHAPES):
+        mats.append(planted_matrix(r, c, _spectrum(name, min(r, c), rng), seed * 100 + i))
+    return mats
+
+
+def _run(precision, name, gram_min_aspect):
+    planted = _planted_set(name, 5)
+    wl = custom_workload(SHAPES, param="f32", grad="f32", seed=51, steps=1)
+    grads = [torch.from_numpy(g.astype(np.float32)).to("cuda:0") for g, _, _, _ in planted]
+    res = run_parity(wl, precision=precision, steps=1, grads_fn=lambda step: grads,
+                     gram_min_aspect=gram_min_aspect, keep_outputs=True)
+    return planted, res
+
+
+def _signal_err(o, ref, u, s, v):
+    r = int(np.count_nonzero(s))
+    ur, vr = u[:, :r], v[:, :r]
+    return rel(ur.T @ o @ vr, ur.T @ ref @ vr)
+
+
+@pytest.mark.parametrize("precision", ["bf16", "fp16", "fp32"])
+@pytest.mark.parametrize("name", SPECTRA)
+def test_planted_spectrum(precision, name):
+    aspect = {"bf16": 2.0, "fp16": 1.4, "fp32": 2.0}[precision]
+    planted, res = _run(precision, name, aspect)
+    plan = MuonPlan([(r, c, "f32", "f32") for r, c in SHAPES], precision=precision, gram_min_aspect=aspect,
+                    host_only=True)
+    forms = ["gram" if plan.matrix_info(i)["gram_space"] else "eq2" for i in range(len(SHAPES))]
+    plan.close()
+    bar = BARS[precision][name]
+    lines = []
+    for i, (g, u, s, v) in enumerate(planted):
+        o, ref = res.outputs[i]
+        # the oracle against the closed form of the planted input
+        cf = _closed_form(u, s, v)
+        oracle_cf = rel(ref, cf)
+        assert oracle_cf <= 1e-5, (i, oracle_cf)
+        err = res.reports[i].o_rel
+        sig = _signal_err(o, ref, u, s, v)
+        lines.append(f"{SHAPES[i]} {forms[i]}: O {err:.2e}, signal {sig:.2e}, oracle vs closed form {oracle_cf:.1e}")
+        if bar is not None:
+            whole, signal = bar
+            assert err <= whole, (i, forms[i], err, whole)
+            if signal is not None:
+                assert sig <= signal, (i, forms[i], sig, signal)
+    print(f"[gpu-test] planted {name} {precision}: " + "; ".join(lines), flush=True)
+    if bar is None:
+        assert_parity(res, precision, f"planted {name}")
+
+
+@pytest.mark.parametrize("precision", ["bf16", "fp16"])
+@pytest.mark.parametrize("name", ["wide", "power", "rank8"])
+def test_gram_form_no_worse_than_eq2_on_ill_conditioned_input(precision, name):
+    aspect = {"bf16": 2.0, "fp16": 1.4}[precision]
+    _, gram = _run(precision, name, aspect)
+    _, eq2 = _run(precision, name, 0.0)
+    out = []
+    for i in (0, 1, 3):   # the Gram-space matrices of the set
+        g, e = gram.reports[i].o_rel, eq2.reports[i].o_rel
+        out.append(f"{SHAPES[i]} Gram {g:.2e} Eq. 2 {e:.2e}")
+        assert g <= 1.25 * e + 2e-3, (i, g, e)
+    print(f"[gpu-test] {name} {precision}: " + "; ".join(out), flush=True)

@@ -186,7 +186,7 @@ def test_orthogonal_equivariance():
 
 
 # ---------------------------------------------------------------- per-step schedules
-# Sec. 5 ("Configurations"): a schedule gives each NS step its own (a, b, c).
+# Sec. 4 ("Configurations"): a schedule gives each NS step its own (a, b, c).
 # Step i then maps a singular value x to p_i(x), so k steps apply the
 # composition p_{k-1} o ... o p_0, in that order.
 
@@ -268,8 +268,22 @@ def test_gram_space_identity():
         x = rng.standard_normal((rows, cols))
         x /= np.linalg.norm(x)
         a = R.newton_schulz(x, 5)
-        b = R.newton_schulz_gram(x, 5)
-        assert _rel(b, a) < 1e-11
+        for restart in (None, 1, 2, 3):
+            b = R.newton_schulz_gram(x, 5, restart=restart)
+            assert _rel(b, a) < 1e-11, restart
+
+
+def test_gram_space_restart_matches_the_svd_map():
+    # restarted segments on a known spectrum: still U p^{o5}(s) V^T
+    rng = np.random.default_rng(10)
+    u, _ = np.linalg.qr(rng.standard_normal((12, 12)))
+    v, _ = np.linalg.qr(rng.standard_normal((30, 12)))
+    s = np.logspace(0, -2, 12)
+    s /= np.linalg.norm(s)
+    x = (u * s) @ v.T
+    want = (u * _pk(s, 5)) @ v.T
+    for restart in (1, 2, 4):
+        assert _rel(R.newton_schulz_gram(x, 5, restart=restart), want) < 1e-11
 
 
 # ---------------------------------------------------------------- momentum / apply
@@ -351,6 +365,75 @@ def test_bf16_round_ties_to_even():
     # 1 + 2^-8 is halfway between 1 and 1 + 2^-7: ties go to the even 1.0
     assert R.bf16_round(np.array([1.0 + 2.0 ** -8]))[0] == 1.0
     assert R.bf16_round(np.array([1.0 + 3 * 2.0 ** -8]))[0] == 1.0 + 2.0 ** -6
+
+
+def _f32_from_bits(bits):
+    return np.asarray(bits, dtype=np.uint32).view(np.float32).astype(np.float64)
+
+
+def test_f32_round_halfway_cases_from_the_grid():
+    # Neighbouring fp32 values lo < hi are built from their bit patterns
+    # (normal and subnormal, both signs); the fp64 midpoint of each pair is
+    # exact.  Round-to-nearest-even sends the midpoint to the one whose last
+    # significand bit is 0, and anything off the midpoint by a quarter step to
+    # the nearer one.  A truncating or ties-away narrowing fails here.
+    rng = np.random.default_rng(17)
+    mags = np.concatenate([rng.integers(1 << 23, 0x7F7FFFFF, size=4000),   # normal
+                           rng.integers(1, 1 << 23, size=1000),            # subnormal
+                           [1, (1 << 23) - 1, 1 << 23, 0x3F800000, 0x7F7FFFFE]]).astype(np.uint64)
+    for sign in (0, 1 << 31):
+        lo_bits = mags | np.uint64(sign)
+        lo = _f32_from_bits(lo_bits)
+        hi = _f32_from_bits(lo_bits + np.uint64(1))   # next magnitude, same sign
+        mid = (lo + hi) / 2.0
+        even = np.where((mags & np.uint64(1)) == 0, lo, hi)
+        assert np.array_equal(R.f32_round(mid), even)
+        quarter = (hi - lo) / 4.0
+        assert np.array_equal(R.f32_round(mid - quarter), lo)
+        assert np.array_equal(R.f32_round(mid + quarter), hi)
+        assert np.array_equal(R.f32_round(lo), lo) and np.array_equal(R.f32_round(hi), hi)
+
+
+def test_f32_round_range_ends():
+    top = _f32_from_bits(0x7F7FFFFF)           # largest finite fp32
+    half_ulp = 2.0 ** (127 - 24)
+    with np.errstate(over="ignore"):
+        assert R.f32_round(np.array([top + 0.5 * half_ulp]))[0] == top
+        # the midpoint between the largest finite and 2^128 rounds to even: inf
+        assert np.isposinf(R.f32_round(np.array([top + half_ulp]))[0])
+        assert np.isneginf(R.f32_round(np.array([-(top + half_ulp)]))[0])
+    tiny = 2.0 ** -149                         # smallest subnormal
+    assert R.f32_round(np.array([0.5 * tiny]))[0] == 0.0          # tie to the even 0
+    assert R.f32_round(np.array([0.75 * tiny]))[0] == tiny
+    assert R.f32_round(np.array([1.5 * tiny]))[0] == 2 * tiny     # tie to the even 2
+    assert R.f32_round(np.array([-0.0]))[0] == 0.0
+
+
+def _f32_truncate(x):
+    # planted mistake: chops the significand (rounds toward zero)
+    x = np.asarray(x, dtype=np.float64)
+    r = np.asarray(x, dtype=np.float32).astype(np.float64)
+    down = np.abs(r) > np.abs(x)
+    r[down] = np.nextafter(r[down].astype(np.float32), np.float32(0)).astype(np.float64)
+    return r
+
+
+def _f32_ties_away(x):
+    # planted mistake: halfway cases go away from zero
+    x = np.asarray(x, dtype=np.float64)
+    r = np.asarray(x, dtype=np.float32).astype(np.float64)
+    other = np.nextafter(r.astype(np.float32), np.where(x > r, np.float32(np.inf), np.float32(-np.inf)))
+    other = other.astype(np.float64)
+    tie = (np.abs(other - x) == np.abs(r - x)) & (np.abs(other) > np.abs(r))
+    r[tie] = other[tie]
+    return r
+
+
+@pytest.mark.parametrize("mutant", [_f32_truncate, _f32_ties_away], ids=["truncate", "ties-away"])
+def test_pins_catch_planted_f32_rounding_mistakes(monkeypatch, mutant):
+    monkeypatch.setattr(R, "f32_round", mutant)
+    with pytest.raises(AssertionError):
+        test_f32_round_halfway_cases_from_the_grid()
 
 
 def test_zero_gradient_bf16_param_is_bitwise_unchanged():

@@ -1,6 +1,8 @@
 """Planner invariants checked on the host: tests/plan_check.cpp is built with
-g++ against csrc/plan.cpp (no HIP) and run on the shape lists of every
-workload, a ragged set and random shapes."""
+g++ against csrc/plan.cpp (no HIP), with AddressSanitizer and
+UndefinedBehaviorSanitizer (the kernels trust the planner's tables and
+padding), and run on the shape lists of every workload, a ragged set and
+random shapes."""
 import os
 import subprocess
 
@@ -15,7 +17,8 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 @pytest.fixture(scope="module")
 def plan_check(tmp_path_factory):
     exe = tmp_path_factory.mktemp("plan") / "plan_check"
-    subprocess.run(["g++", "-std=c++17", "-O1", "-I", os.path.join(ROOT, "include"),
+    subprocess.run(["g++", "-std=c++17", "-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+                    "-fno-sanitize-recover=all", "-I", os.path.join(ROOT, "include"),
                     os.path.join(ROOT, "tests", "plan_check.cpp"),
                     os.path.join(ROOT, "paper_2606_27153_amd", "csrc", "plan.cpp"), "-o", str(exe)],
                    check=True)
