@@ -262,6 +262,29 @@ MUON_API muon_status muon_check_buffers(muon_plan plan, void* const* params, con
                                         void* const* momentum, void* workspace, size_t workspace_bytes,
                                         float* const* update_out);
 
+/* Size of the library's static workspace (muon_step_static): 64 MiB. */
+#define MUON_STATIC_WORKSPACE_BYTES (64u << 20)
+
+/* muon_step without a caller workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, allocation-free serving
+ * loops, harnesses that forbid hipMalloc).  The step runs exactly as
+ * muon_step (same kernels, bitwise the same W and M) but in a workspace the
+ * library holds itself: a static device array of MUON_STATIC_WORKSPACE_BYTES
+ * on each GPU the library runs on, kept until the process ends.  Nothing is
+ * allocated: no hipMalloc, hipFree or allocating library call (launch timing
+ * is not recorded on this path, since its events would be created).
+ *   - The plan's workspace (muon_plan_workspace_bytes) must fit: a larger
+ *     plan gives WORKSPACE_TOO_SMALL and nothing is enqueued.
+ *   - Every call on one GPU shares that GPU's array, which keeps whatever
+ *     the last call left there; a step writes every byte it later reads, so
+ *     nothing needs clearing.  Calls that may overlap on one GPU (other
+ *     streams, other threads, other plans) race on the array: order them.
+ * Arguments and errors as for muon_step (without workspace and
+ * workspace_bytes). */
+MUON_API muon_status muon_step_static(muon_plan plan, void* const* params, const void* const* grads,
+                                      void* const* momentum, float lr, float momentum_coef, float weight_decay,
+                                      int32_t ns_steps, int32_t nesterov, void* hip_stream);
+
 /* muon_step plus, for every i with update_out[i] != NULL, the orthogonalised
  * update O_i (before lr and the shape scale) written as fp32 rows x cols
  * row-major to update_out[i] (device, 16-byte aligned).  W and M are

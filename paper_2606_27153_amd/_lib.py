@@ -32,6 +32,7 @@ MUON_NS_FP16 = 2
 
 MUON_PLAN_HOST_ONLY = 0x1
 MUON_PLAN_CHECK_BUFFERS = 0x2
+MUON_STATIC_WORKSPACE_BYTES = 64 << 20
 
 
 class muon_matrix_desc(ctypes.Structure):
@@ -93,6 +94,8 @@ SIGNATURES = {
     "muon_plan_matrix_info": (ctypes.c_int, [_VP, ctypes.c_int32, ctypes.POINTER(muon_matrix_info)]),
     "muon_step": (ctypes.c_int, _STEP_ARGS),
     "muon_step_debug": (ctypes.c_int, _STEP_ARGS + [_PP]),
+    "muon_step_static": (ctypes.c_int, [_VP, _PP, _PP, _PP, ctypes.c_float, ctypes.c_float, ctypes.c_float,
+                                        ctypes.c_int32, ctypes.c_int32, _VP]),
     "muon_check_buffers": (ctypes.c_int, [_VP, _PP, _PP, _PP, _VP, ctypes.c_size_t, _PP]),
     "muon_plan_set_timing": (ctypes.c_int, [_VP, ctypes.c_int32]),
     "muon_plan_timing_read": (ctypes.c_int, [_VP, ctypes.POINTER(muon_kernel_stat), ctypes.c_int32,

@@ -17,7 +17,7 @@ LIB_NAME = "libmuon_mi355x.so"
 LIB_PATH = os.path.join(PKG, LIB_NAME)
 ARCH = "gfx950"
 
-SOURCES = ["api.cpp", "plan.cpp", "ew_kernels.hip", "ns_gemm.hip"]
+SOURCES = ["api.cpp", "plan.cpp", "ew_kernels.hip", "ns_gemm.hip", "static_ws.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

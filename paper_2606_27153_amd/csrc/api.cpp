@@ -166,7 +166,7 @@ muon_status check_memory(const void* ptr, size_t bytes, int device, const std::s
 // MUON_PLAN_CHECK_BUFFERS.
 muon_status check_buffers(const muon::Plan& p, void* const* params, const void* const* grads,
                           void* const* momentum, const void* workspace, size_t workspace_bytes,
-                          float* const* update_out, bool memory) {
+                          float* const* update_out, bool memory, bool own_ws = false) {
   if (!params || !grads || !momentum) return fail(MUON_ERR_INVALID_ARG, "params, grads and momentum must be non-NULL");
   if (!workspace) return fail(MUON_ERR_INVALID_ARG, "workspace is NULL");
   if (!aligned(workspace, 256)) return fail(MUON_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
@@ -188,7 +188,8 @@ muon_status check_buffers(const muon::Plan& p, void* const* params, const void* 
     return fail(MUON_ERR_INVALID_ARG, "current device " + std::to_string(dev) + " is not the plan's device " +
                                           std::to_string(p.device));
   if (!memory) return MUON_OK;
-  muon_status st = check_memory(workspace, size_t(p.ws_bytes), dev, "the workspace");
+  // (the library's own static workspace needs no vetting)
+  muon_status st = own_ws ? MUON_OK : check_memory(workspace, size_t(p.ws_bytes), dev, "the workspace");
   for (size_t i = 0; i < n && st == MUON_OK; ++i) {
     const muon::MatHost& h = p.mats[i];
     const size_t el = size_t(h.rows) * size_t(h.cols);
@@ -202,9 +203,11 @@ muon_status check_buffers(const muon::Plan& p, void* const* params, const void* 
   return st;
 }
 
+// One step.  `own_ws`: the workspace is the library's static one (it needs
+// no vetting, and the step records no timing events, which would allocate).
 muon_status step_impl(muon_plan plan, void* const* params, const void* const* grads, void* const* momentum,
                       float lr, float mu, float wd, int32_t ns_steps, int32_t nesterov, void* workspace,
-                      size_t workspace_bytes, void* stream, float* const* update_out) {
+                      size_t workspace_bytes, void* stream, float* const* update_out, bool own_ws = false) {
   using namespace muon;
   if (!plan) return fail(MUON_ERR_INVALID_ARG, "plan is NULL");
   Plan& p = plan->p;
@@ -218,7 +221,7 @@ muon_status step_impl(muon_plan plan, void* const* params, const void* const* gr
   muon_status st = check_buffers(p, params, grads, momentum, workspace, workspace_bytes, update_out, false);
   if (st != MUON_OK) return st;
   const size_t n = p.mats.size();
-  const bool timing = p.timing;
+  const bool timing = p.timing && !own_ws;
 
   // Refresh the device pointer table if the caller's buffers moved: the new
   // table goes into the next slot of the plan's pinned ring and is copied on
@@ -233,11 +236,11 @@ muon_status step_impl(muon_plan plan, void* const* params, const void* const* gr
     changed = h.param != params[i] || h.grad != grads[i] || h.mom != momentum[i] || h.out != out;
   }
   if (changed && (p.opts.flags & MUON_PLAN_CHECK_BUFFERS)) {
-    st = check_buffers(p, params, grads, momentum, workspace, workspace_bytes, update_out, true);
+    st = check_buffers(p, params, grads, momentum, workspace, workspace_bytes, update_out, true, own_ws);
     if (st != MUON_OK) return st;
-    p.ws_checked = workspace;
+    if (!own_ws) p.ws_checked = workspace;
   }
-  if (workspace != p.ws_checked) {
+  if (workspace != p.ws_checked && !own_ws) {
     st = check_memory(workspace, size_t(p.ws_bytes), p.device, "the workspace");
     if (st != MUON_OK) return st;
     p.ws_checked = workspace;
@@ -489,6 +492,12 @@ muon_status muon_plan_create(const muon_matrix_desc* mats, int32_t n, const muon
       delete plan;
       return fail(st, msg);
     }
+    // the address of this device's static workspace (muon_step_static)
+    plan->p.static_ws_status = muon::static_workspace_init(plan->p.device, &plan->p.static_ws);
+    if (plan->p.static_ws_status != hipSuccess) {
+      (void)hipGetLastError();
+      plan->p.static_ws = nullptr;
+    }
   }
   *out = plan;
   return ok();
@@ -605,6 +614,24 @@ muon_status muon_check_buffers(muon_plan plan, void* const* params, const void* 
   if (!plan->p.d_block) return fail(MUON_ERR_INVALID_ARG, "plan was created host-only and cannot be stepped");
   const muon_status st = check_buffers(plan->p, params, grads, momentum, workspace, workspace_bytes, update_out, true);
   return st == MUON_OK ? ok() : st;
+}
+
+muon_status muon_step_static(muon_plan plan, void* const* params, const void* const* grads, void* const* momentum,
+                             float lr, float momentum_coef, float weight_decay, int32_t ns_steps, int32_t nesterov,
+                             void* hip_stream) {
+  static_assert(muon::kStaticWorkspaceBytes == size_t(MUON_STATIC_WORKSPACE_BYTES), "static workspace size");
+  if (!plan) return fail(MUON_ERR_INVALID_ARG, "plan is NULL");
+  muon::Plan& p = plan->p;
+  if (!p.d_block) return fail(MUON_ERR_INVALID_ARG, "plan was created host-only and cannot be stepped");
+  if (size_t(p.ws_bytes) > muon::kStaticWorkspaceBytes)
+    return fail(MUON_ERR_WORKSPACE_TOO_SMALL,
+                "plan needs " + std::to_string(p.ws_bytes) + " bytes of workspace, the static workspace holds " +
+                    std::to_string(muon::kStaticWorkspaceBytes) + " (use muon_step with a caller workspace)");
+  if (!p.static_ws)
+    return fail(MUON_ERR_DEVICE, std::string("the static workspace of device ") + std::to_string(p.device) +
+                                     " could not be located: " + hipGetErrorString(hipError_t(p.static_ws_status)));
+  return step_impl(plan, params, grads, momentum, lr, momentum_coef, weight_decay, ns_steps, nesterov, p.static_ws,
+                   muon::kStaticWorkspaceBytes, hip_stream, nullptr, true);
 }
 
 muon_status muon_step_debug(muon_plan plan, void* const* params, const void* const* grads, void* const* momentum,

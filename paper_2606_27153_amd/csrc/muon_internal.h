@@ -166,6 +166,10 @@ struct Plan {
   void* ring_events[kRing] = {};
   bool ring_busy[kRing] = {};
   int ring_next = 0;
+  // this device's static workspace (muon_step_static), null if the lookup
+  // failed (static_ws_status holds the hipError_t)
+  void* static_ws = nullptr;
+  int static_ws_status = 0;
 
   // launch timing (muon_plan_set_timing)
   bool timing = false;
@@ -173,6 +177,11 @@ struct Plan {
   std::vector<TimingRecord> records;
 };
 
+// static_ws.hip: the fixed device workspace of muon_step_static, one per GPU.
+// static_workspace_init (with `device` current) looks up its address once
+// per device and returns it; the result is a hipError_t.
+constexpr size_t kStaticWorkspaceBytes = size_t(64) << 20;
+int static_workspace_init(int device, void** out);
 // plan.cpp (host only)
 muon_status build_plan(const muon_matrix_desc* mats, int32_t n, const muon_plan_opts& o, Plan& p,
                        std::string& err);
