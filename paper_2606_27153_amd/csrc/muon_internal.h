@@ -33,6 +33,7 @@ struct ClassInfo {
   int32_t fp32;     // operands stored as fp32 (else 16-bit)
   int32_t f16;      // 16-bit operands are fp16 (else bf16)
   const char* name;
+  int32_t strip;    // 256 classes: the 128 class that computes their edge strips (else -1)
 };
 
 const ClassInfo& class_info(int32_t kc);
@@ -90,6 +91,11 @@ enum MatFlag : int32_t { FLAG_LIVE = 0, FLAG_ZERO = 1, FLAG_SKIP = 2 };
 struct MatHost {
   int64_t rows, cols, m, n;
   int64_t m_pad, n_pad, rows_pad, cols_pad;
+  // Edge strips: a matrix of a 256 class whose extent ends 128 or fewer
+  // past a multiple of 256 is padded to 128 only; its outputs are computed
+  // on 256 tiles up to m_main x n_main and on 128 tiles of the strip class
+  // beyond (otherwise m_main = m_pad, n_main = n_pad).
+  int64_t m_main, n_main;
   int32_t transposed, kclass, fp32_ns, gram;
   int32_t param_dtype, grad_dtype, momentum_dtype;
   int32_t wave, slot, bucket;
@@ -110,6 +116,13 @@ struct ClassLaunch {
   int64_t full_off;    // TileEntry offset of the full list
   int32_t n_full;
   bool padded;         // some matrix is padded by a whole wave block (rows or columns)
+  // edge-strip tiles (in units of the strip class's 128 tile), launched
+  // with that class after each main launch
+  int32_t strip_kclass;
+  int64_t strip_lower_off;
+  int32_t n_strip_lower;
+  int64_t strip_full_off;
+  int32_t n_strip_full;
 };
 
 struct WaveHost {

@@ -1048,14 +1048,41 @@ int launch_stage(int32_t stage, unsigned nblocks, const GemmArgs& g, hipStream_t
 
 }  // namespace
 
+namespace {
+
+// One grouped launch of class kc over `nblocks` tiles (twice that for a
+// paired ST_SYM step, whose second half computes the second product).
+int launch_tiles(int32_t kc, bool padded, int32_t stage, const TileEntry* tiles, unsigned nblocks, bool pair,
+                 GemmArgs g, hipStream_t st) {
+  if (nblocks == 0) return 0;
+  g.tiles = tiles;
+  g.split = pair ? int32_t(nblocks) : INT32_MAX;
+  const unsigned grid = stage == ST_SYM && pair ? 2 * nblocks : nblocks;
+  switch (kc) {
+    // the 256 tile puts two waves on each SIMD, so a skipped wave speeds up
+    // its partner; with one wave per SIMD (the 4-wave classes) nothing would
+    case KC_BF16_256:
+      return padded ? launch_stage<__bf16, 256, 2, 4, true>(stage, grid, g, st)
+                    : launch_stage<__bf16, 256, 2, 4>(stage, grid, g, st);
+    case KC_BF16_128: return launch_stage<__bf16, 128, 2, 2>(stage, grid, g, st);
+    case KC_BF16_64: return launch_stage<__bf16, 64, 2, 2>(stage, grid, g, st);
+    case KC_F32_128: return launch_stage<float, 128, 2, 2>(stage, grid, g, st);
+    case KC_F32_64: return launch_stage<float, 64, 2, 2>(stage, grid, g, st);
+    case KC_F16_256:
+      return padded ? launch_stage<_Float16, 256, 2, 4, true>(stage, grid, g, st)
+                    : launch_stage<_Float16, 256, 2, 4>(stage, grid, g, st);
+    case KC_F16_128: return launch_stage<_Float16, 128, 2, 2>(stage, grid, g, st);
+    case KC_F16_64: return launch_stage<_Float16, 64, 2, 2>(stage, grid, g, st);
+    default: return -1;
+  }
+}
+
+}  // namespace
+
 int launch_ns_gemm(const Plan& p, const WaveHost& w, const ClassLaunch& cl, int32_t stage, const GemmStep& gs,
                    char* ws, const StepScalars& sc, void* stream) {
   GemmArgs g{};
   g.mats = p.d_mats;
-  const bool full = stage == ST_BX;
-  g.tiles = p.d_tiles + (full ? cl.full_off : cl.lower_off);
-  const unsigned nblocks = unsigned(full ? cl.n_full : cl.n_lower);
-  const unsigned grid = stage == ST_SYM && gs.pair ? 2 * nblocks : nblocks;
   g.ws = ws;
   g.scale = reinterpret_cast<const float*>(ws + w.scale_off);
   g.flag = reinterpret_cast<const int32_t*>(ws + w.flag_off);
@@ -1071,29 +1098,20 @@ int launch_ns_gemm(const Plan& p, const WaveHost& w, const ClassLaunch& cl, int3
   g.l2 = gs.l2;
   g.r2 = gs.r2;
   g.out2 = gs.out2;
-  g.split = gs.pair ? int32_t(nblocks) : INT32_MAX;
   g.ptrs = p.d_ptrs;
   g.lr = sc.lr;
   g.decay = sc.decay;
-  if (nblocks == 0) return 0;
   hipStream_t st = hipStream_t(stream);
-  switch (cl.kclass) {
-    // the 256 tile puts two waves on each SIMD, so a skipped wave speeds up
-    // its partner; with one wave per SIMD (the 4-wave classes) nothing would
-    case KC_BF16_256:
-      return cl.padded ? launch_stage<__bf16, 256, 2, 4, true>(stage, grid, g, st)
-                       : launch_stage<__bf16, 256, 2, 4>(stage, grid, g, st);
-    case KC_BF16_128: return launch_stage<__bf16, 128, 2, 2>(stage, grid, g, st);
-    case KC_BF16_64: return launch_stage<__bf16, 64, 2, 2>(stage, grid, g, st);
-    case KC_F32_128: return launch_stage<float, 128, 2, 2>(stage, grid, g, st);
-    case KC_F32_64: return launch_stage<float, 64, 2, 2>(stage, grid, g, st);
-    case KC_F16_256:
-      return cl.padded ? launch_stage<_Float16, 256, 2, 4, true>(stage, grid, g, st)
-                       : launch_stage<_Float16, 256, 2, 4>(stage, grid, g, st);
-    case KC_F16_128: return launch_stage<_Float16, 128, 2, 2>(stage, grid, g, st);
-    case KC_F16_64: return launch_stage<_Float16, 64, 2, 2>(stage, grid, g, st);
-    default: return -1;
-  }
+  const bool full = stage == ST_BX;
+  // the 256-tile part, then the edge strips of the same matrices on the
+  // strip class's 128 tiles (their outputs are disjoint)
+  int e = launch_tiles(cl.kclass, cl.padded, stage, p.d_tiles + (full ? cl.full_off : cl.lower_off),
+                       unsigned(full ? cl.n_full : cl.n_lower), gs.pair != 0, g, st);
+  if (e == 0 && cl.strip_kclass >= 0)
+    e = launch_tiles(cl.strip_kclass, false, stage,
+                     p.d_tiles + (full ? cl.strip_full_off : cl.strip_lower_off),
+                     unsigned(full ? cl.n_strip_full : cl.n_strip_lower), gs.pair != 0, g, st);
+  return e;
 }
 
 }  // namespace muon

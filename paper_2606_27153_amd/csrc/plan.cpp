@@ -18,32 +18,49 @@ namespace muon {
 namespace {
 
 constexpr ClassInfo kClasses[KC_COUNT] = {
-    {256, 0, 0, "bf16_t256"},
-    {128, 0, 0, "bf16_t128"},
-    {64, 0, 0, "bf16_t64"},
-    {128, 1, 0, "f32_t128"},
-    {64, 1, 0, "f32_t64"},
-    {256, 0, 1, "f16_t256"},
-    {128, 0, 1, "f16_t128"},
-    {64, 0, 1, "f16_t64"},
+    {256, 0, 0, "bf16_t256", KC_BF16_128},
+    {128, 0, 0, "bf16_t128", -1},
+    {64, 0, 0, "bf16_t64", -1},
+    {128, 1, 0, "f32_t128", -1},
+    {64, 1, 0, "f32_t64", -1},
+    {256, 0, 1, "f16_t256", KC_F16_128},
+    {128, 0, 1, "f16_t128", -1},
+    {64, 0, 1, "f16_t64", -1},
 };
-
-// Relative throughput assumed for each class when choosing a tile: larger
-// tiles re-use each loaded byte more often.
-constexpr double kClassEfficiency[KC_COUNT] = {1.0, 0.8, 0.45, 1.0, 0.6, 1.0, 0.8, 0.45};
 
 constexpr int64_t kDefaultWaveBytes = int64_t(12) << 30;  // 12 GiB
 constexpr int64_t kAlign = 256;
 
 int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 
-// Flops of one Eq. 2 step as the kernels issue them: output tiles cover the
-// padded extent, while each K loop stops at the last slab of bk elements that
-// holds real data (Gram: K = n; A*A and B*X: K = m).
-double padded_cost(int64_t m, int64_t n, int32_t tile, int64_t bk) {
-  const double mp = double(round_up(m, tile)), np = double(round_up(n, tile));
+// Extent of the 256-tile part of a padded extent: a 256-class matrix whose
+// extent ends 128 or fewer past a multiple of 256 (and holds at least one
+// whole 256 tile) is padded to 128 only, and its last 128 rows or columns
+// form an edge strip computed on 128 tiles.
+int64_t main_extent(int64_t v, int32_t tile, int32_t strip_class) {
+  const int64_t p128 = round_up(v, 128);
+  if (tile != 256 || strip_class < 0 || p128 == round_up(v, 256) || p128 < 384) return round_up(v, tile);
+  return p128 - 128;
+}
+
+// Relative throughput assumed for each class when choosing a tile: larger
+// tiles re-use each loaded byte more often.
+constexpr double kClassEfficiency[KC_COUNT] = {1.0, 0.8, 0.45, 1.0, 0.6, 1.0, 0.8, 0.45};
+
+// Time-like cost of one Eq. 2 step as the kernels issue it: output tiles
+// cover the padded extent, the K loops stop at the last slab of bk elements
+// that holds real data (Gram: K = n; A*A and B*X: K = m), and the flops of
+// edge strips count at the strip class's efficiency.
+double padded_cost(int64_t m, int64_t n, int32_t kc, int64_t bk) {
+  const ClassInfo& ci = kClasses[kc];
+  const int64_t mm = main_extent(m, ci.tile, ci.strip), nm = main_extent(n, ci.tile, ci.strip);
+  const double mp = double(mm < round_up(m, ci.tile) ? round_up(m, 128) : mm);
+  const double np = double(nm < round_up(n, ci.tile) ? round_up(n, 128) : nm);
   const double km = double(round_up(m, bk)), kn = double(round_up(n, bk));
-  return mp * mp * kn + mp * mp * km + 2.0 * mp * np * km;
+  const double main = double(mm) * double(mm) * (kn + km) + 2.0 * double(mm) * double(nm) * km;
+  const double all = mp * mp * (kn + km) + 2.0 * mp * np * km;
+  const double strip_eff = ci.strip >= 0 ? kClassEfficiency[ci.strip] : kClassEfficiency[kc];
+  return main / kClassEfficiency[kc] + (all - main) / strip_eff;
 }
 
 // Kernel class of an m x n matrix: the operand type follows the precision
@@ -63,7 +80,7 @@ int32_t choose_class(int64_t m, int64_t n, const muon_plan_opts& o, int32_t tile
   int32_t best = hi;
   double best_cost = 0;
   for (int32_t kc = lo; kc <= hi; ++kc) {
-    const double cost = padded_cost(m, n, kClasses[kc].tile, kClasses[kc].fp32 ? 32 : 64) / kClassEfficiency[kc];
+    const double cost = padded_cost(m, n, kc, kClasses[kc].fp32 ? 32 : 64);
     if (kc == lo || cost < best_cost) {
       best = kc;
       best_cost = cost;
@@ -72,38 +89,25 @@ int32_t choose_class(int64_t m, int64_t n, const muon_plan_opts& o, int32_t tile
   return best;
 }
 
-// Full tile list of one matrix (tm x tn output tiles) in dispatch order.
-//
-// Blocks are dispatched round-robin over the 8 XCDs (block b runs on XCD
-// b % 8), and about 256 of them (one per CU) run at a time.  Tiles are
-// taken in chunks of 8 row panels x up to 32 column panels; within a chunk
-// XCD x receives the 4 x W/4 sub-block at rows 4*(x%2), columns (x/2)*W/4.
-// The blocks running together thus read 8 + 32 operand panels chip-wide
-// (shared through the MALL) and 4 + 8 within each XCD's L2.  Chunks that do
-// not fit that pattern fall back to column-major order in groups of 4 rows.
-void emit_full(std::vector<TileEntry>& t, int32_t mat, int64_t tm, int64_t tn) {
-  int64_t g0 = 0;
-  for (; g0 + 8 <= tm; g0 += 8) {
-    for (int64_t c0 = 0; c0 < tn; c0 += 32) {
-      const int64_t w = std::min<int64_t>(32, tn - c0);
-      if (w % 4 != 0 || t.size() % 8 != 0) {
-        for (int64_t tj = c0; tj < c0 + w; ++tj)
-          for (int64_t ti = g0; ti < g0 + 8; ++ti) t.push_back(TileEntry{mat, int32_t(ti), int32_t(tj)});
-        continue;
-      }
-      for (int64_t b = 0; b < 8 * w; ++b) {
-        const int64_t x = b % 8, k = b / 8;
-        const int64_t r = 4 * (x % 2) + k % 4, c = (x / 2) * (w / 4) + k / 4;
-        t.push_back(TileEntry{mat, int32_t(g0 + r), int32_t(c0 + c)});
-      }
-    }
-  }
-  constexpr int64_t kGroup = 4;  // remaining row panels: column-major in groups of 4
-  for (; g0 < tm; g0 += kGroup) {
-    const int64_t g1 = std::min(tm, g0 + kGroup);
-    for (int64_t tj = 0; tj < tn; ++tj)
-      for (int64_t ti = g0; ti < g1; ++ti) t.push_back(TileEntry{mat, int32_t(ti), int32_t(tj)});
-  }
+// Full tiles (all tm x tn output tiles) of one matrix, cut into units of up
+// to 4 row panels x 8 column panels: the 32 tiles of a unit, about the
+// number of blocks one XCD runs at once, read 4 + 8 operand panels, so an
+// XCD working through a unit finds them in its own L2.  The units are dealt
+// to the XCDs like the lower-tile units (interleave_units), listed chunk by
+// chunk of 8 row x 32 column panels, so the eight units running at once
+// share 8 + 32 panels chip-wide (through the MALL).  A small matrix (an MoE
+// expert, 5 x 8 tiles) thus sits on one or two XCDs instead of being spread
+// over all eight.
+void full_units(std::vector<std::vector<TileEntry>>& units, int32_t mat, int64_t tm, int64_t tn) {
+  for (int64_t g0 = 0; g0 < tm; g0 += 8)
+    for (int64_t c0 = 0; c0 < tn; c0 += 32)
+      for (int64_t r0 = g0; r0 < std::min(tm, g0 + 8); r0 += 4)
+        for (int64_t u0 = c0; u0 < std::min(tn, c0 + 32); u0 += 8) {
+          units.emplace_back();
+          for (int64_t ti = r0; ti < std::min(tm, r0 + 4); ++ti)
+            for (int64_t tj = u0; tj < std::min(tn, u0 + 8); ++tj)
+              units.back().push_back(TileEntry{mat, int32_t(ti), int32_t(tj)});
+        }
 }
 
 // Lower-triangular tiles (tj <= ti) of one matrix, cut into compact units:
@@ -159,21 +163,27 @@ void interleave_units(std::vector<TileEntry>& out, const std::vector<std::vector
 const ClassInfo& class_info(int32_t kc) { return kClasses[kc]; }
 
 int64_t launches_per_step(const Plan& p, int32_t ns_steps) {
-  // Eq. 2: Gram, A*A and B*X per step.  Gram space, per segment of L steps:
-  // the Gram product and B*X once, P_i per step, P Q and G P (one launch
-  // when both are due) and P (G P) on all but the last step: 3L + 1
-  // launches, 3 for L = 1.  A cubic step (c = 0) of Eq. 2 has no A*A launch.
+  // Per (class, form) group, lower-tile stages and B*X stages.  Eq. 2: Gram,
+  // A*A and B*X per step (a cubic step, c = 0, has no A*A).  Gram space, per
+  // segment of L steps: the Gram product and B*X once, P_i per step, P Q and
+  // G P (one launch when both are due) and P (G P) on all but the last step,
+  // i.e. 3L lower-tile launches and one B*X (2 and 1 for L = 1).  A stage
+  // whose group has edge-strip tiles launches the strip class after it.
   int64_t n = 0;
   const int64_t k = ns_steps;
-  int64_t eq2 = 0, gram = 0;
-  for (int32_t it = 0; it < ns_steps; ++it) eq2 += p.abc[size_t(3 * it + 2)] != 0.f ? 3 : 2;
+  int64_t eq2_lower = 0, gram_lower = 0, gram_bx = 0;
+  for (int32_t it = 0; it < ns_steps; ++it) eq2_lower += p.abc[size_t(3 * it + 2)] != 0.f ? 2 : 1;
   for (int64_t s0 = 0; s0 < k; s0 += p.gram_restart) {
     const int64_t len = std::min<int64_t>(p.gram_restart, k - s0);
-    gram += len > 1 ? 3 * len + 1 : 3;
+    gram_lower += len > 1 ? 3 * len : 2;
+    gram_bx += 1;
   }
   for (const auto& w : p.waves) {
     n += k > 0 ? 2 : 3;  // momentum, finalize (and apply when no NS step runs)
-    for (const auto& cl : w.launches) n += cl.gram ? gram : eq2;
+    for (const auto& cl : w.launches) {
+      const int64_t lw = cl.n_strip_lower > 0 ? 2 : 1, bw = cl.n_strip_full > 0 ? 2 : 1;
+      n += cl.gram ? gram_lower * lw + gram_bx * bw : eq2_lower * lw + k * bw;
+    }
   }
   return n;
 }
@@ -229,8 +239,10 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
                  ? 1
                  : 0;
     p.n_gram += h.gram;
-    h.m_pad = round_up(h.m, ci.tile);
-    h.n_pad = round_up(h.n, ci.tile);
+    h.m_main = main_extent(h.m, ci.tile, ci.strip);
+    h.n_main = main_extent(h.n, ci.tile, ci.strip);
+    h.m_pad = h.m_main < round_up(h.m, ci.tile) ? round_up(h.m, 128) : h.m_main;
+    h.n_pad = h.n_main < round_up(h.n, ci.tile) ? round_up(h.n, 128) : h.n_main;
     if (h.n_pad >= (int64_t(1) << 31)) {
       err = "matrix " + std::to_string(i) + ": padded to the tile, its larger dimension reaches 2^31";
       return MUON_ERR_UNSUPPORTED;
@@ -390,33 +402,54 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
 
     for (int32_t kg = 0; kg < 2 * KC_COUNT; ++kg) {
       const int32_t kc = kg / 2, gram = kg % 2;
-      std::vector<TileEntry> lower, full;
-      std::vector<std::vector<TileEntry>> units;
+      std::vector<TileEntry> lower, full, strip_lower, strip_full;
+      std::vector<std::vector<TileEntry>> units, funits, strip_lunits, strip_funits;
       const int64_t tile = kClasses[kc].tile;
       double fg = 0, fp = 0, fb = 0;
       bool padded = false;
+      // groups consecutive strip tiles into units of up to 8 (one XCD each)
+      auto strip_unit = [](std::vector<std::vector<TileEntry>>& u, const TileEntry& t) {
+        if (u.empty() || u.back().size() == 8 || u.back().back().mat != t.mat) u.emplace_back();
+        u.back().push_back(t);
+      };
       for (int32_t s = 0; s < w.count; ++s) {
         const MatHost& h = p.mats[size_t(p.order[size_t(w.first + s)])];
         if (h.kclass != kc || h.gram != gram) continue;
         const int32_t pos = w.first + s;
         const double m = double(h.m), nn = double(h.n);
-        // a wave block of the 256 tile is 128 rows x 64 columns
-        padded = padded || h.m_pad - h.m >= 64 || h.n_pad - h.n >= 64;
+        // a wave block of the 256 tile is 128 rows x 64 columns (edge strips
+        // lie outside the main extent, whose rows are all real)
+        padded = padded || h.m_main - h.m >= 64 || h.n_main - h.n >= 64;
         fg += m * m * nn;
         fp += m * m * m;
         fb += 2 * m * m * nn;
-        lower_units(units, pos, h.m_pad / tile);
-        emit_full(full, pos, h.m_pad / tile, h.n_pad / tile);
-        const double t2 = double(tile) * double(tile);
-        const int64_t tm = h.m_pad / tile;
-        const double nl = double(tm * (tm + 1) / 2);
+        const int64_t tm = h.m_main / tile, tn = h.n_main / tile;
+        lower_units(units, pos, tm);
+        full_units(funits, pos, tm, tn);
+        // edge strips on 128 tiles: the last 128 rows (the lower row strip of
+        // the square outputs, the whole row strip of the m x n outputs) and
+        // the last 128 columns of the m x n outputs above it
+        const int32_t r = int32_t(h.m_main / 128), c = int32_t(h.n_main / 128);
+        if (h.m_pad > h.m_main) {
+          for (int32_t tj = 0; tj <= r; ++tj) strip_unit(strip_lunits, TileEntry{pos, r, tj});
+          for (int32_t tj = 0; tj < int32_t(h.n_pad / 128); ++tj) strip_unit(strip_funits, TileEntry{pos, r, tj});
+        }
+        if (h.n_pad > h.n_main)
+          for (int32_t ti = 0; ti < r; ++ti) strip_unit(strip_funits, TileEntry{pos, ti, c});
         // the K loops stop at the last 128-byte slab holding real data
         const int64_t bk = kClasses[kc].fp32 ? 32 : 64;
         const double kn = double(round_up(h.n, bk)), km = double(round_up(h.m, bk));
-        p.padded_flops += nl * 2.0 * t2 * kn + nl * 2.0 * t2 * km + double(tm * (h.n_pad / tile)) * 2.0 * t2 * km;
+        const double mp = double(h.m_pad), np = double(h.n_pad), mmain = double(tm * tile);
+        // lower tiles: the main triangle in tiles, the strip row in 128 tiles
+        const double t2 = double(tile) * double(tile);
+        const double sq = double(tm * (tm + 1) / 2) * t2 + (h.m_pad > h.m_main ? (mp - mmain) * mp : 0.0);
+        p.padded_flops += sq * 2.0 * kn + sq * 2.0 * km + mp * np * 2.0 * km;
       }
-      if (full.empty()) continue;
+      if (funits.empty() && strip_funits.empty()) continue;
       interleave_units(lower, units);
+      interleave_units(full, funits);
+      interleave_units(strip_lower, strip_lunits);
+      interleave_units(strip_full, strip_funits);
       ClassLaunch cl{};
       cl.kclass = kc;
       cl.gram = gram;
@@ -430,6 +463,13 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
       cl.full_off = int64_t(p.h_tiles.size());
       cl.n_full = int32_t(full.size());
       p.h_tiles.insert(p.h_tiles.end(), full.begin(), full.end());
+      cl.strip_kclass = kClasses[kc].strip;
+      cl.strip_lower_off = int64_t(p.h_tiles.size());
+      cl.n_strip_lower = int32_t(strip_lower.size());
+      p.h_tiles.insert(p.h_tiles.end(), strip_lower.begin(), strip_lower.end());
+      cl.strip_full_off = int64_t(p.h_tiles.size());
+      cl.n_strip_full = int32_t(strip_full.size());
+      p.h_tiles.insert(p.h_tiles.end(), strip_full.begin(), strip_full.end());
       w.launches.push_back(cl);
     }
   }

@@ -11,6 +11,7 @@
 // under fp16).  Prints "OK" or the first violation.
 // Arguments: precision, wave_bytes, gram_min_aspect.
 #include <algorithm>
+#include <cmath>
 #include <cstdio>
 #include <cstdlib>
 #include <map>
@@ -105,29 +106,83 @@ int main(int argc, char** argv) {
     if (w.ws_bytes > p.ws_bytes) return fail("wave larger than plan workspace");
     for (const ClassLaunch& cl : w.launches) {
       const int tile = class_info(cl.kclass).tile;
-      std::map<int, std::set<std::pair<int, int>>> lower, full;
-      for (int t = 0; t < cl.n_lower; ++t) {
-        const TileEntry& e = p.h_tiles[size_t(cl.lower_off + t)];
-        if (!lower[e.mat].insert({e.ti, e.tj}).second) return fail("duplicate lower tile");
+      // every tile as a rectangle of 64 x 64 cells: (mat, cell row, cell col,
+      // cells per side)
+      struct Rect { int mat; long long r, c, k; };
+      std::vector<Rect> lower, full;
+      auto add = [&](std::vector<Rect>& v, int64_t off, int32_t cnt, int t) {
+        for (int32_t i = 0; i < cnt; ++i) {
+          const TileEntry& e = p.h_tiles[size_t(off + i)];
+          v.push_back(Rect{e.mat, (long long)e.ti * (t / 64), (long long)e.tj * (t / 64), t / 64});
+        }
+      };
+      add(lower, cl.lower_off, cl.n_lower, tile);
+      add(full, cl.full_off, cl.n_full, tile);
+      if (cl.n_strip_lower || cl.n_strip_full) {
+        if (cl.strip_kclass < 0 || class_info(cl.strip_kclass).tile != 128 || tile != 256 ||
+            class_info(cl.strip_kclass).f16 != class_info(cl.kclass).f16 || class_info(cl.strip_kclass).fp32)
+          return fail("strip class");
+        add(lower, cl.strip_lower_off, cl.n_strip_lower, 128);
+        add(full, cl.strip_full_off, cl.n_strip_full, 128);
       }
-      for (int t = 0; t < cl.n_full; ++t) {
-        const TileEntry& e = p.h_tiles[size_t(cl.full_off + t)];
-        if (!full[e.mat].insert({e.ti, e.tj}).second) return fail("duplicate full tile");
-      }
+      std::map<int, std::vector<int>> lcells, fcells;
       for (int s = 0; s < w.count; ++s) {
         const int pos = w.first + s;
         const MatHost& h = p.mats[size_t(p.order[size_t(pos)])];
-        if (h.kclass != cl.kclass || h.gram != cl.gram) {
-          if (lower.count(pos) || full.count(pos)) return fail("tile of another class or form");
-          continue;
+        if (h.kclass != cl.kclass || h.gram != cl.gram) continue;
+        if (h.m_pad % 64 || h.n_pad % 64 || h.m_pad < h.m || h.n_pad < h.n) return fail("padded extent");
+        // the 256 part of an edge-strip matrix ends exactly 128 before the
+        // padded extent, which is the extent rounded to 128
+        // per dimension: either padded to the tile, or (256 classes) to 128
+        // with the 256 part ending 128 before it, after at least one tile
+        const long long ext[2][3] = {{h.m, h.m_pad, h.m_main}, {h.n, h.n_pad, h.n_main}};
+        for (const auto& e : ext) {
+          if (e[2] == e[1]) {
+            if (e[1] % tile || e[1] - e[0] >= tile) return fail("tile padding");
+          } else if (tile != 256 || e[1] != (e[0] + 127) / 128 * 128 || e[2] != e[1] - 128 || e[2] % 256 ||
+                     e[2] < 256) {
+            return fail("edge-strip extents");
+          }
         }
-        const int tm = int(h.m_pad / tile), tn = int(h.n_pad / tile);
-        if (int(full[pos].size()) != tm * tn) return fail("full tile count");
-        if (int(lower[pos].size()) != tm * (tm + 1) / 2) return fail("lower tile count");
-        for (const auto& t : full[pos])
-          if (t.first >= tm || t.second >= tn) return fail("full tile out of range");
-        for (const auto& t : lower[pos])
-          if (t.first >= tm || t.second > t.first) return fail("lower tile out of range");
+        lcells[pos].assign(size_t(h.m_pad / 64) * size_t(h.m_pad / 64), 0);
+        fcells[pos].assign(size_t(h.m_pad / 64) * size_t(h.n_pad / 64), 0);
+      }
+      // full outputs: every cell of m_pad x n_pad exactly once
+      for (const Rect& t : full) {
+        auto it = fcells.find(t.mat);
+        if (it == fcells.end()) return fail("tile of another class or form");
+        const MatHost& h = p.mats[size_t(p.order[size_t(t.mat)])];
+        const long long cm = h.m_pad / 64, cn = h.n_pad / 64;
+        if (t.r + t.k > cm || t.c + t.k > cn) return fail("full tile out of range");
+        for (long long i = t.r; i < t.r + t.k; ++i)
+          for (long long j = t.c; j < t.c + t.k; ++j)
+            if (++it->second[size_t(i * cn + j)] != 1) return fail("duplicate full tile");
+      }
+      // symmetric outputs: each tile is a diagonal block or lies strictly
+      // below the diagonal, and every cell is computed exactly once directly
+      // or through its mirror
+      for (const Rect& t : lower) {
+        auto it = lcells.find(t.mat);
+        if (it == lcells.end()) return fail("tile of another class or form");
+        const MatHost& h = p.mats[size_t(p.order[size_t(t.mat)])];
+        const long long cm = h.m_pad / 64;
+        if (t.r + t.k > cm || t.c + t.k > cm) return fail("lower tile out of range");
+        const bool diag = t.r == t.c;
+        if (!diag && t.r < t.c + t.k) return fail("lower tile not below the diagonal");
+        for (long long i = t.r; i < t.r + t.k; ++i)
+          for (long long j = t.c; j < t.c + t.k; ++j) {
+            if (diag && j > i) continue;   // counted through its mirror cell
+            if (++it->second[size_t(i * cm + j)] != 1) return fail("duplicate lower tile");
+          }
+      }
+      for (const auto& kv : fcells)
+        for (int v : kv.second)
+          if (v != 1) return fail("full outputs not covered");
+      for (const auto& kv : lcells) {
+        const long long cm = (long long)std::llround(std::sqrt(double(kv.second.size())));
+        for (long long i = 0; i < cm; ++i)
+          for (long long j = 0; j <= i; ++j)
+            if (kv.second[size_t(i * cm + j)] != 1) return fail("symmetric outputs not covered");
       }
     }
   }
@@ -144,9 +199,15 @@ int main(int argc, char** argv) {
       groups.insert({h.kclass, h.gram});
     }
     launches += 2;
-    // k = 5: Eq. 2 runs 3 launches per step; the Gram-space form, in
-    // segments of 2, 2 and 1 steps, 7 + 7 + 3
-    for (const auto& g : groups) launches += g.second ? 17 : 15;
+    // k = 5: Eq. 2 runs 2 lower-tile launches and one B*X per step; the
+    // Gram-space form, in segments of 2, 2 and 1 steps, 6 + 6 + 2 lower-tile
+    // launches and 3 B*X; a group with edge strips doubles the launches of
+    // the kind its strips have
+    for (const ClassLaunch& cl : w.launches) {
+      const long long lw = cl.n_strip_lower ? 2 : 1, bw = cl.n_strip_full ? 2 : 1;
+      launches += cl.gram ? 14 * lw + 3 * bw : 10 * lw + 5 * bw;
+    }
+    if (groups.size() != w.launches.size()) return fail("one launch group per (class, form)");
   }
   if (launches != launches_per_step(p, 5)) return fail("launches per step");
   std::printf("OK %zu matrices %zu waves %zu tiles\n", descs.size(), p.waves.size(), p.h_tiles.size());

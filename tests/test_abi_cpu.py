@@ -92,7 +92,9 @@ def test_host_only_plan_of_each_workload(key):
         mi = plan.matrix_info(i)
         assert mi["m"] == min(m.rows, m.cols) and mi["n"] == max(m.rows, m.cols)
         assert mi["transposed"] == int(m.rows > m.cols)
-        assert mi["m_pad"] % mi["tile"] == 0 and mi["n_pad"] % mi["tile"] == 0
+        # padded to the tile, or (256 tiles) to 128 with a 128-wide edge strip
+        for v, pad in ((mi["m"], mi["m_pad"]), (mi["n"], mi["n_pad"])):
+            assert pad >= v and (pad % mi["tile"] == 0 or (mi["tile"] == 256 and pad % 128 == 0 and pad - v < 128))
         assert mi["m"] <= mi["m_pad"] < mi["m"] + mi["tile"]
         assert mi["n"] <= mi["n_pad"] < mi["n"] + mi["tile"]
         assert mi["fp32_ns"] == int(mi["m"] <= 64)
@@ -292,9 +294,13 @@ def test_tile_choice_prices_the_k_loop_at_the_real_extent():
     # 1152 x 1152: 256 tile 4 * 1280^2 * 1152 = 7.55e9; 128 tile 4 * 1152^3 / 0.8 = 7.64e9
     # 640 x 640:   256 tile 4 * 768^2 * 640 = 1.51e9;   128 tile 4 * 640^3 / 0.8 = 1.31e9
     # (pricing K at the padded extent, as the loops once ran, chose 128 for 1152)
+    # With edge strips a 256-class 640 x 640 matrix pads to 640 only: its
+    # 512 x 512 part at 1.0 and the rest (640^2 - 512^2 of the outputs) at the
+    # 128 class's 0.8: 2560 * (512^2 + (640^2 - 512^2) / 0.8) = 1.14e9 < 1.31e9.
     plan = MuonPlan([(1152, 1152, "bf16", "bf16"), (3456, 1152, "bf16", "bf16"), (640, 640, "bf16", "bf16"),
-                     (4096, 4096, "bf16", "bf16")], host_only=True)
-    assert [plan.matrix_info(i)["tile"] for i in range(4)] == [256, 256, 128, 256]
+                     (4096, 4096, "bf16", "bf16"), (300, 300, "bf16", "bf16")], host_only=True)
+    assert [plan.matrix_info(i)["tile"] for i in range(5)] == [256, 256, 256, 256, 256]
+    assert [plan.matrix_info(i)["m_pad"] for i in range(5)] == [1152, 1152, 640, 4096, 384]
     plan.close()
 
 

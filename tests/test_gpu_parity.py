@@ -126,6 +126,31 @@ def test_long_thin_matrices(precision):
     assert_parity(res, precision, "long-thin")
 
 
+STRIP_SET = [(1408, 2048), (2048, 1408), (1152, 3456), (3456, 1152), (640, 1100), (1408, 1408), (300, 2000),
+             (1000, 1000)]
+
+
+@pytest.mark.parametrize("precision", ["bf16", "fp16"])
+@pytest.mark.parametrize("aspect", [0.0, 1.4])
+def test_edge_strips(precision, aspect):
+    # 256-tile matrices whose extents end 128 or fewer past a multiple of 256
+    # are padded to 128, and their last 128 rows or columns run on the 128
+    # class after each 256-tile launch (1408 = 5 x 256 + 128, 1152, 3456,
+    # 1100 -> 1152, 640, 300 -> 384; 2000 and 1000 have none).  Both forms.
+    wl = custom_workload(STRIP_SET, seed=25)
+    plan = MuonPlan([(m.rows, m.cols, m.param, m.grad, 256) for m in wl.matrices], precision=precision,
+                    gram_min_aspect=aspect)
+    info = [plan.matrix_info(i) for i in range(wl.n)]
+    assert [(i["m_pad"], i["n_pad"]) for i in info] == [
+        (1408, 2048), (1408, 2048), (1152, 3456), (1152, 3456), (640, 1152), (1408, 1408), (384, 2048),
+        (1024, 1024)]
+    _banner(f"edge strips {precision} aspect {aspect}: {plan.info()['n_gram']} Gram-space matrices")
+    res = run_parity(wl, precision=precision, steps=2, plan=plan)
+    _banner(f"edge strips {precision} aspect {aspect}: {res.summary()}")
+    plan.close()
+    assert_parity(res, precision, "edge strips")
+
+
 def test_ragged_shapes_small_waves():
     # every matrix in a wave of its own: same results as the single-wave plan
     wl = custom_workload(RAGGED, seed=12)
