@@ -257,7 +257,21 @@ def cpu_baseline(wl, budget_s: float):
             sampled.append(f"{m}x{n} extrapolated by flops")
     return {"value": round(total_ms, 1), "unit": "ms", "cores": int(threads), "kind": "oracle",
             "sample": ("fp64 numpy oracle, one matrix per shape bucket, one step each ("
-                       + "; ".join(sampled) + "), scaled by bucket counts to the whole set")}
+                       + "; ".join(sampled) + "), scaled by bucket counts to the whole set"),
+            "cpu_model": cpu_model(), "affinity_cores": len(os.sched_getaffinity(0)),
+            "blas_threads": int(threads)}
+
+
+def cpu_model() -> str:
+    """The host CPU's model name (from /proc/cpuinfo), or '' if unknown."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return ""
 
 
 GRAM_MIN_M = 256      # smaller matrices stay on Eq. 2
