@@ -40,6 +40,8 @@ def kernel_sources_hash() -> str:
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2606_27153_amd", "csrc")
     for name in sorted(os.listdir(csrc)):
+        if not os.path.isfile(os.path.join(csrc, name)):
+            continue  # diag/: the ceiling probe, not a kernel the traffic was taken on
         with open(os.path.join(csrc, name), "rb") as f:
             h.update(name.encode() + f.read())
     return h.hexdigest()[:16]
@@ -356,10 +358,41 @@ def measure_peaks(torch, dev, copy_mib: int = 1024, reps: int = 5) -> dict:
     z = torch.empty(batch, m, n, device=dev, dtype=torch.bfloat16)
     t_mm = timed(lambda: torch.bmm(x, y, out=z))
     del x, y, z
+    ceil = measure_mfma_ceiling(torch, dev, timed)
     return {"hbm_device_copy_gbs": round(2.0 * nb / t_copy / 1e9, 1),
             "bf16_bmm_tflops": round(2.0 * batch * m * n * k / t_mm / 1e12, 1),
+            **ceil,
             "what": f"device-to-device copy of {copy_mib} MiB (read + write bytes); torch.bmm bf16 "
-                    f"{batch} x ({m}x{k} @ {k}x{n}), the vendor BLAS on the B*X shape"}
+                    f"{batch} x ({m}x{k} @ {k}x{n}), the vendor BLAS on the B*X shape; the bf16 matrix-core "
+                    f"rate sustained with no global-memory traffic (libmuon_diag.so): MFMAs alone on random "
+                    f"operands, with the 256-tile K loop's LDS reads (6 per 8 MFMAs), and on constant operands"}
+
+
+DIAG_LIB = os.path.join(ROOT, "paper_2606_27153_amd", "libmuon_diag.so")
+
+
+def measure_mfma_ceiling(torch, dev, timed, blocks: int = 1024, iters: int = 20000) -> dict:
+    """Runs the three modes of muon_diag_mfma_ceiling (4 blocks of 8 waves per
+    CU) and returns their rates in TFLOP/s."""
+    import ctypes
+    if not os.path.exists(DIAG_LIB):
+        raise RuntimeError(f"{DIAG_LIB} is missing: run __graft_entry__.build() first")
+    lib = ctypes.CDLL(DIAG_LIB)
+    fn = lib.muon_diag_mfma_ceiling
+    fn.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    fn.restype = ctypes.c_int
+    out = torch.empty(blocks * 512, dtype=torch.float32, device=dev)
+    stream = ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+    rates = {}
+    for mode, key, nmfma in ((0, "mfma_bf16_random_tflops", 16), (1, "mfma_bf16_lds_mix_tflops", 8),
+                             (2, "mfma_bf16_const_tflops", 16)):
+        def launch():
+            if fn(blocks, iters, mode, ctypes.c_void_p(out.data_ptr()), stream) != 0:
+                raise RuntimeError(f"muon_diag_mfma_ceiling mode {mode} failed")
+        t = timed(launch)
+        rates[key] = round(blocks * 8 * iters * nmfma * 32768.0 / t / 1e12, 1)
+    del out
+    return rates
 
 
 def lpt_partition(costs, n_owners: int):
@@ -677,6 +710,7 @@ def main(argv=None) -> int:
             # the dominant kernel against the vendor BLAS on the same box
             # (box-to-box clock differences move both alike)
             roof["vs_vendor_bf16_bmm"] = round(roof["achieved"] / peaks["bf16_bmm_tflops"], 3)
+            roof["vs_measured_mfma_ceiling"] = round(roof["achieved"] / peaks["mfma_bf16_lds_mix_tflops"], 3)
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] timing the fp64 oracle on a sample of the same set ...")

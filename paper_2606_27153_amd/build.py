@@ -1,4 +1,6 @@
-"""Builds libmuon_mi355x.so for gfx950 with hipcc (in-tree, no JIT cache).
+"""Builds libmuon_mi355x.so (the optimizer) and libmuon_diag.so (a matrix-core
+ceiling probe the bench reports as context) for gfx950 with hipcc, in-tree,
+no JIT cache.
 
 Usage: python -m paper_2606_27153_amd.build [-v]
 """
@@ -18,6 +20,8 @@ LIB_PATH = os.path.join(PKG, LIB_NAME)
 ARCH = "gfx950"
 
 SOURCES = ["api.cpp", "plan.cpp", "ew_kernels.hip", "ns_gemm.hip", "static_ws.hip"]
+DIAG_SOURCES = ["diag/mfma_ceiling.hip"]
+DIAG_LIB_PATH = os.path.join(PKG, "libmuon_diag.so")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
@@ -48,18 +52,24 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD, exist_ok=True)
-    with cf.ThreadPoolExecutor(max_workers=min(4, len(SOURCES))) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
-    tmp = LIB_PATH + ".tmp"
+def _link(objs, path: str, verbose: bool) -> None:
+    tmp = path + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}{r.stderr}")
-    os.replace(tmp, LIB_PATH)
+    os.replace(tmp, path)
+
+
+def build(verbose: bool = False) -> str:
+    os.makedirs(BUILD, exist_ok=True)
+    srcs = SOURCES + DIAG_SOURCES
+    with cf.ThreadPoolExecutor(max_workers=4) as ex:
+        objs = list(ex.map(lambda s: _compile(s, verbose), srcs))
+    _link(objs[:len(SOURCES)], LIB_PATH, verbose)
+    _link(objs[len(SOURCES):], DIAG_LIB_PATH, verbose)
     return LIB_PATH
 
 

@@ -357,3 +357,18 @@ def test_step_path_never_waits_for_the_stream():
     for call in ("hipStreamSynchronize", "hipDeviceSynchronize", "hipMemcpy(", "hipMalloc", "hipHostMalloc",
                  "hipFree"):
         assert call not in body, call
+
+
+def test_diag_library_exports_the_ceiling_probe():
+    """The bench's matrix-core ceiling probe lives in its own library; its
+    argument checks run before any HIP call."""
+    from paper_2606_27153_amd.build import DIAG_LIB_PATH
+    diag = ctypes.CDLL(DIAG_LIB_PATH)
+    fn = diag.muon_diag_mfma_ceiling
+    fn.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    fn.restype = ctypes.c_int
+    dummy = ctypes.c_void_p(16)
+    assert fn(0, 10, 0, dummy, None) == -1
+    assert fn(4, 0, 0, dummy, None) == -1
+    assert fn(4, 10, 3, dummy, None) == -1
+    assert fn(4, 10, 0, None, None) == -1

@@ -157,3 +157,11 @@ def test_live_flop_share():
     assert share[("symm", cls)] == pytest.approx(1.0)   # only the Gram-space matrix has symmetric products
     assert share[("bx", cls)] == pytest.approx(3 * 2 * 1024 ** 2 * 4096 / (3 * 2 * 1024 ** 2 * 4096 + 5 * 2 * 1024 ** 3))
     plan.close()
+
+
+def test_kernel_sources_hash_covers_files_only():
+    """The hash that keys the committed traffic summary reads the kernel
+    source files and passes over sub-directories (the diagnostic probe)."""
+    import re
+    h = bench.kernel_sources_hash()
+    assert re.fullmatch(r"[0-9a-f]{16}", h)
