@@ -33,7 +33,7 @@ struct ClassInfo {
   int32_t fp32;     // operands stored as fp32 (else 16-bit)
   int32_t f16;      // 16-bit operands are fp16 (else bf16)
   const char* name;
-  int32_t strip;    // 256 classes: the 128 class that computes their edge strips (else -1)
+  int32_t strip;    // 256 classes: the 128 class that computes their column edge strips (else -1)
 };
 
 const ClassInfo& class_info(int32_t kc);
@@ -72,7 +72,13 @@ struct MatDev {
 struct TileEntry {
   int32_t mat;     // index into the MatDev array (global, wave order)
   int32_t ti, tj;  // output tile row and column
+  int32_t flags;   // kTileHalf: only the first half of the tile's rows
 };
+// A 256 tile of a square (m x m) output of which only the top 128 rows
+// exist: the row strip of a matrix whose m ends 128 or fewer past a multiple
+// of 256.  Its operand panels hold 128 real rows (the padded extent ends
+// there) and its 8 waves share those rows, 64 each (see ns_gemm.hip).
+constexpr int32_t kTileHalf = 1;
 
 // Per-matrix device pointers, refreshed when the caller's buffers change.
 struct PtrEntry {
@@ -116,11 +122,10 @@ struct ClassLaunch {
   int64_t full_off;    // TileEntry offset of the full list
   int32_t n_full;
   bool padded;         // some matrix is padded by a whole wave block (rows or columns)
-  // edge-strip tiles (in units of the strip class's 128 tile), launched
-  // with that class after each main launch
+  // edge strips of the B*X outputs (tiles in units of the strip class's 128
+  // tile), launched with that class after each main B*X launch; the square
+  // outputs' row strips are half tiles among their lower tiles
   int32_t strip_kclass;
-  int64_t strip_lower_off;
-  int32_t n_strip_lower;
   int64_t strip_full_off;
   int32_t n_strip_full;
 };

@@ -128,6 +128,15 @@ struct Cfg {
   static_assert(CPW >= 1 && TILE_ / 8 % NW == 0, "tile too small for the block");
 };
 
+// The 256 tile's 8 waves on a half tile (128 real rows): 2 x 4 pieces of
+// 64 x 64, i.e. the wave tile of C with half its rows.  The slab layout and
+// loads are C's.
+template <class C>
+struct HalfCfg : C {
+  static constexpr int WTM = C::WTM / 2;
+  static constexpr int NBM = C::NBM / 2;
+};
+
 // One direct-to-LDS 16-byte load per lane: lane l's 16 bytes from g land at
 // LDS byte lds + 16*l.  Written as inline assembly: the compiler counts the
 // builtin's LDS write against the LDS-read counter as an out-of-order event
@@ -158,6 +167,20 @@ template <class C, typename E>
 __device__ __forceinline__ void load_slab(const E* src, int64_t K, int kt, char* lds, int wid) {
 #pragma unroll
   for (int i = 0; i < C::CPW; ++i) {
+    const E* g = src + int64_t(i) * (8 * C::NW) * K + int64_t(kt) * C::BK;
+    dma16(g, lds + (wid + C::NW * i) * 1024);
+  }
+}
+
+// The same for a slab of which only the first nchunk chunks per wave exist
+// (nchunk wave-uniform): chunk i covers rows 8 (wid + NW i) .. + 7, so
+// nchunk = CPW / 2 loads the first half of the rows.  The rest of the LDS
+// slab keeps whatever it held.
+template <class C, typename E>
+__device__ __forceinline__ void load_slab_part(const E* src, int64_t K, int kt, char* lds, int wid, int nchunk) {
+#pragma unroll
+  for (int i = 0; i < C::CPW; ++i) {
+    if (i >= nchunk) break;
     const E* g = src + int64_t(i) * (8 * C::NW) * K + int64_t(kt) * C::BK;
     dma16(g, lds + (wid + C::NW * i) * 1024);
   }
@@ -265,6 +288,11 @@ __device__ __forceinline__ void slab_body(const char* st, const int (&oa)[4], co
 template <bool B>
 struct BoolTag {
   static constexpr bool value = B;
+};
+
+template <class T>
+struct TypeTag {
+  typedef T type;
 };
 
 __device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
@@ -499,10 +527,12 @@ struct ApplyLay {
   }
 };
 
+// rows: bit i set when MFMA block row i of the wave tile is the wave's to
+// apply (a half tile's waves each own half of theirs).
 template <class C, bool TRANS, typename P>
 __device__ __forceinline__ void apply_via_lds(const f32x16 (&acc)[C::NBM][C::NBN], char* region,
                                               const PtrEntry& pe, const MatDev& d, float lrs, float decay,
-                                              int64_t row0, int64_t col0, int lane) {
+                                              int64_t row0, int64_t col0, int lane, uint32_t rows = ~0u) {
   using A = ApplyLay<C, TRANS>;
   const int64_t srow_end = TRANS ? col0 + C::WTN : row0 + C::WTM;
   const int64_t scol_end = TRANS ? row0 + C::WTM : col0 + C::WTN;
@@ -515,6 +545,7 @@ __device__ __forceinline__ void apply_via_lds(const f32x16 (&acc)[C::NBM][C::NBN
     for (int pass = 0; pass < A::NPASS; ++pass)
 #pragma unroll
       for (int it = 0; it < A::NP; ++it) {
+        if (!((rows >> (pass >> 1)) & 1u)) continue;
         int off;
         int64_t row, col;
         A::at(pass, lane + 64 * it, row0, col0, off, row, col);
@@ -522,6 +553,7 @@ __device__ __forceinline__ void apply_via_lds(const f32x16 (&acc)[C::NBM][C::NBN
       }
 #pragma unroll
     for (int pass = 0; pass < A::NPASS; ++pass) {
+      if (!((rows >> (pass >> 1)) & 1u)) continue;
       A::stage(acc, region, pass >> 1, pass & 1, lane);
       __builtin_amdgcn_s_waitcnt(0xc07f);
 #pragma unroll
@@ -542,6 +574,7 @@ __device__ __forceinline__ void apply_via_lds(const f32x16 (&acc)[C::NBM][C::NBN
   }
 #pragma unroll
   for (int pass = 0; pass < A::NPASS; ++pass) {
+    if (!((rows >> (pass >> 1)) & 1u)) continue;
     A::stage(acc, region, pass >> 1, pass & 1, lane);
     apply_pass<P, A::NP>(region, pe, d, lrs, decay, lane, [&](int piece, int& off, int64_t& row, int64_t& col) {
       A::at(pass, piece, row0, col0, off, row, col);
@@ -757,10 +790,45 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
   // launches the second store pass costs more than the skipped blocks save.)
   constexpr bool DSPLIT = TILE == 256 && WGM == 2 && WGN == 4 && sizeof(E) == 2 && STAGE != ST_BX;
   const bool dtile = DSPLIT && ti == tj && args.mats[te.mat].m_pad > TILE;
+  // A half tile (kTileHalf: the row strip of a matrix whose padded m ends 128
+  // rows into this tile) has only its top 128 rows, and its own operand
+  // panel (on the diagonal of a square output, the other one too) only 128
+  // rows in memory: those slab loads fetch half the rows.  Off the diagonal
+  // the 8 waves run an unmasked K loop on 64 x 64 pieces (HalfCfg): waves 0-3
+  // take the top 64 rows of column pieces 0-3, waves 4-7 the next 64, so each
+  // SIMD carries 8 block streams, half a full tile's; their blocks sit in
+  // acc[0..1][*] and are stored like an off-diagonal tile's.  The diagonal
+  // half tile (one per strip row) keeps the 128 x 64 pieces and computes, in
+  // the masked K loop, the blocks of its real 128 x 128 part on or below the
+  // diagonal, stored like a diagonal tile's.
+  constexpr bool HSPLIT = TILE == 256 && WGM == 2 && WGN == 4 && sizeof(E) == 2;
+  const bool htile = HSPLIT && STAGE != ST_BX && (te.flags & kTileHalf) != 0;
+  const bool hfast = htile && !dtile;
   int wm = wid / WGN, wn = wid % WGN;
-  uint32_t bmask = 0, rmask = 0;  // diagonal tile: blocks to compute / to store as computed
+  int wrow = wm * C::WTM;  // first row of the wave's piece within the tile
+  uint32_t bmask = 0, rmask = 0;  // masked tiles: blocks to compute / to store as computed
   bool dlive = true;
-  if (dtile) {
+  if (hfast) {
+    wm = 0;
+    wn = wid & 3;
+    wrow = (wid >> 2) * HalfCfg<C>::WTM;
+    bmask = rmask = (1u << (HalfCfg<C>::NBM * C::NBN)) - 1u;  // acc[0..1][*]
+  } else if (htile) {
+    wm = 0;
+    wn = wid & 3;
+    wrow = 0;  // the 128 x 64 piece at the top; the mask picks the wave's rows
+    const int hr = wid >> 2;
+#pragma unroll
+    for (int i = 0; i < C::NBM; ++i)
+#pragma unroll
+      for (int j = 0; j < C::NBN; ++j) {
+        const int rb = i, cb = wn * C::NBN + j;
+        if ((i >> 1) != hr) continue;
+        if (rb >= cb) bmask |= 1u << (i * C::NBN + j);
+        if (rb > cb) rmask |= 1u << (i * C::NBN + j);
+      }
+    dlive = bmask != 0;
+  } else if (dtile) {
     switch (wid) {  // wave -> (row piece, column piece)
       case 0: wm = 1; wn = 0; break;
       case 1: wm = 1; wn = 1; break;
@@ -770,6 +838,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
       case 5: wm = 1; wn = 3; break;
       default: wm = 0; wn = 0; dlive = false; break;
     }
+    wrow = wm * C::WTM;
     if (dlive) {
 #pragma unroll
       for (int i = 0; i < C::NBM; ++i)
@@ -781,6 +850,13 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
         }
     }
   }
+  // the epilogue's masked stores serve diagonal and half tiles
+  const bool masked = htile || dtile;
+  // MFMA block rows that hold the wave's results (the apply's pass mask)
+  uint32_t arows = 0;
+#pragma unroll
+  for (int i = 0; i < C::NBM; ++i)
+    if ((bmask >> (i * C::NBN)) & ((1u << C::NBN) - 1u)) arows |= 1u << i;
   const int64_t mp = d.m_pad, np = d.n_pad;
 
   const E* opa;
@@ -830,129 +906,126 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
   // end) are folded in while the slab holding them is in LDS.
   const bool FUSE = (STAGE == ST_POLY || STAGE == ST_BX) && args.fcoef != 0.f;
   const float fcoef = args.fcoef;
-  const int frow0 = ti * TILE + wm * C::WTM;
+  const int frow0 = ti * TILE + wrow;
   const bool live = !PAD || (int64_t(frow0) < d.m &&
                              int64_t(tj) * TILE + wn * C::WTN <
                                  (STAGE == ST_BX ? int64_t(d.rows > d.cols ? d.rows : d.cols) : int64_t(d.m)));
-  if (!zero) {
-    if constexpr (TRB) {
-      const E* srca = lane_src<C>(opa, K, wid, lane);
-      const E* srcb = lane_src_rows<C, E>(opb, np, wid, lane);
-      int oa[4], ot[2 * C::NBN];
+  // One K loop over configuration CC (C, or HalfCfg<C> for the unmasked half
+  // tiles) with accumulators a.  M: MFMA blocks masked by bmask (diagonal
+  // tiles).  PA / PB: the first / second operand's slabs hold only their
+  // first 128 rows.  TB: the second operand is row-major X (transposing
+  // reads).
+  auto kloop = [&](auto cc_tag, auto m_tag, auto pa_tag, auto pb_tag, auto& a) {
+    using CC = typename decltype(cc_tag)::type;
+    constexpr bool M = decltype(m_tag)::value, PA = decltype(pa_tag)::value, PB = decltype(pb_tag)::value;
+    constexpr bool TB = TRB;
+    const E* srca = lane_src<C>(opa, K, wid, lane);
+    const E* srcb;
+    if constexpr (TB)
+      srcb = lane_src_rows<C, E>(opb, np, wid, lane);
+    else
+      srcb = lane_src<C>(opb, K, wid, lane);
+    int oa[4], ob[4], ot[2 * C::NBN];
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) oa[ks] = frag_off(wm * C::WTM, lane, ks);
-      tr_offsets<C>(wn, lane, ot);
-      typename Frag<E>::T fa0[C::NBM], fb0[C::NBN], fa1[C::NBM], fb1[C::NBN];
-      load_slab<C>(srca, K, 0, stage0, wid);
-      load_slab_rows<C>(srcb, np, 0, stage0 + C::OPB, wid);
+    for (int ks = 0; ks < 4; ++ks) {
+      oa[ks] = frag_off(wrow, lane, ks);
+      ob[ks] = frag_off(wn * C::WTN, lane, ks);
+    }
+    if constexpr (TB) tr_offsets<C>(wn, lane, ot);
+    auto load = [&](int kt, char* st) {
+      if constexpr (PA)
+        load_slab_part<C>(srca, K, kt, st, wid, C::CPW / 2);
+      else
+        load_slab<C>(srca, K, kt, st, wid);
+      if constexpr (TB)
+        load_slab_rows<C>(srcb, np, kt, st + C::OPB, wid);
+      else if constexpr (PB)
+        load_slab_part<C>(srcb, K, kt, st + C::OPB, wid, C::CPW / 2);
+      else
+        load_slab<C>(srcb, K, kt, st + C::OPB, wid);
+    };
+    typename Frag<E>::T fa0[CC::NBM], fb0[CC::NBN], fa1[CC::NBM], fb1[CC::NBN];
+    // fp32 operands: each slab's products are summed into a zeroed partial
+    // accumulator, which is added to the result after the slab.  This
+    // two-level sum keeps the rounding error of long K loops (K = n up to
+    // 14336 for the Gram product) near sqrt(K / 32) + sqrt(32) roundings
+    // instead of sqrt(K / 2), the chain of one accumulator through every
+    // 32x32x2 step.  The 16-bit classes accumulate directly.
+    f32x16 part[CC::NBM][CC::NBN];
+    if constexpr (sizeof(E) == 4) {
+#pragma unroll
+      for (int i = 0; i < CC::NBM; ++i)
+#pragma unroll
+        for (int j = 0; j < CC::NBN; ++j)
+#pragma unroll
+          for (int q = 0; q < 16; ++q) part[i][j][q] = 0.f;
+    }
+    auto first_frags = [&](const char* st) {
+      if constexpr (TB)
+        read_frags_tr<CC, E>(st, st + C::OPB, oa[0], ot, 0, fa0, fb0);
+      else
+        read_frags<CC, E>(st, st + C::OPB, oa[0], ob[0], fa0, fb0);
+    };
+    auto body = [&](const char* st, int kt) {
+      if constexpr (TB) {
+        slab_body_tr<CC, E>(st, oa, ot, fa0, fb0, fa1, fb1, a);
+      } else if constexpr (sizeof(E) == 4) {
+        slab_body<CC, E, M>(st, oa, ob, fa0, fb0, fa1, fb1, part, bmask);
+#pragma unroll
+        for (int i = 0; i < CC::NBM; ++i)
+#pragma unroll
+          for (int j = 0; j < CC::NBN; ++j)
+#pragma unroll
+            for (int q = 0; q < 16; ++q) {
+              a[i][j][q] += part[i][j][q];
+              part[i][j][q] = 0.f;
+            }
+      } else {
+        slab_body<CC, E, M>(st, oa, ob, fa0, fb0, fa1, fb1, a, bmask);
+      }
+      if (FUSE) fuse_input<CC, E, TB>(st + C::OPB, kt, frow0, wn, lane, fcoef, a);
+    };
+    load(0, stage0);
+    wait_vm_all();
+    __syncthreads();
+    if (live) first_frags(stage0);
+    int kt = 0;
+    for (; kt + 2 <= nk; kt += 2) {
+      load(kt + 1, stage1);
+      if (live) body(stage0, kt);
       wait_vm_all();
       __syncthreads();
-      if (live) read_frags_tr<C, E>(stage0, stage0 + C::OPB, oa[0], ot, 0, fa0, fb0);
-      int kt = 0;
-      for (; kt + 2 <= nk; kt += 2) {
-        load_slab<C>(srca, K, kt + 1, stage1, wid);
-        load_slab_rows<C>(srcb, np, kt + 1, stage1 + C::OPB, wid);
-        if (live) slab_body_tr<C, E>(stage0, oa, ot, fa0, fb0, fa1, fb1, acc);
-        if (FUSE && live) fuse_input<C, E, true>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
-        wait_vm_all();
-        __syncthreads();
-        if (live) read_frags_tr<C, E>(stage1, stage1 + C::OPB, oa[0], ot, 0, fa0, fb0);
-        __builtin_amdgcn_sched_barrier(0);
-        if (kt + 2 < nk) {
-          load_slab<C>(srca, K, kt + 2, stage0, wid);
-          load_slab_rows<C>(srcb, np, kt + 2, stage0 + C::OPB, wid);
-        }
-        if (live) slab_body_tr<C, E>(stage1, oa, ot, fa0, fb0, fa1, fb1, acc);
-        if (FUSE && live) fuse_input<C, E, true>(stage1 + C::OPB, kt + 1, frow0, wn, lane, fcoef, acc);
-        wait_vm_all();
-        __syncthreads();
-        if (kt + 2 < nk && live) read_frags_tr<C, E>(stage0, stage0 + C::OPB, oa[0], ot, 0, fa0, fb0);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-      if (kt < nk) {  // odd slab count: the last slab is in stage 0
-        if (live) slab_body_tr<C, E>(stage0, oa, ot, fa0, fb0, fa1, fb1, acc);
-        if (FUSE && live) fuse_input<C, E, true>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
-        __syncthreads();
+      if (live) first_frags(stage1);
+      __builtin_amdgcn_sched_barrier(0);
+      if (kt + 2 < nk) load(kt + 2, stage0);
+      if (live) body(stage1, kt + 1);
+      wait_vm_all();
+      __syncthreads();
+      if (kt + 2 < nk && live) first_frags(stage0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (kt < nk) {  // odd slab count: the last slab is in stage 0
+      if (live) body(stage0, kt);
+      __syncthreads();
+    }
+  };
+  if (!zero) {
+    using T = BoolTag<true>;
+    using F = BoolTag<false>;
+    if constexpr (HSPLIT && STAGE != ST_BX) {
+      if (hfast) {
+        // the 64 x 64 pieces' accumulators are acc[0..1][*]
+        auto& acc2 = reinterpret_cast<f32x16(&)[HalfCfg<C>::NBM][C::NBN]>(acc);
+        kloop(TypeTag<HalfCfg<C>>{}, F{}, T{}, F{}, acc2);
+      } else if (htile) {
+        kloop(TypeTag<C>{}, T{}, T{}, T{}, acc);
+      } else if (dtile) {
+        kloop(TypeTag<C>{}, T{}, F{}, F{}, acc);
+      } else {
+        kloop(TypeTag<C>{}, F{}, F{}, F{}, acc);
       }
     } else {
-      const E* srca = lane_src<C>(opa, K, wid, lane);
-      const E* srcb = lane_src<C>(opb, K, wid, lane);
-      int oa[4], ob[4];
-    #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        oa[ks] = frag_off(wm * C::WTM, lane, ks);
-        ob[ks] = frag_off(wn * C::WTN, lane, ks);
-      }
-      typename Frag<E>::T fa0[C::NBM], fb0[C::NBN], fa1[C::NBM], fb1[C::NBN];
-      // fp32 operands: each slab's products are summed into a zeroed partial
-      // accumulator, which is added to acc after the slab.  This two-level
-      // sum keeps the rounding error of long K loops (K = n up to 14336 for
-      // the Gram product) near sqrt(K / 32) + sqrt(32) roundings instead of
-      // sqrt(K / 2), the chain of one accumulator through every
-      // 32x32x2 step.  The 16-bit classes accumulate directly.
-      f32x16 part[C::NBM][C::NBN];
-      if constexpr (sizeof(E) == 4) {
-#pragma unroll
-        for (int i = 0; i < C::NBM; ++i)
-#pragma unroll
-          for (int j = 0; j < C::NBN; ++j)
-#pragma unroll
-            for (int q = 0; q < 16; ++q) part[i][j][q] = 0.f;
-      }
-      auto body = [&](const char* st, auto masked) {
-        constexpr bool M = decltype(masked)::value;
-        if constexpr (sizeof(E) == 4) {
-          slab_body<C, E, M>(st, oa, ob, fa0, fb0, fa1, fb1, part, bmask);
-#pragma unroll
-          for (int i = 0; i < C::NBM; ++i)
-#pragma unroll
-            for (int j = 0; j < C::NBN; ++j)
-#pragma unroll
-              for (int q = 0; q < 16; ++q) {
-                acc[i][j][q] += part[i][j][q];
-                part[i][j][q] = 0.f;
-              }
-        } else {
-          slab_body<C, E, M>(st, oa, ob, fa0, fb0, fa1, fb1, acc, bmask);
-        }
-      };
-      auto kloop = [&](auto masked) {
-        load_slab<C>(srca, K, 0, stage0, wid);
-        load_slab<C>(srcb, K, 0, stage0 + C::OPB, wid);
-        wait_vm_all();
-        __syncthreads();
-        if (live) read_frags<C, E>(stage0, stage0 + C::OPB, oa[0], ob[0], fa0, fb0);
-        int kt = 0;
-        for (; kt + 2 <= nk; kt += 2) {
-          load_slab<C>(srca, K, kt + 1, stage1, wid);
-          load_slab<C>(srcb, K, kt + 1, stage1 + C::OPB, wid);
-          if (live) body(stage0, masked);
-          if (FUSE && live) fuse_input<C, E, false>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
-          wait_vm_all();
-          __syncthreads();
-          if (live) read_frags<C, E>(stage1, stage1 + C::OPB, oa[0], ob[0], fa0, fb0);
-          __builtin_amdgcn_sched_barrier(0);
-          if (kt + 2 < nk) {
-            load_slab<C>(srca, K, kt + 2, stage0, wid);
-            load_slab<C>(srcb, K, kt + 2, stage0 + C::OPB, wid);
-          }
-          if (live) body(stage1, masked);
-          if (FUSE && live) fuse_input<C, E, false>(stage1 + C::OPB, kt + 1, frow0, wn, lane, fcoef, acc);
-          wait_vm_all();
-          __syncthreads();
-          if (kt + 2 < nk && live) read_frags<C, E>(stage0, stage0 + C::OPB, oa[0], ob[0], fa0, fb0);
-          __builtin_amdgcn_sched_barrier(0);
-        }
-        if (kt < nk) {  // odd slab count: the last slab is in stage 0
-          if (live) body(stage0, masked);
-          if (FUSE && live) fuse_input<C, E, false>(stage0 + C::OPB, kt, frow0, wn, lane, fcoef, acc);
-          __syncthreads();
-        }
-      };
-      if (dtile)
-        kloop(BoolTag<true>{});
-      else
-        kloop(BoolTag<false>{});
+      kloop(TypeTag<C>{}, F{}, F{}, F{}, acc);
     }
   }
 
@@ -963,7 +1036,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
   // region (the stages are free after the K loop), so that every global
   // access is a full-line, 16-byte-per-lane row access.
   const float sc = args.first ? args.scale[d.slot] : 1.f;
-  const int64_t row0 = int64_t(ti) * TILE + wm * C::WTM;
+  const int64_t row0 = int64_t(ti) * TILE + wrow;
   const int64_t col0 = int64_t(tj) * TILE + wn * C::WTN;
   char* region = (wid < C::NW / 2 ? stage0 : stage1) + (wid % (C::NW / 2)) * C::WAVE_LDS;
   E* out_t = nullptr;        // transposed output (leading dimension mp)
@@ -987,7 +1060,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
       for (int j = 0; j < C::NBN; ++j)
 #pragma unroll
         for (int q = 0; q < 16; ++q) {
-          const int r = wm * C::WTM + 32 * i + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
+          const int r = wrow + 32 * i + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
           const int c = wn * C::WTN + 32 * j + (lane & 31);
           if (r == c && ti * TILE + r < d.m) acc[i][j][q] += args.diag;
         }
@@ -1004,19 +1077,23 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
   if (STAGE == ST_BX && args.last) {
     const PtrEntry pe = args.ptrs[d.index];
     const float lrs = update_lr(args.lr, d.rows, d.cols);
+    const uint32_t rows = masked ? arows : ~0u;
     if (d.param_dtype == MUON_BF16) {
       if (d.transposed)
-        apply_via_lds<C, true, __bf16>(acc, region, pe, d, lrs, args.decay, row0, col0, lane);
+        apply_via_lds<C, true, __bf16>(acc, region, pe, d, lrs, args.decay, row0, col0, lane, rows);
       else
-        apply_via_lds<C, false, __bf16>(acc, region, pe, d, lrs, args.decay, row0, col0, lane);
+        apply_via_lds<C, false, __bf16>(acc, region, pe, d, lrs, args.decay, row0, col0, lane, rows);
     } else {
       if (d.transposed)
-        apply_via_lds<C, true, float>(acc, region, pe, d, lrs, args.decay, row0, col0, lane);
+        apply_via_lds<C, true, float>(acc, region, pe, d, lrs, args.decay, row0, col0, lane, rows);
       else
-        apply_via_lds<C, false, float>(acc, region, pe, d, lrs, args.decay, row0, col0, lane);
+        apply_via_lds<C, false, float>(acc, region, pe, d, lrs, args.decay, row0, col0, lane, rows);
     }
-  } else if (dtile) {
-    if (dlive) {
+  } else if (masked) {
+    if (dlive && STAGE == ST_BX) {
+      if (!TRB) store_t_via_lds<C, E, true>(acc, region, out_t, mp, row0, col0, lane, bmask);
+      store_rows_via_lds<C, E, true>(acc, region, out_r, ld_r, row0, col0, lane, bmask);
+    } else if (dlive) {
       store_t_via_lds<C, E, true>(acc, region, out_t, mp, row0, col0, lane, bmask);
       if (rmask) store_rows_via_lds<C, E, true>(acc, region, out_r, ld_r, row0, col0, lane, rmask);
     }
@@ -1103,14 +1180,14 @@ int launch_ns_gemm(const Plan& p, const WaveHost& w, const ClassLaunch& cl, int3
   g.decay = sc.decay;
   hipStream_t st = hipStream_t(stream);
   const bool full = stage == ST_BX;
-  // the 256-tile part, then the edge strips of the same matrices on the
+  // the 256-tile part (the square outputs' row edge strips as half tiles
+  // among them), then for B*X the edge strips of the same matrices on the
   // strip class's 128 tiles (their outputs are disjoint)
   int e = launch_tiles(cl.kclass, cl.padded, stage, p.d_tiles + (full ? cl.full_off : cl.lower_off),
                        unsigned(full ? cl.n_full : cl.n_lower), gs.pair != 0, g, st);
-  if (e == 0 && cl.strip_kclass >= 0)
-    e = launch_tiles(cl.strip_kclass, false, stage,
-                     p.d_tiles + (full ? cl.strip_full_off : cl.strip_lower_off),
-                     unsigned(full ? cl.n_strip_full : cl.n_strip_lower), gs.pair != 0, g, st);
+  if (e == 0 && full && cl.strip_kclass >= 0)
+    e = launch_tiles(cl.strip_kclass, false, stage, p.d_tiles + cl.strip_full_off, unsigned(cl.n_strip_full),
+                     gs.pair != 0, g, st);
   return e;
 }
 

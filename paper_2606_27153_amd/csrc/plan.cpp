@@ -36,7 +36,8 @@ int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 // Extent of the 256-tile part of a padded extent: a 256-class matrix whose
 // extent ends 128 or fewer past a multiple of 256 (and holds at least one
 // whole 256 tile) is padded to 128 only, and its last 128 rows or columns
-// form an edge strip computed on 128 tiles.
+// form an edge strip: in the square outputs on half tiles of the 256 class
+// itself, in the B*X outputs on tiles of the 128 class.
 int64_t main_extent(int64_t v, int32_t tile, int32_t strip_class) {
   const int64_t p128 = round_up(v, 128);
   if (tile != 256 || strip_class < 0 || p128 == round_up(v, 256) || p128 < 384) return round_up(v, tile);
@@ -49,18 +50,19 @@ constexpr double kClassEfficiency[KC_COUNT] = {1.0, 0.8, 0.45, 1.0, 0.6, 1.0, 0.
 
 // Time-like cost of one Eq. 2 step as the kernels issue it: output tiles
 // cover the padded extent, the K loops stop at the last slab of bk elements
-// that holds real data (Gram: K = n; A*A and B*X: K = m), and the flops of
-// edge strips count at the strip class's efficiency.
+// that holds real data (Gram: K = n; A*A and B*X: K = m), the square outputs'
+// row strips (half tiles) run at the class's efficiency and the flops of the
+// B*X edge strips count at the strip class's efficiency.
 double padded_cost(int64_t m, int64_t n, int32_t kc, int64_t bk) {
   const ClassInfo& ci = kClasses[kc];
   const int64_t mm = main_extent(m, ci.tile, ci.strip), nm = main_extent(n, ci.tile, ci.strip);
   const double mp = double(mm < round_up(m, ci.tile) ? round_up(m, 128) : mm);
   const double np = double(nm < round_up(n, ci.tile) ? round_up(n, 128) : nm);
   const double km = double(round_up(m, bk)), kn = double(round_up(n, bk));
-  const double main = double(mm) * double(mm) * (kn + km) + 2.0 * double(mm) * double(nm) * km;
-  const double all = mp * mp * (kn + km) + 2.0 * mp * np * km;
+  const double square = mp * mp * (kn + km), bx_main = 2.0 * double(mm) * double(nm) * km;
+  const double bx_strips = 2.0 * mp * np * km - bx_main;
   const double strip_eff = ci.strip >= 0 ? kClassEfficiency[ci.strip] : kClassEfficiency[kc];
-  return main / kClassEfficiency[kc] + (all - main) / strip_eff;
+  return (square + bx_main) / kClassEfficiency[kc] + bx_strips / strip_eff;
 }
 
 // Kernel class of an m x n matrix: the operand type follows the precision
@@ -106,7 +108,7 @@ void full_units(std::vector<std::vector<TileEntry>>& units, int32_t mat, int64_t
           units.emplace_back();
           for (int64_t ti = r0; ti < std::min(tm, r0 + 4); ++ti)
             for (int64_t tj = u0; tj < std::min(tn, u0 + 8); ++tj)
-              units.back().push_back(TileEntry{mat, int32_t(ti), int32_t(tj)});
+              units.back().push_back(TileEntry{mat, int32_t(ti), int32_t(tj), 0});
         }
 }
 
@@ -123,11 +125,11 @@ void lower_units(std::vector<std::vector<TileEntry>>& units, int32_t mat, int64_
       for (int64_t h0 = r0; h0 < r1; h0 += 4) {
         units.emplace_back();
         for (int64_t ti = h0; ti < std::min(r1, h0 + 4); ++ti)
-          for (int64_t tj = c0; tj < c0 + 8; ++tj) units.back().push_back(TileEntry{mat, int32_t(ti), int32_t(tj)});
+          for (int64_t tj = c0; tj < c0 + 8; ++tj) units.back().push_back(TileEntry{mat, int32_t(ti), int32_t(tj), 0});
       }
     units.emplace_back();
     for (int64_t ti = r0; ti < r1; ++ti)
-      for (int64_t tj = r0; tj <= ti; ++tj) units.back().push_back(TileEntry{mat, int32_t(ti), int32_t(tj)});
+      for (int64_t tj = r0; tj <= ti; ++tj) units.back().push_back(TileEntry{mat, int32_t(ti), int32_t(tj), 0});
   }
 }
 
@@ -181,8 +183,8 @@ int64_t launches_per_step(const Plan& p, int32_t ns_steps) {
   for (const auto& w : p.waves) {
     n += k > 0 ? 2 : 3;  // momentum, finalize (and apply when no NS step runs)
     for (const auto& cl : w.launches) {
-      const int64_t lw = cl.n_strip_lower > 0 ? 2 : 1, bw = cl.n_strip_full > 0 ? 2 : 1;
-      n += cl.gram ? gram_lower * lw + gram_bx * bw : eq2_lower * lw + k * bw;
+      const int64_t bw = cl.n_strip_full > 0 ? 2 : 1;
+      n += cl.gram ? gram_lower + gram_bx * bw : eq2_lower + k * bw;
     }
   }
   return n;
@@ -402,8 +404,8 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
 
     for (int32_t kg = 0; kg < 2 * KC_COUNT; ++kg) {
       const int32_t kc = kg / 2, gram = kg % 2;
-      std::vector<TileEntry> lower, full, strip_lower, strip_full;
-      std::vector<std::vector<TileEntry>> units, funits, strip_lunits, strip_funits;
+      std::vector<TileEntry> lower, full, strip_full;
+      std::vector<std::vector<TileEntry>> units, funits, strip_funits;
       const int64_t tile = kClasses[kc].tile;
       double fg = 0, fp = 0, fb = 0;
       bool padded = false;
@@ -426,21 +428,26 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
         const int64_t tm = h.m_main / tile, tn = h.n_main / tile;
         lower_units(units, pos, tm);
         full_units(funits, pos, tm, tn);
-        // edge strips on 128 tiles: the last 128 rows (the lower row strip of
-        // the square outputs, the whole row strip of the m x n outputs) and
-        // the last 128 columns of the m x n outputs above it
+        // edge strips: the lower row strip of the square outputs on half
+        // tiles of this class, one unit per matrix (its last tile on the
+        // diagonal); the m x n outputs' last 128 rows and, above them, last 128
+        // columns on 128 tiles of the strip class (in B*X, half tiles ran
+        // slower than these whether launched with the main tiles or apart)
         const int32_t r = int32_t(h.m_main / 128), c = int32_t(h.n_main / 128);
         if (h.m_pad > h.m_main) {
-          for (int32_t tj = 0; tj <= r; ++tj) strip_unit(strip_lunits, TileEntry{pos, r, tj});
-          for (int32_t tj = 0; tj < int32_t(h.n_pad / 128); ++tj) strip_unit(strip_funits, TileEntry{pos, r, tj});
+          units.emplace_back();
+          for (int32_t tj = 0; tj <= int32_t(tm); ++tj)
+            units.back().push_back(TileEntry{pos, int32_t(tm), tj, kTileHalf});
+          for (int32_t tj = 0; tj < int32_t(h.n_pad / 128); ++tj) strip_unit(strip_funits, TileEntry{pos, r, tj, 0});
         }
         if (h.n_pad > h.n_main)
-          for (int32_t ti = 0; ti < r; ++ti) strip_unit(strip_funits, TileEntry{pos, ti, c});
+          for (int32_t ti = 0; ti < r; ++ti) strip_unit(strip_funits, TileEntry{pos, ti, c, 0});
         // the K loops stop at the last 128-byte slab holding real data
         const int64_t bk = kClasses[kc].fp32 ? 32 : 64;
         const double kn = double(round_up(h.n, bk)), km = double(round_up(h.m, bk));
         const double mp = double(h.m_pad), np = double(h.n_pad), mmain = double(tm * tile);
-        // lower tiles: the main triangle in tiles, the strip row in 128 tiles
+        // lower tiles: the main triangle in tiles, the strip row in half
+        // tiles (the diagonal one computes its lower 128 x 128 part)
         const double t2 = double(tile) * double(tile);
         const double sq = double(tm * (tm + 1) / 2) * t2 + (h.m_pad > h.m_main ? (mp - mmain) * mp : 0.0);
         p.padded_flops += sq * 2.0 * kn + sq * 2.0 * km + mp * np * 2.0 * km;
@@ -448,7 +455,6 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
       if (funits.empty() && strip_funits.empty()) continue;
       interleave_units(lower, units);
       interleave_units(full, funits);
-      interleave_units(strip_lower, strip_lunits);
       interleave_units(strip_full, strip_funits);
       ClassLaunch cl{};
       cl.kclass = kc;
@@ -464,9 +470,6 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
       cl.n_full = int32_t(full.size());
       p.h_tiles.insert(p.h_tiles.end(), full.begin(), full.end());
       cl.strip_kclass = kClasses[kc].strip;
-      cl.strip_lower_off = int64_t(p.h_tiles.size());
-      cl.n_strip_lower = int32_t(strip_lower.size());
-      p.h_tiles.insert(p.h_tiles.end(), strip_lower.begin(), strip_lower.end());
       cl.strip_full_off = int64_t(p.h_tiles.size());
       cl.n_strip_full = int32_t(strip_full.size());
       p.h_tiles.insert(p.h_tiles.end(), strip_full.begin(), strip_full.end());

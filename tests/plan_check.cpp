@@ -107,24 +107,30 @@ int main(int argc, char** argv) {
     for (const ClassLaunch& cl : w.launches) {
       const int tile = class_info(cl.kclass).tile;
       // every tile as a rectangle of 64 x 64 cells: (mat, cell row, cell col,
-      // cells per side)
-      struct Rect { int mat; long long r, c, k; };
+      // cell rows, cell columns); a half tile has half the rows
+      struct Rect { int mat; long long r, c, kr, kc; };
       std::vector<Rect> lower, full;
+      bool bad_flags = false;
       auto add = [&](std::vector<Rect>& v, int64_t off, int32_t cnt, int t) {
         for (int32_t i = 0; i < cnt; ++i) {
           const TileEntry& e = p.h_tiles[size_t(off + i)];
-          v.push_back(Rect{e.mat, (long long)e.ti * (t / 64), (long long)e.tj * (t / 64), t / 64});
+          if (e.flags & ~kTileHalf || ((e.flags & kTileHalf) && t != 256)) bad_flags = true;
+          const long long k = t / 64;
+          v.push_back(Rect{e.mat, (long long)e.ti * k, (long long)e.tj * k, (e.flags & kTileHalf) ? k / 2 : k, k});
         }
       };
       add(lower, cl.lower_off, cl.n_lower, tile);
       add(full, cl.full_off, cl.n_full, tile);
-      if (cl.n_strip_lower || cl.n_strip_full) {
+      if (cl.n_strip_full) {
         if (cl.strip_kclass < 0 || class_info(cl.strip_kclass).tile != 128 || tile != 256 ||
             class_info(cl.strip_kclass).f16 != class_info(cl.kclass).f16 || class_info(cl.strip_kclass).fp32)
           return fail("strip class");
-        add(lower, cl.strip_lower_off, cl.n_strip_lower, 128);
         add(full, cl.strip_full_off, cl.n_strip_full, 128);
       }
+      if (bad_flags) return fail("tile flags");
+      // half tiles exist only in the square outputs' lists
+      for (int32_t i = 0; i < cl.n_full; ++i)
+        if (p.h_tiles[size_t(cl.full_off + i)].flags & kTileHalf) return fail("half tile in a B*X list");
       std::map<int, std::vector<int>> lcells, fcells;
       for (int s = 0; s < w.count; ++s) {
         const int pos = w.first + s;
@@ -153,9 +159,11 @@ int main(int argc, char** argv) {
         if (it == fcells.end()) return fail("tile of another class or form");
         const MatHost& h = p.mats[size_t(p.order[size_t(t.mat)])];
         const long long cm = h.m_pad / 64, cn = h.n_pad / 64;
-        if (t.r + t.k > cm || t.c + t.k > cn) return fail("full tile out of range");
-        for (long long i = t.r; i < t.r + t.k; ++i)
-          for (long long j = t.c; j < t.c + t.k; ++j)
+        if (t.r + t.kr > cm || t.c + t.kc > cn) return fail("full tile out of range");
+        // a half tile's operand panel is the padded extent's last 128 rows
+        if (t.kr != t.kc && t.r + t.kr != cm) return fail("half tile not on the last 128 rows");
+        for (long long i = t.r; i < t.r + t.kr; ++i)
+          for (long long j = t.c; j < t.c + t.kc; ++j)
             if (++it->second[size_t(i * cn + j)] != 1) return fail("duplicate full tile");
       }
       // symmetric outputs: each tile is a diagonal block or lies strictly
@@ -166,11 +174,14 @@ int main(int argc, char** argv) {
         if (it == lcells.end()) return fail("tile of another class or form");
         const MatHost& h = p.mats[size_t(p.order[size_t(t.mat)])];
         const long long cm = h.m_pad / 64;
-        if (t.r + t.k > cm || t.c + t.k > cm) return fail("lower tile out of range");
         const bool diag = t.r == t.c;
-        if (!diag && t.r < t.c + t.k) return fail("lower tile not below the diagonal");
-        for (long long i = t.r; i < t.r + t.k; ++i)
-          for (long long j = t.c; j < t.c + t.k; ++j) {
+        // a diagonal half tile reaches past the padded extent by 128
+        // columns, which it does not compute
+        if (t.r + t.kr > cm || (!diag && t.c + t.kc > cm)) return fail("lower tile out of range");
+        if (t.kr != t.kc && t.r + t.kr != cm) return fail("half tile not on the last 128 rows");
+        if (!diag && t.r < t.c + t.kc) return fail("lower tile not below the diagonal");
+        for (long long i = t.r; i < t.r + t.kr; ++i)
+          for (long long j = t.c; j < t.c + t.kc; ++j) {
             if (diag && j > i) continue;   // counted through its mirror cell
             if (++it->second[size_t(i * cm + j)] != 1) return fail("duplicate lower tile");
           }
@@ -201,11 +212,10 @@ int main(int argc, char** argv) {
     launches += 2;
     // k = 5: Eq. 2 runs 2 lower-tile launches and one B*X per step; the
     // Gram-space form, in segments of 2, 2 and 1 steps, 6 + 6 + 2 lower-tile
-    // launches and 3 B*X; a group with edge strips doubles the launches of
-    // the kind its strips have
+    // launches and 3 B*X; edge strips add a launch to every B*X
     for (const ClassLaunch& cl : w.launches) {
-      const long long lw = cl.n_strip_lower ? 2 : 1, bw = cl.n_strip_full ? 2 : 1;
-      launches += cl.gram ? 14 * lw + 3 * bw : 10 * lw + 5 * bw;
+      const long long bw = cl.n_strip_full ? 2 : 1;
+      launches += cl.gram ? 14 + 3 * bw : 10 + 5 * bw;
     }
     if (groups.size() != w.launches.size()) return fail("one launch group per (class, form)");
   }
