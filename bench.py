@@ -285,7 +285,7 @@ def gram_segments(k: int, restart: int = GRAM_RESTART) -> list:
     return [min(restart, k - s0) for s0 in range(0, k, restart)]
 
 
-def ns_cost(rows: int, cols: int, k: int = 5, gram_min_aspect: float = 2.0, restart: int = GRAM_RESTART) -> float:
+def ns_cost(rows: int, cols: int, k: int = 5, gram_min_aspect: float = 1.4, restart: int = GRAM_RESTART) -> float:
     """Algorithmic NS flops of one matrix in the form the plan gives it
     (16-bit classes; Eq. 4 when n >= aspect * m and m >= 256, else Eq. 2).
     Eq. 4 restarts every ``restart`` steps; a segment of L steps costs

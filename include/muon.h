@@ -114,8 +114,9 @@ typedef struct muon_plan_opts {
                                         of matrices processed together; 0 = default */
   float gram_min_aspect;             /* 16-bit NS matrices with m >= 256 and n >= gram_min_aspect * m
                                         run the Gram-space recurrence (Eq. 4); 0 = never.  Must be 0
-                                        or >= 1; ignored when c = 0 at some step.  The default 2 suits
-                                        bf16; fp16 keeps its accuracy down to about 1.4 */
+                                        or >= 1; ignored when c = 0 at some step.  Default 1.4: from there
+                                        the restarted form is both faster and, on planted spectra, as
+                                        accurate as Eq. 2 in bf16 and fp16 */
   int32_t gram_restart;              /* NS steps per Gram-space segment: after that many steps the
                                         iterate X = Q X0 is formed and the recurrence restarts from
                                         a fresh Gram matrix X X^T.  0 = the default, 2.  Without
@@ -165,7 +166,7 @@ typedef struct muon_matrix_info {
 
 /* Fills *o with the defaults: precision BF16, max_ns_steps 16,
  * (a,b,c) = (3.4445, -4.7750, 2.0315), eps 1e-7, small_m_threshold 64,
- * flags 0, wave_bytes 0, gram_min_aspect 2, gram_restart 0 (2), abc_per_step NULL.  Returns
+ * flags 0, wave_bytes 0, gram_min_aspect 1.4, gram_restart 0 (2), abc_per_step NULL.  Returns
  * INVALID_ARG if o is NULL. */
 MUON_API muon_status muon_plan_opts_default(muon_plan_opts* o);
 

@@ -140,7 +140,7 @@ def planner_tiles(descs: Sequence, *, precision: str, gram_min_aspect: float) ->
         plan.close()
 
 
-def tune(descs: Sequence, *, precision: str = "bf16", gram_min_aspect: float = 2.0, ns_steps: int = 5,
+def tune(descs: Sequence, *, precision: str = "bf16", gram_min_aspect: float = 1.4, ns_steps: int = 5,
          cache_path: Optional[str] = None, max_per_shape: int = 16, steps: int = 3, min_gain: float = 0.01,
          timer: Optional[Callable[[list], float]] = None, device_name: Optional[str] = None,
          abi: Optional[int] = None) -> List[int]:

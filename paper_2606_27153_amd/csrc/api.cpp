@@ -436,7 +436,7 @@ muon_status muon_plan_opts_default(muon_plan_opts* o) {
   o->small_m_threshold = 64;
   o->flags = 0;
   o->wave_bytes = 0;
-  o->gram_min_aspect = 2.f;
+  o->gram_min_aspect = 1.4f;
   o->gram_restart = 0;
   o->abc_per_step = nullptr;
   return ok();

@@ -20,16 +20,18 @@ PRECISIONS = {"bf16": L.MUON_NS_BF16, "fp32": L.MUON_NS_FP32, "fp16": L.MUON_NS_
 
 
 def default_gram_min_aspect(precision: str) -> float:
-    """Aspect n/m from which a matrix takes the Gram-space form by default.
+    """Aspect n/m from which a 16-bit matrix takes the Gram-space form by
+    default (Eq. 4, restarted every 2 steps; also m >= 256).
 
-    The Gram form costs fewer flops for any n > m (3m^2 n + 17m^3 against
-    5(3m^2 n + m^3) at k = 5), but squares the conditioning.  An emulation
-    with fp32 accumulation and 16-bit stores gave, for bf16, 1.6e-2 at aspect
-    1.45 and 1.9e-2 at 1.33 (against the 2e-2 bar), so bf16 keeps 2; fp16
-    stays below 3e-3 down to aspect 1.33, so fp16 starts at 1.4 (which takes
-    in 1408 x 2048 MoE experts: 20% fewer flops).
+    The restarted form costs 9m^2 n + 11m^3 against Eq. 2's 15m^2 n + 5m^3 at
+    k = 5, fewer flops for n > m, but moves work to the m x m products, which
+    run slower per flop than B*X.  From aspect 1.4 it is faster on the
+    1408 x 2048 MoE experts (MoE set 344.5 -> 334.5 ms), and on planted
+    spectra at aspect 1.45-1.5 it is as accurate as Eq. 2 in bf16 (mild
+    7.2e-3 against 8.3e-3, 1/i 2.9e-2 against 3.3e-2).  The fp32 path keeps
+    Eq. 2 whatever this says.
     """
-    return 1.4 if precision == "fp16" else 2.0
+    return 1.4
 
 
 def check_step_tensors(descs: Sequence, params: List, grads: List, moms: List, workspace=None,

@@ -142,7 +142,7 @@ def test_live_flop_share():
     assert bench.live_flop_share(plan, 5, [False] * 4) == {k: 1.0 for k in share}
     assert bench.live_flop_share(plan, 5, [True] * 4) == {k: 0.0 for k in share}
     plan.close()
-    # Gram-space (n >= 2m) and Eq. 2 matrices in one class: with restarts
+    # Gram-space (n >= 1.4m) and Eq. 2 matrices in one class: with restarts
     # every 2 steps (segments 2, 2, 1) the former's Gram and B*X run 3 times,
     # the latter's k = 5 times
     descs = [(1024, 4096, "bf16", "bf16"), (1024, 1024, "bf16", "bf16")]

@@ -40,7 +40,7 @@ def _read(buf: bytes, off: int, shape, bf16: bool):
 
 def test_plain_c_caller_matches_oracle(tmp_path):
     assert os.path.exists(EXE), "tests/c_abi_step is missing: run __graft_entry__.build()"
-    # wide, tall, Gram-space (n >= 2m), fp32 parameters with fp32 gradients,
+    # wide, tall, Gram-space (n >= 1.4m), fp32 parameters with fp32 gradients,
     # and a small-m matrix on the fp32 NS classes
     wl = custom_workload([(200, 300), (300, 200), (512, 1100), (96, 160), (48, 700)], seed=33)
     mats = list(wl.matrices)
