@@ -527,12 +527,10 @@ struct ApplyLay {
   }
 };
 
-// rows: bit i set when MFMA block row i of the wave tile is the wave's to
-// apply (a half tile's waves each own half of theirs).
 template <class C, bool TRANS, typename P>
 __device__ __forceinline__ void apply_via_lds(const f32x16 (&acc)[C::NBM][C::NBN], char* region,
                                               const PtrEntry& pe, const MatDev& d, float lrs, float decay,
-                                              int64_t row0, int64_t col0, int lane, uint32_t rows = ~0u) {
+                                              int64_t row0, int64_t col0, int lane) {
   using A = ApplyLay<C, TRANS>;
   const int64_t srow_end = TRANS ? col0 + C::WTN : row0 + C::WTM;
   const int64_t scol_end = TRANS ? row0 + C::WTM : col0 + C::WTN;
@@ -545,7 +543,6 @@ __device__ __forceinline__ void apply_via_lds(const f32x16 (&acc)[C::NBM][C::NBN
     for (int pass = 0; pass < A::NPASS; ++pass)
 #pragma unroll
       for (int it = 0; it < A::NP; ++it) {
-        if (!((rows >> (pass >> 1)) & 1u)) continue;
         int off;
         int64_t row, col;
         A::at(pass, lane + 64 * it, row0, col0, off, row, col);
@@ -553,7 +550,6 @@ __device__ __forceinline__ void apply_via_lds(const f32x16 (&acc)[C::NBM][C::NBN
       }
 #pragma unroll
     for (int pass = 0; pass < A::NPASS; ++pass) {
-      if (!((rows >> (pass >> 1)) & 1u)) continue;
       A::stage(acc, region, pass >> 1, pass & 1, lane);
       __builtin_amdgcn_s_waitcnt(0xc07f);
 #pragma unroll
@@ -574,7 +570,6 @@ __device__ __forceinline__ void apply_via_lds(const f32x16 (&acc)[C::NBM][C::NBN
   }
 #pragma unroll
   for (int pass = 0; pass < A::NPASS; ++pass) {
-    if (!((rows >> (pass >> 1)) & 1u)) continue;
     A::stage(acc, region, pass >> 1, pass & 1, lane);
     apply_pass<P, A::NP>(region, pe, d, lrs, decay, lane, [&](int piece, int& off, int64_t& row, int64_t& col) {
       A::at(pass, piece, row0, col0, off, row, col);
@@ -852,11 +847,6 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
   }
   // the epilogue's masked stores serve diagonal and half tiles
   const bool masked = htile || dtile;
-  // MFMA block rows that hold the wave's results (the apply's pass mask)
-  uint32_t arows = 0;
-#pragma unroll
-  for (int i = 0; i < C::NBM; ++i)
-    if ((bmask >> (i * C::NBN)) & ((1u << C::NBN) - 1u)) arows |= 1u << i;
   const int64_t mp = d.m_pad, np = d.n_pad;
 
   const E* opa;
@@ -1077,23 +1067,19 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
   if (STAGE == ST_BX && args.last) {
     const PtrEntry pe = args.ptrs[d.index];
     const float lrs = update_lr(args.lr, d.rows, d.cols);
-    const uint32_t rows = masked ? arows : ~0u;
     if (d.param_dtype == MUON_BF16) {
       if (d.transposed)
-        apply_via_lds<C, true, __bf16>(acc, region, pe, d, lrs, args.decay, row0, col0, lane, rows);
+        apply_via_lds<C, true, __bf16>(acc, region, pe, d, lrs, args.decay, row0, col0, lane);
       else
-        apply_via_lds<C, false, __bf16>(acc, region, pe, d, lrs, args.decay, row0, col0, lane, rows);
+        apply_via_lds<C, false, __bf16>(acc, region, pe, d, lrs, args.decay, row0, col0, lane);
     } else {
       if (d.transposed)
-        apply_via_lds<C, true, float>(acc, region, pe, d, lrs, args.decay, row0, col0, lane, rows);
+        apply_via_lds<C, true, float>(acc, region, pe, d, lrs, args.decay, row0, col0, lane);
       else
-        apply_via_lds<C, false, float>(acc, region, pe, d, lrs, args.decay, row0, col0, lane, rows);
+        apply_via_lds<C, false, float>(acc, region, pe, d, lrs, args.decay, row0, col0, lane);
     }
-  } else if (masked) {
-    if (dlive && STAGE == ST_BX) {
-      if (!TRB) store_t_via_lds<C, E, true>(acc, region, out_t, mp, row0, col0, lane, bmask);
-      store_rows_via_lds<C, E, true>(acc, region, out_r, ld_r, row0, col0, lane, bmask);
-    } else if (dlive) {
+  } else if (masked) {  // square outputs only
+    if (dlive) {
       store_t_via_lds<C, E, true>(acc, region, out_t, mp, row0, col0, lane, bmask);
       if (rmask) store_rows_via_lds<C, E, true>(acc, region, out_r, ld_r, row0, col0, lane, rmask);
     }
