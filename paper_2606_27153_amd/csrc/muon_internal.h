@@ -44,7 +44,8 @@ constexpr int32_t EW_TILE = 64;
 
 // The m_pad x m_pad buffers of a matrix.  Eq. 2 uses A (Gram) and B
 // (polynomial); the Gram-space recurrence of Eq. 4 uses G in A, P_i in B,
-// the running product Q in a ping-pong pair and R = G P.
+// the running product Q in a ping-pong pair and R = G P (with segments of
+// at most two steps R is B's memory and Q1 is A's).
 enum SqBuf : int32_t { SQ_A = 0, SQ_B = 1, SQ_Q0 = 2, SQ_Q1 = 3, SQ_R = 4, SQ_COUNT = 5 };
 
 // Device descriptor of one matrix inside a wave.  All *_off fields are byte
@@ -209,6 +210,11 @@ double plan_ns_flops(const Plan& p, int32_t ns_steps);
 // fresh Gram product, the segment's polynomials and products, and X = Q X
 // (the update itself after the last segment).
 constexpr int32_t kGramMinM = 256;   // smaller m stays on Eq. 2
+// Segments of at most two steps let R share B and Q1 share A (the
+// Gram-space recurrence then keeps three square buffers, not five).
+inline bool gram_shares_buffers(const Plan& p, int32_t max_ns_steps) {
+  return (p.gram_restart < max_ns_steps ? p.gram_restart : max_ns_steps) <= 2;
+}
 
 // Per-launch arguments shared by the kernel launchers.
 struct StepScalars {

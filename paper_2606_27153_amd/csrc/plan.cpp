@@ -267,13 +267,22 @@ muon_status build_plan(const muon_matrix_desc* descs, int32_t n, const muon_plan
     // X in both layouts for the fp32 classes; the bf16 classes read X^T
     // straight from X with LDS transposing reads and keep X only.  The
     // Gram-space form needs the ping-pong pair only when it restarts, and
-    // keeps five square buffers instead of two.
+    // up to five square buffers instead of two.
     for (int pp = 0; pp < 2; ++pp) {
       const bool need = pp == 0 || !h.gram || p.gram_restart < o.max_ns_steps;
       h.x_off[pp] = need ? take(h.m_pad * h.n_pad * esz) : -1;
       h.xt_off[pp] = need && ci.fp32 ? take(h.m_pad * h.n_pad * esz) : -1;
     }
-    for (int q = 0; q < SQ_COUNT; ++q) h.sq_off[q] = q < 2 || h.gram ? take(h.m_pad * h.m_pad * esz) : -1;
+    for (int q = 0; q < SQ_COUNT; ++q) h.sq_off[q] = q < 2 || (h.gram && q < 3) ? take(h.m_pad * h.m_pad * esz) : -1;
+    if (h.gram) {
+      // A segment of one or two steps never holds all five at once: R = G P_0
+      // is dead once G <- P_0 R is formed, before P_1 is written to B, and
+      // the last step's Q_{i+1} = P_i Q_i overwrites G, which is dead once
+      // P_i is formed.  Longer segments keep R and Q1 apart.
+      const bool share = gram_shares_buffers(p, o.max_ns_steps);
+      h.sq_off[SQ_R] = share ? h.sq_off[SQ_B] : take(h.m_pad * h.m_pad * esz);
+      h.sq_off[SQ_Q1] = share ? h.sq_off[SQ_A] : take(h.m_pad * h.m_pad * esz);
+    }
     h.partial_off = take(h.ew_tiles * 4);
     h.ws_bytes = off;  // relative offsets for now, rebased per wave below
 

@@ -33,6 +33,7 @@ int main(int argc, char** argv) {
   const int precision = argc > 1 ? std::atoi(argv[1]) : 0;
   const long long wave_bytes = argc > 2 ? std::atoll(argv[2]) : 0;
   const float aspect = argc > 3 ? float(std::atof(argv[3])) : 2.f;
+  const int restart = argc > 4 ? std::atoi(argv[4]) : 0;
   std::vector<muon_matrix_desc> descs;
   long long r, c;
   while (std::scanf("%lld %lld", &r, &c) == 2) descs.push_back(muon_matrix_desc{r, c, MUON_BF16, MUON_BF16, MUON_F32, 0});
@@ -46,6 +47,7 @@ int main(int argc, char** argv) {
   o.small_m_threshold = 64;
   o.wave_bytes = wave_bytes;
   o.gram_min_aspect = aspect;
+  o.gram_restart = restart;
   Plan p;
   std::string err;
   if (build_plan(descs.data(), int32_t(descs.size()), o, p, err) != MUON_OK) return fail("build_plan: " + err);
@@ -66,9 +68,16 @@ int main(int argc, char** argv) {
       const long long esz = h.fp32_ns ? 4 : 2;
       const long long xb = h.m_pad * h.n_pad * esz;
       const long long ab = h.m_pad * h.m_pad * esz;
+      // with segments of at most two steps the Gram-space form keeps R in
+      // B's memory and Q1 in A's (each shared region is listed once)
+      const bool share = h.gram && std::min(p.gram_restart, p.opts.max_ns_steps) <= 2;
+      if (h.gram && share != gram_shares_buffers(p, p.opts.max_ns_steps)) return fail("square-buffer sharing rule");
+      if (share && (h.sq_off[SQ_R] != h.sq_off[SQ_B] || h.sq_off[SQ_Q1] != h.sq_off[SQ_A]))
+        return fail("Gram-space square buffers not shared");
       const std::pair<long long, long long> rs[] = {
           {h.x_off[0], xb}, {h.x_off[1], xb}, {h.xt_off[0], xb}, {h.xt_off[1], xb},
-          {h.sq_off[0], ab},  {h.sq_off[1], ab},  {h.sq_off[2], ab}, {h.sq_off[3], ab}, {h.sq_off[4], ab},
+          {h.sq_off[SQ_A], ab}, {h.sq_off[SQ_B], ab}, {h.sq_off[SQ_Q0], ab},
+          {share ? -1 : h.sq_off[SQ_Q1], ab}, {share ? -1 : h.sq_off[SQ_R], ab},
           {h.partial_off, h.ew_tiles * 4}};
       // operand type: fp32 for the fp32 mode and for small m under bf16,
       // fp16 for every matrix under fp16, bf16 otherwise
@@ -199,9 +208,17 @@ int main(int argc, char** argv) {
   }
   for (size_t i = 0; i < seen.size(); ++i)
     if (seen[i] != 1) return fail("matrix not in exactly one wave");
-  // launch count at k = 5: per wave 2 elementwise launches, per (class, form)
-  // group 15 (Eq. 2) or 1 Gram + 5 P_i + (G P | P Q) 4 + P Q 1 + P (G P) 4
-  // + 1 B*X = 16 (Gram space)
+  // launch count at k = 5: per wave 2 elementwise launches; per (class,
+  // form) group 10 lower-tile launches and 5 B*X (Eq. 2) or, per Gram-space
+  // segment, the Gram product, then per step P_i, one launch for P Q and/or
+  // G P when either is due and P (G P) when G P is, and one B*X
+  long long gram_lower = 0, gram_bx = 0;
+  for (int s0 = 0; s0 < 5; s0 += p.gram_restart) {
+    const int len = std::min(p.gram_restart, 5 - s0);
+    gram_lower += 1;
+    for (int j = 0; j < len; ++j) gram_lower += 1 + (j > 0 || j + 1 < len) + (j + 1 < len);
+    gram_bx += 1;
+  }
   long long launches = 0;
   for (const WaveHost& w : p.waves) {
     std::set<std::pair<int, int>> groups;
@@ -210,12 +227,11 @@ int main(int argc, char** argv) {
       groups.insert({h.kclass, h.gram});
     }
     launches += 2;
-    // k = 5: Eq. 2 runs 2 lower-tile launches and one B*X per step; the
-    // Gram-space form, in segments of 2, 2 and 1 steps, 6 + 6 + 2 lower-tile
-    // launches and 3 B*X; edge strips add a launch to every B*X
+    // edge strips add a launch to every B*X (with the default restart of 2
+    // the Gram-space form runs 6 + 6 + 2 lower-tile launches and 3 B*X)
     for (const ClassLaunch& cl : w.launches) {
       const long long bw = cl.n_strip_full ? 2 : 1;
-      launches += cl.gram ? 14 + 3 * bw : 10 + 5 * bw;
+      launches += cl.gram ? gram_lower + gram_bx * bw : 10 + 5 * bw;
     }
     if (groups.size() != w.launches.size()) return fail("one launch group per (class, form)");
   }

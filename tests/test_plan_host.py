@@ -25,10 +25,10 @@ def plan_check(tmp_path_factory):
     return str(exe)
 
 
-def _run(exe, shapes, precision=0, wave_bytes=0, aspect=2.0):
+def _run(exe, shapes, precision=0, wave_bytes=0, aspect=2.0, restart=0):
     inp = "\n".join(f"{r} {c}" for r, c in shapes)
-    out = subprocess.run([exe, str(precision), str(wave_bytes), str(aspect)], input=inp, capture_output=True,
-                         text=True)
+    out = subprocess.run([exe, str(precision), str(wave_bytes), str(aspect), str(restart)], input=inp,
+                         capture_output=True, text=True)
     assert out.returncode == 0 and out.stdout.startswith("OK"), out.stdout + out.stderr
 
 
@@ -50,6 +50,9 @@ def test_ragged_and_random_plans(plan_check):
     _run(plan_check, ragged, precision=2)
     _run(plan_check, ragged, aspect=1.0)
     _run(plan_check, ragged, aspect=0.0)
+    # segments of one, two (shared square buffers), three and all steps
+    for restart in (1, 2, 3, 16):
+        _run(plan_check, ragged, aspect=1.0, restart=restart)
     # more than 65535 tiles along one dimension
     _run(plan_check, [(1, 1 << 22), ((1 << 22) + 5, 3), (70, 1 << 18)])
     for trial in range(5):
