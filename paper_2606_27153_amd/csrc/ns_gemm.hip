@@ -57,6 +57,7 @@ struct GemmArgs {
   char* ws;
   const float* scale;
   const int32_t* flag;
+  int32_t mat_base;  // plan index of the wave's first matrix: tile.mat - mat_base indexes scale and flag
   float fcoef;     // coefficient of the term folded in from the resident slab
   float diag;      // ST_POLY: added on the diagonal
   float oscale;    // output factor (times s^2 / s for ST_GRAM / ST_BX in the first step)
@@ -765,8 +766,10 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
   const MatDev& d = args.mats[te.mat];
   // An all-zero NS input has O = 0: its products are skipped, and the last
   // B*X only applies the weight decay.  A matrix without a gradient this
-  // step is not touched at all.
-  const int32_t mflag = args.flag[d.slot];
+  // step is not touched at all.  The flag is indexed from the tile entry, so
+  // its load does not wait for the descriptor's.
+  const int32_t slot = te.mat - args.mat_base;
+  const int32_t mflag = args.flag[slot];
   const bool zero = mflag != FLAG_LIVE;
   if (mflag == FLAG_SKIP || (zero && !(STAGE == ST_BX && args.last))) return;
 
@@ -1025,7 +1028,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void ns_gemm_kernel(GemmArgs args) 
   // rows of one column.  The outputs pass through the wave's private LDS
   // region (the stages are free after the K loop), so that every global
   // access is a full-line, 16-byte-per-lane row access.
-  const float sc = args.first ? args.scale[d.slot] : 1.f;
+  const float sc = args.first ? args.scale[slot] : 1.f;
   const int64_t row0 = int64_t(ti) * TILE + wrow;
   const int64_t col0 = int64_t(tj) * TILE + wn * C::WTN;
   char* region = (wid < C::NW / 2 ? stage0 : stage1) + (wid % (C::NW / 2)) * C::WAVE_LDS;
@@ -1149,6 +1152,7 @@ int launch_ns_gemm(const Plan& p, const WaveHost& w, const ClassLaunch& cl, int3
   g.ws = ws;
   g.scale = reinterpret_cast<const float*>(ws + w.scale_off);
   g.flag = reinterpret_cast<const int32_t*>(ws + w.flag_off);
+  g.mat_base = w.first;
   g.fcoef = gs.fcoef;
   g.diag = gs.diag;
   g.oscale = gs.oscale;

@@ -119,11 +119,13 @@ int main(int argc, char** argv) {
       // cell rows, cell columns); a half tile has half the rows
       struct Rect { int mat; long long r, c, kr, kc; };
       std::vector<Rect> lower, full;
-      bool bad_flags = false;
+      bool bad_flags = false, bad_mat = false;
       auto add = [&](std::vector<Rect>& v, int64_t off, int32_t cnt, int t) {
         for (int32_t i = 0; i < cnt; ++i) {
           const TileEntry& e = p.h_tiles[size_t(off + i)];
           if (e.flags & ~kTileHalf || ((e.flags & kTileHalf) && t != 256)) bad_flags = true;
+          // the kernels index the wave's flags and scales by mat - first
+          if (e.mat < w.first || e.mat >= w.first + w.count) bad_mat = true;
           const long long k = t / 64;
           v.push_back(Rect{e.mat, (long long)e.ti * k, (long long)e.tj * k, (e.flags & kTileHalf) ? k / 2 : k, k});
         }
@@ -137,6 +139,7 @@ int main(int argc, char** argv) {
         add(full, cl.strip_full_off, cl.n_strip_full, 128);
       }
       if (bad_flags) return fail("tile flags");
+      if (bad_mat) return fail("tile of a matrix outside its wave");
       // half tiles exist only in the square outputs' lists
       for (int32_t i = 0; i < cl.n_full; ++i)
         if (p.h_tiles[size_t(cl.full_off + i)].flags & kTileHalf) return fail("half tile in a B*X list");
