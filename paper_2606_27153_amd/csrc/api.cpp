@@ -352,7 +352,9 @@ muon_status step_impl(muon_plan plan, void* const* params, const void* const* gr
     // (the segment's first P is written straight into Q0); R = G P_i and
     // G <- P_i R except after the segment's last step; then X <- Q X, which
     // after the last segment is O and goes into the update.  P Q and G P
-    // only need P_i, so they share one launch.
+    // only need P_i, so they share one launch.  In segments of at most two
+    // steps R lives in B's memory and the second Q in A's (gram_shares_buffers):
+    // this order writes each only after the last read of what it replaces.
     for (const ClassLaunch& cl : w.launches) {
       if (!cl.gram) continue;
       int32_t pin = 0;

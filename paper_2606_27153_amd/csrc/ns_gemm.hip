@@ -21,9 +21,10 @@
 //                                 or, on the last step, O in fp32 in the
 //                                 matrix's own (un-oriented) layout
 //
-// Eq. 2 runs GRAM, POLY, BX per NS step; the Gram-space recurrence runs GRAM
-// once, then POLY (P_i = a I + b G + c G^2) and SYM (P Q, G P, P (G P)) per
-// step, and BX (O = s Q X0) once.  s = 1/(||u||_F + eps) is applied where X0
+// Eq. 2 runs GRAM, POLY, BX per NS step; the Gram-space recurrence runs, per
+// segment of at most gram_restart steps, GRAM once, then POLY (P_i = a I +
+// b G + c G^2) and SYM (P Q, G P, P (G P)) per step, and BX (X <- Q X; O
+// after the last segment) once.  s = 1/(||u||_F + eps) is applied where X0
 // = s*u would first enter (X0 is never materialised).  Buffers are padded to
 // the tile with zeros, and the zeros stay zero through all products, so the
 // kernels need no bounds checks.
@@ -535,9 +536,9 @@ __device__ __forceinline__ void apply_via_lds(const f32x16 (&acc)[C::NBM][C::NBN
   using A = ApplyLay<C, TRANS>;
   const int64_t srow_end = TRANS ? col0 + C::WTN : row0 + C::WTM;
   const int64_t scol_end = TRANS ? row0 + C::WTM : col0 + C::WTN;
-  if (sizeof(P) == 2 && (d.cols & 3) == 0 && srow_end <= d.rows && scol_end <= d.cols) {
-    // whole wave tile inside W: every parameter load of the tile goes out
-    // before the first update, so their latencies overlap
+  if (__is_same(P, __bf16) && (d.cols & 3) == 0 && srow_end <= d.rows && scol_end <= d.cols) {
+    // bf16 W, whole wave tile inside W: every parameter load of the tile goes
+    // out before the first update, so their latencies overlap
     typename Vec4<__bf16>::T w[A::NPASS][A::NP];
     __bf16* wb = reinterpret_cast<__bf16*>(pe.param);
 #pragma unroll
