@@ -371,6 +371,39 @@ def test_null_grads_skip_their_matrices():
     sub.close()
 
 
+def test_non_finite_gradients_poison_only_their_matrix():
+    # NaN or Inf in a gradient is not sanitised: the matrix's momentum holds
+    # it at that element, the norm of its NS input is not finite, and its
+    # whole update -- hence every element of W -- turns NaN.  Every other
+    # matrix is bitwise as in a clean step (Gram-space, Eq. 2 and the small
+    # fp32 class each take one bad value).
+    shapes = [(256, 768), (768, 256), (300, 300), (64, 200), (512, 2048), (1024, 1024)]
+    wl = custom_workload(shapes, seed=28)
+    dev = "cuda:0"
+    kw = dict(lr=0.02, momentum=0.95, weight_decay=0.01, ns_steps=5)
+    plan = MuonPlan([(m.rows, m.cols, m.param, m.grad) for m in wl.matrices])
+    pa, ma = make_state(torch, wl, dev)
+    pb, mb = make_state(torch, wl, dev)
+    g = make_grads(torch, wl, 0, dev)
+    gb = [x.clone() for x in g]
+    bad = {1: float("nan"), 2: float("inf"), 3: float("-inf"), 4: float("nan")}
+    for i, v in bad.items():
+        gb[i][5, 7] = v
+    plan.step(pa, g, ma, **kw)
+    plan.step(pb, gb, mb, **kw)
+    torch.cuda.synchronize()
+    for i in range(wl.n):
+        if i not in bad:
+            assert torch.equal(pa[i], pb[i]) and torch.equal(ma[i], mb[i]), i
+            continue
+        assert torch.isnan(pb[i].float()).all(), i
+        assert not torch.isfinite(mb[i][5, 7]), i
+        same = torch.eq(ma[i], mb[i])
+        same[5, 7] = True
+        assert same.all(), i
+    plan.close()
+
+
 def test_optimizer_reuses_one_plan_while_experts_come_and_go():
     # MoE-like: each step a different subset of parameters has no gradient.
     # One plan per group, built once; GPU memory stays flat; every step is
