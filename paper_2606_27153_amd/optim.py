@@ -99,7 +99,7 @@ class MuonPlan:
     dtypes are 'f32' or 'bf16'; momentum is always fp32.  16-bit-path
     matrices with max(rows, cols) >= gram_min_aspect * min(rows, cols) run the
     Gram-space recurrence (Eq. 4); 0 keeps every matrix on Eq. 2; None takes
-    ``default_gram_min_aspect(precision)`` (2 for bf16, 1.4 for fp16).  ``abc`` is
+    ``default_gram_min_aspect(precision)`` (1.4 in both 16-bit precisions).  ``abc`` is
     one (a, b, c) for every NS step or a list with one triple per step (the
     per-step coefficient sets of Sec. 4); a list sets max_ns_steps to its
     length.  ``autotune`` picks each shape's GEMM tile by measurement on
