@@ -111,7 +111,7 @@ typedef struct muon_plan_opts {
   int32_t small_m_threshold;         /* bf16 plans: min(rows,cols) <= this -> fp32 NS */
   uint32_t flags;                    /* MUON_PLAN_* */
   int64_t wave_bytes;                /* cap on the NS working set of one group ("wave")
-                                        of matrices processed together; 0 = default */
+                                        of matrices processed together; 0 = default (12 GiB) */
   float gram_min_aspect;             /* 16-bit NS matrices with m >= 256 and n >= gram_min_aspect * m
                                         run the Gram-space recurrence (Eq. 4); 0 = never.  Must be 0
                                         or >= 1; ignored when c = 0 at some step.  Default 1.4: from there
@@ -298,7 +298,9 @@ MUON_API muon_status muon_step_debug(muon_plan plan, void* const* params, const 
                             float* const* update_out);
 
 /* Launch timing.  While enabled, muon_step records a pair of HIP events on
- * its stream around every kernel launch (a few microseconds per launch).
+ * its stream around every launch (a few microseconds per launch; a B*X
+ * launch and the launch of its matrices' edge strips on 128 tiles, which
+ * follows it, are one record).
  * muon_plan_timing_read waits for the recorded events, and aggregates the
  * launches by (kind, kernel class) into stats[0..capacity), setting *count
  * to the number of entries; with reset != 0 the records are dropped
