@@ -115,22 +115,22 @@ def test_gram_space_step_counts(ns_steps):
         assert r.o_rel <= max(TOL_O["bf16"], 1.25 * q.o_rel), (r.index, r.o_rel, q.o_rel)
 
 
-@pytest.mark.parametrize("restart", [1, 3, 5])
-def test_gram_space_restart_periods(restart):
+@pytest.mark.parametrize("precision,restart", [("bf16", 1), ("bf16", 3), ("bf16", 5), ("fp16", 1), ("fp16", 3)])
+def test_gram_space_restart_periods(precision, restart):
     # Segments of one or two steps keep R in B's buffer and Q1 in A's (the
     # default of 2 runs in every other Gram-space test); longer segments keep
     # all five square buffers.  Three steps per segment also run the paired
     # P Q | G P launch, and 5 (of k = 5) is the unrestarted recurrence, which
     # meets the bf16 bar on these well-conditioned Gaussian inputs.
     wl = custom_workload([(256, 1024), (1536, 512), (384, 1408), (200, 900)], seed=23)
-    plan = MuonPlan([(m.rows, m.cols, m.param, m.grad) for m in wl.matrices], gram_min_aspect=1.4,
-                    gram_restart=restart)
+    plan = MuonPlan([(m.rows, m.cols, m.param, m.grad) for m in wl.matrices], precision=precision,
+                    gram_min_aspect=1.4, gram_restart=restart)
     info = plan.info()
     assert info["gram_restart"] == restart and info["n_gram"] == 3
-    res = run_parity(wl, precision="bf16", steps=2, plan=plan)
+    res = run_parity(wl, precision=precision, steps=2, plan=plan)
     plan.close()
-    _banner(f"gram-space restart {restart}: {res.summary()}")
-    assert_parity(res, "bf16", f"gram-space restart {restart}")
+    _banner(f"gram-space {precision} restart {restart}: {res.summary()}")
+    assert_parity(res, precision, f"gram-space {precision} restart {restart}")
 
 
 @pytest.mark.parametrize("precision", ["bf16", "fp16"])
