@@ -19,7 +19,12 @@ LIB_NAME = "libmuon_mi355x.so"
 LIB_PATH = os.path.join(PKG, LIB_NAME)
 ARCH = "gfx950"
 
-SOURCES = ["api.cpp", "plan.cpp", "ew_kernels.hip", "ns_gemm.hip", "static_ws.hip"]
+# the GEMM kernels are instantiated in several translation units (the 256
+# tile's B*X and square-output kernels per operand type, the smaller tiles)
+# so that they compile in parallel
+SOURCES = ["api.cpp", "plan.cpp", "ew_kernels.hip", "ns_gemm.hip", "ns_gemm_t256_bf16_bx.hip",
+           "ns_gemm_t256_bf16_sq.hip", "ns_gemm_t256_f16_bx.hip", "ns_gemm_t256_f16_sq.hip", "ns_gemm_small.hip",
+           "static_ws.hip"]
 DIAG_SOURCES = ["diag/mfma_ceiling.hip"]
 DIAG_LIB_PATH = os.path.join(PKG, "libmuon_diag.so")
 
@@ -66,7 +71,7 @@ def _link(objs, path: str, verbose: bool) -> None:
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     srcs = SOURCES + DIAG_SOURCES
-    with cf.ThreadPoolExecutor(max_workers=4) as ex:
+    with cf.ThreadPoolExecutor(max_workers=min(8, os.cpu_count() or 4)) as ex:
         objs = list(ex.map(lambda s: _compile(s, verbose), srcs))
     _link(objs[:len(SOURCES)], LIB_PATH, verbose)
     _link(objs[len(SOURCES):], DIAG_LIB_PATH, verbose)

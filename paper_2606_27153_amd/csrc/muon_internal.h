@@ -78,7 +78,7 @@ struct TileEntry {
 // A 256 tile of a square (m x m) output of which only the top 128 rows
 // exist: the row strip of a matrix whose m ends 128 or fewer past a multiple
 // of 256.  Its operand panels hold 128 real rows (the padded extent ends
-// there) and its 8 waves share those rows, 64 each (see ns_gemm.hip).
+// there) and its 8 waves share those rows, 64 each (see ns_gemm_kernel.h).
 constexpr int32_t kTileHalf = 1;
 
 // Per-matrix device pointers, refreshed when the caller's buffers change.
@@ -228,7 +228,7 @@ int launch_momentum(const Plan& p, const WaveHost& w, char* ws, const StepScalar
 int launch_finalize(const Plan& p, const WaveHost& w, char* ws, const StepScalars& s, void* stream);
 int launch_apply(const Plan& p, const WaveHost& w, char* ws, const StepScalars& s, void* stream);
 
-// ns_gemm.hip.  Stages (lower tiles, mirrored, unless noted):
+// ns_gemm.hip (kernels in ns_gemm_kernel.h).  Stages (lower tiles, mirrored, unless noted):
 //   ST_GRAM  sq[out] = oscale * s^2 * X X^T            (X = x[pin])
 //   ST_POLY  sq[out] = oscale * (L L + fcoef * L + diag * I),  L = sq[l]
 //   ST_BX    X' or O = s * (sq[l] X + fcoef * X)        (all tiles)
